@@ -1,0 +1,217 @@
+"""CPU oracle for the EC2MoE hot path: the group-gated MoE layer forward and the
+low-rank encoder/decoder at the end-cloud cut.
+
+TEST INFRASTRUCTURE, NOT PRODUCT CODE. Only the test suite, the smoke check and
+the benchmark's CPU-baseline leg may import or run this module. The HIP library
+never calls it, and it shares no code with the HIP library: it reads plain NumPy
+arrays (the exact values of the inputs, upcast to float64) and computes every step
+in float64 with no blocking, fusion or reordering beyond what the definitions say.
+
+Sources (EC2MoE, arXiv 2508.06024):
+  * Mixture-of-Experts, Eq. (1): y = sum_i G(x)_i E_i(x) with sum_i G(x)_i = 1.
+  * Local Expert Selection, Eq. (4): the candidate set E_local; here a bitmask.
+  * Lightweight Group Gate Network, Eq. (5): per-group softmax gate over the
+    group's M_k experts; Eq. (6): the global softmax over the K groups
+    (stage 1); Eq. (7): the fused probability g_i = p_group^(k) * p_local,i^(k).
+  * Encoder-Decoder based on Low-Rank Compression: Z = U^T X V at the end,
+    X_hat = U_hat Z V_hat^T in the cloud.
+  * Parameter Selection: top-1 routing in the paper's runs; top-k in general.
+
+Readings where the paper is silent (each is also listed with the design notes):
+  * the candidate filter acts before both softmaxes: non-candidates get no
+    probability and a group without candidates drops out of the group softmax;
+  * experts are grouped contiguously: group k holds experts [k*M/K, (k+1)*M/K);
+  * top-k orders by descending g, exact ties going to the lower expert index;
+    the selected weights are renormalised to sum to 1 (Eq. (1)'s constraint
+    applied to the sparse gate) unless renormalize=False;
+  * the expert network is a SwiGLU feed-forward layer without biases:
+    E(x) = W_down (silu(W_gate x) * (W_up x)), silu(z) = z / (1 + exp(-z));
+  * tokens are permuted into per-expert segments by a stable sort on the expert
+    id of each (token, slot) assignment a = t*k + j;
+  * the codec acts on the [T][d] block of hidden states (h = tokens, w = model
+    width, one slice), and U_hat, V_hat are inputs of their own.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+class TooFewCandidates(ValueError):
+    """The candidate set holds fewer experts than the top-k asks for."""
+
+
+# ----------------------------------------------------------------------------- Eq. (4)
+
+def candidate_set(mask_words, n_experts):
+    """Experts whose bit is set in the candidate mask (bit e of word e // 64)."""
+    return [e for e in range(n_experts) if (int(mask_words[e // 64]) >> (e % 64)) & 1]
+
+
+def expert_groups(n_experts, n_groups):
+    """Contiguous equal groups: group k = experts [k*M/K, (k+1)*M/K)."""
+    if n_experts % n_groups:
+        raise ValueError("the number of groups must divide the number of experts")
+    size = n_experts // n_groups
+    return [list(range(k * size, (k + 1) * size)) for k in range(n_groups)]
+
+
+def softmax(v):
+    """Softmax of a 1-D float64 vector."""
+    v = np.asarray(v, dtype=np.float64)
+    e = np.exp(v - v.max())
+    return e / e.sum()
+
+
+# ----------------------------------------------------------------------------- Eq. (5)-(7)
+
+def group_gate_probs(x, w_global, b_global, w_local, b_local, mask_words, n_groups):
+    """Fused expert distribution g [T][M] of the lightweight group gate.
+
+    Stage 1 (Eq. 6): p_group = Softmax(W_global x + b_global) over the groups that
+    hold at least one candidate. Stage 2 (Eq. 5): inside group k,
+    p_local^(k) = Softmax(W_k x + b_k) over the group's candidates. Fusion (Eq. 7):
+    g_i = p_group^(k) * p_local,i^(k). Non-candidates get g = 0.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    T = x.shape[0]
+    M = w_local.shape[0]
+    local_logits = x @ np.asarray(w_local, np.float64).T + np.asarray(b_local, np.float64)
+    group_logits = x @ np.asarray(w_global, np.float64).T + np.asarray(b_global, np.float64)
+    cand = set(candidate_set(mask_words, M))
+    groups = expert_groups(M, n_groups)
+    cand_in_group = [[i for i in grp if i in cand] for grp in groups]
+    active = [k for k in range(n_groups) if cand_in_group[k]]
+
+    g = np.zeros((T, M), dtype=np.float64)
+    for t in range(T):
+        p_group = softmax(group_logits[t, active])
+        for a, k in enumerate(active):
+            members = cand_in_group[k]
+            p_local = softmax(local_logits[t, members])
+            for i, p in zip(members, p_local):
+                g[t, i] = p_group[a] * p
+    return g
+
+
+def topk_select(g_row, cand, k):
+    """The k candidates with the largest g, in descending order; ties -> lower index."""
+    cand = sorted(cand)
+    if len(cand) < k:
+        raise TooFewCandidates(f"{len(cand)} candidates for top-{k}")
+    order = sorted(cand, key=lambda i: (-g_row[i], i))
+    return order[:k]
+
+
+def group_gate(x, w_global, b_global, w_local, b_local, mask_words, n_groups, top_k,
+               renormalize=True):
+    """Routing of every token: (idx int32 [T][k], w float64 [T][k], g float64 [T][M]).
+
+    w holds g of the selected experts, divided by their sum when renormalize is set.
+    """
+    M = w_local.shape[0]
+    cand = candidate_set(mask_words, M)
+    if len(cand) < top_k:
+        raise TooFewCandidates(f"{len(cand)} candidates for top-{top_k}")
+    g = group_gate_probs(x, w_global, b_global, w_local, b_local, mask_words, n_groups)
+    T = g.shape[0]
+    idx = np.zeros((T, top_k), dtype=np.int32)
+    w = np.zeros((T, top_k), dtype=np.float64)
+    for t in range(T):
+        sel = topk_select(g[t], cand, top_k)
+        idx[t] = sel
+        w[t] = g[t, sel]
+        if renormalize:
+            w[t] = w[t] / w[t].sum()
+    return idx, w, g
+
+
+# ----------------------------------------------------------------------------- dispatch
+
+def permute(idx, n_experts):
+    """Per-expert segments of the (token, slot) assignments a = t*k + j.
+
+    Returns seg_offsets [M+1] (segment e = positions [seg[e], seg[e+1])),
+    perm_src [T*k] (token of each position) and inv_perm [T*k] (position of each
+    assignment). Within a segment the assignments keep ascending order.
+    """
+    idx = np.asarray(idx)
+    k = idx.shape[1]
+    flat = idx.reshape(-1).astype(np.int64)
+    order = np.argsort(flat, kind="stable")
+    seg = np.zeros(n_experts + 1, dtype=np.int64)
+    seg[1:] = np.cumsum(np.bincount(flat, minlength=n_experts))
+    perm_src = (order // k).astype(np.int32)
+    inv_perm = np.empty(flat.size, dtype=np.int32)
+    inv_perm[order] = np.arange(flat.size, dtype=np.int32)
+    return seg.astype(np.int32), perm_src, inv_perm
+
+
+# ----------------------------------------------------------------------------- experts, Eq. (1)
+
+def silu(z):
+    return z / (1.0 + np.exp(-z))
+
+
+def swiglu_expert(x_rows, w_gate_up_e, w_down_e):
+    """E(x) = W_down (silu(W_gate x) * (W_up x)) for a block of rows."""
+    H = w_down_e.shape[1]
+    h = np.asarray(x_rows, np.float64) @ np.asarray(w_gate_up_e, np.float64).T
+    act = silu(h[:, :H]) * h[:, H:]
+    return act @ np.asarray(w_down_e, np.float64).T
+
+
+def expert_outputs(x, idx, w_gate_up, w_down):
+    """Y_perm [T*k][d]: every assignment's expert output, in segment order.
+    w_gate_up[e] / w_down[e] may be any per-expert indexable of 2-D arrays."""
+    M = len(w_gate_up)
+    seg, perm_src, inv_perm = permute(idx, M)
+    x = np.asarray(x, np.float64)
+    d = x.shape[1]
+    y_perm = np.zeros((perm_src.size, d), dtype=np.float64)
+    for e in range(M):
+        lo, hi = int(seg[e]), int(seg[e + 1])
+        if hi > lo:
+            y_perm[lo:hi] = swiglu_expert(x[perm_src[lo:hi]], w_gate_up[e], w_down[e])
+    return y_perm, seg, perm_src, inv_perm
+
+
+def combine(y_perm, inv_perm, w):
+    """Eq. (1): y[t] = sum_j w[t, j] * E_{idx[t,j]}(x_t), summed over slots j in order."""
+    w = np.asarray(w, np.float64)
+    T, k = w.shape
+    y = np.zeros((T, y_perm.shape[1]), dtype=np.float64)
+    for j in range(k):
+        y += w[:, j:j + 1] * y_perm[inv_perm.reshape(T, k)[:, j]]
+    return y
+
+
+def moe_forward(x, idx, w, w_gate_up, w_down):
+    """The sparse MoE output y [T][d] for given routing (idx, w)."""
+    y_perm, _, _, inv_perm = expert_outputs(x, idx, w_gate_up, w_down)
+    return combine(y_perm, inv_perm, w)
+
+
+# ----------------------------------------------------------------------------- codec
+
+def lowrank_encode(x, u, v):
+    """Z = U^T X V."""
+    return np.asarray(u, np.float64).T @ np.asarray(x, np.float64) @ np.asarray(v, np.float64)
+
+
+def lowrank_decode(z, u_hat, v_hat):
+    """X_hat = U_hat Z V_hat^T."""
+    return np.asarray(u_hat, np.float64) @ np.asarray(z, np.float64) @ np.asarray(v_hat, np.float64).T
+
+
+# ----------------------------------------------------------------------------- the layer
+
+def layer(x, mask_words, w_global, b_global, w_local, b_local, w_gate_up, w_down,
+          u, v, u_hat, v_hat, n_groups, top_k, renormalize=True):
+    """Routing is taken on the end side from X; the experts run in the cloud on the
+    reconstruction X_hat = decode(encode(X)). Returns a dict of every stage output."""
+    idx, w, g = group_gate(x, w_global, b_global, w_local, b_local, mask_words,
+                           n_groups, top_k, renormalize)
+    z = lowrank_encode(x, u, v)
+    x_hat = lowrank_decode(z, u_hat, v_hat)
+    y = moe_forward(x_hat, idx, w, w_gate_up, w_down)
+    return {"idx": idx, "w": w, "g": g, "z": z, "x_hat": x_hat, "y": y}

@@ -1,0 +1,369 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these compares the oracle with itself: each check is a hand-derived value
+(tests/golden), a special case that reduces to a library routine, brute force on
+tiny inputs, or an identity that a dropped term, a wrong sign or index, or a
+transposed operand would break.
+"""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle as O
+from paper_2508_06024_amd import workload as W
+from tests._expr import value
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand_gate(rng, T, d, M, K, scale=1.0):
+    x = rng.standard_normal((T, d))
+    wl = rng.standard_normal((M, d)) * scale / np.sqrt(d)
+    bl = rng.standard_normal(M) * 0.3
+    wg = rng.standard_normal((K, d)) * scale / np.sqrt(d)
+    bg = rng.standard_normal(K) * 0.3
+    return x, wg, bg, wl, bl
+
+
+def _random_mask(rng, M, n_keep):
+    keep = rng.choice(M, n_keep, replace=False)
+    return W.mask_words(sorted(keep), M), sorted(int(e) for e in keep)
+
+
+# ----------------------------------------------------------------------------- gate, Eq. (4)-(7)
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("case", _load("gate_hand.json")["cases"], ids=lambda c: c["name"])
+def test_gate_hand_examples(case):
+    ev = lambda a: np.array([[value(e) for e in row] for row in a]) if isinstance(a[0], list) \
+        else np.array([value(e) for e in a])
+    x, wl, bl, wg, bg = (ev(case[k]) for k in ("x", "w_local", "b_local", "w_global", "b_global"))
+    M = wl.shape[0]
+    mask = W.mask_words(case["candidates"], M)
+    renorm = case.get("renormalize", True)
+    idx, w, g = O.group_gate(x, wg, bg, wl, bl, mask, case["n_groups"], case["top_k"], renorm)
+    np.testing.assert_allclose(g[0], [value(e) for e in case["g"]], rtol=0, atol=1e-14)
+    assert idx[0].tolist() == case["idx"]
+    np.testing.assert_allclose(w[0], [value(e) for e in case["w"]], rtol=0, atol=1e-14)
+
+
+def test_gate_single_group_is_plain_softmax_gate():
+    """K = 1: the fused gate is the traditional single-layer softmax gate over the
+    candidates (scipy's softmax)."""
+    rng = np.random.default_rng(10)
+    x, wg, bg, wl, bl = _rand_gate(rng, 32, 24, 8, 1)
+    mask, cand = _random_mask(rng, 8, 5)
+    g = O.group_gate_probs(x, wg, bg, wl, bl, mask, 1)
+    ref = scipy.special.softmax((x @ wl.T + bl)[:, cand], axis=1)
+    np.testing.assert_allclose(g[:, cand], ref, rtol=1e-13, atol=1e-15)
+    assert np.all(g[:, [e for e in range(8) if e not in cand]] == 0)
+
+
+def test_gate_one_expert_per_group_is_global_softmax():
+    """K = M: every in-group softmax is over one expert, so g is the global softmax over
+    the candidate groups."""
+    rng = np.random.default_rng(11)
+    x, wg, bg, wl, bl = _rand_gate(rng, 32, 24, 8, 8)
+    mask, cand = _random_mask(rng, 8, 6)
+    g = O.group_gate_probs(x, wg, bg, wl, bl, mask, 8)
+    ref = scipy.special.softmax((x @ wg.T + bg)[:, cand], axis=1)
+    np.testing.assert_allclose(g[:, cand], ref, rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("M,K,keep", [(8, 2, 6), (16, 4, 12), (64, 8, 48), (64, 8, 16), (12, 3, 5)])
+def test_gate_distribution_sums_to_one_over_candidates(M, K, keep):
+    rng = np.random.default_rng(M * 100 + keep)
+    x, wg, bg, wl, bl = _rand_gate(rng, 40, 32, M, K, scale=3.0)
+    mask, cand = _random_mask(rng, M, keep)
+    g = O.group_gate_probs(x, wg, bg, wl, bl, mask, K)
+    np.testing.assert_allclose(g.sum(axis=1), 1.0, rtol=0, atol=1e-13)
+    non = [e for e in range(M) if e not in cand]
+    assert np.all(g[:, non] == 0)
+    assert np.all(g[:, cand] > 0)
+
+
+def test_gate_zero_weights_reproduce_zipf_popularity():
+    """With zero gate weights and biases b_global,k = log(sum of z over group k),
+    b_local,i = log z_i - log(sum of z over i's group), Eq. (5)-(7) give g = z."""
+    cfg = W.CONFIGS["finegrained"]
+    z = W.zipf_popularity(cfg, cfg.seed)
+    M, K, Mk = cfg.n_experts, cfg.n_groups, cfg.group_size
+    zg = z.reshape(K, Mk).sum(axis=1)
+    bg = np.log(zg)
+    bl = np.log(z) - np.repeat(np.log(zg), Mk)
+    d = 16
+    x = np.random.default_rng(0).standard_normal((5, d))
+    g = O.group_gate_probs(x, np.zeros((K, d)), bg, np.zeros((M, d)), bl,
+                           W.mask_words(range(M), M), K)
+    np.testing.assert_allclose(g, np.broadcast_to(z, g.shape), rtol=1e-12, atol=0)
+    # Zipf(1.1) over 64 experts: the most popular expert carries about a quarter
+    assert abs(z.max() - 0.2497) < 1e-3
+
+
+def test_gate_scale_invariance_of_in_group_softmax():
+    """Adding a constant to every local logit of one group leaves g unchanged, while
+    adding it to a group logit moves mass between groups: pins which logits enter
+    which softmax."""
+    rng = np.random.default_rng(12)
+    x, wg, bg, wl, bl = _rand_gate(rng, 8, 10, 8, 2)
+    mask = W.mask_words(range(8), 8)
+    g0 = O.group_gate_probs(x, wg, bg, wl, bl, mask, 2)
+    bl2 = bl.copy()
+    bl2[4:] += 5.0
+    np.testing.assert_allclose(O.group_gate_probs(x, wg, bg, wl, bl2, mask, 2), g0, rtol=1e-12)
+    bg2 = bg.copy()
+    bg2[1] += np.log(3.0)
+    g2 = O.group_gate_probs(x, wg, bg2, wl, bl, mask, 2)
+    # odds of group 1 vs group 0 multiply by exactly 3
+    r0 = g0[:, 4:].sum(1) / g0[:, :4].sum(1)
+    r2 = g2[:, 4:].sum(1) / g2[:, :4].sum(1)
+    np.testing.assert_allclose(r2 / r0, 3.0, rtol=1e-12)
+
+
+# ----------------------------------------------------------------------------- top-k
+
+def _brute_topk(g_row, cand, k):
+    """Exhaustive search over all k-subsets of the candidates: largest sum of g, ties to
+    the lexicographically smallest index tuple; then order by (-g, index)."""
+    best, best_key = None, None
+    for sub in itertools.combinations(sorted(cand), k):
+        key = (-sum(g_row[i] for i in sub), sub)
+        if best_key is None or key < best_key:
+            best, best_key = sub, key
+    return sorted(best, key=lambda i: (-g_row[i], i))
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_topk_matches_exhaustive_search(seed):
+    rng = np.random.default_rng(seed)
+    M = int(rng.integers(2, 9))
+    k = int(rng.integers(1, M + 1))
+    keep = int(rng.integers(k, M + 1))
+    cand = sorted(rng.choice(M, keep, replace=False).tolist())
+    # coarse values make exact ties common
+    g = rng.integers(0, 4, M).astype(np.float64) / 4.0
+    assert O.topk_select(g, cand, k) == _brute_topk(g, cand, k)
+    # counting rule: i is selected iff fewer than k candidates beat it
+    sel = set(O.topk_select(g, cand, k))
+    for i in cand:
+        beat = sum(1 for j in cand if g[j] > g[i] or (g[j] == g[i] and j < i))
+        assert (i in sel) == (beat < k)
+
+
+def test_topk_never_selects_a_non_candidate():
+    rng = np.random.default_rng(3)
+    for _ in range(50):
+        M = 16
+        mask, cand = _random_mask(rng, M, 5)
+        x, wg, bg, wl, bl = _rand_gate(rng, 6, 8, M, 4, scale=4.0)
+        idx, _, _ = O.group_gate(x, wg, bg, wl, bl, mask, 4, 3)
+        assert set(idx.ravel().tolist()) <= set(cand)
+
+
+def test_topk_too_few_candidates_is_an_error():
+    rng = np.random.default_rng(4)
+    x, wg, bg, wl, bl = _rand_gate(rng, 2, 8, 8, 2)
+    with pytest.raises(O.TooFewCandidates):
+        O.group_gate(x, wg, bg, wl, bl, W.mask_words([1], 8), 2, 2)
+
+
+def test_renormalised_weights():
+    rng = np.random.default_rng(5)
+    x, wg, bg, wl, bl = _rand_gate(rng, 64, 16, 16, 4, scale=2.0)
+    mask = W.mask_words(range(16), 16)
+    _, w, g = O.group_gate(x, wg, bg, wl, bl, mask, 4, 3)
+    np.testing.assert_allclose(w.sum(1), 1.0, rtol=0, atol=4e-16)
+    assert np.all(w[:, :-1] >= w[:, 1:])
+    _, w1, _ = O.group_gate(x, wg, bg, wl, bl, mask, 4, 1)
+    assert np.all(w1 == 1.0)
+    idx_raw, w_raw, _ = O.group_gate(x, wg, bg, wl, bl, mask, 4, 3, renormalize=False)
+    np.testing.assert_array_equal(w_raw, np.take_along_axis(g, idx_raw.astype(np.int64), 1))
+
+
+# ----------------------------------------------------------------------------- permutation
+
+def _brute_segments(idx, M):
+    """Scan experts in order and, for each, the assignments in order."""
+    flat = [int(e) for e in np.asarray(idx).ravel()]
+    k = np.asarray(idx).shape[1]
+    seg, perm_src, inv = [0], [], [0] * len(flat)
+    for e in range(M):
+        for a, ea in enumerate(flat):
+            if ea == e:
+                inv[a] = len(perm_src)
+                perm_src.append(a // k)
+        seg.append(len(perm_src))
+    return seg, perm_src, inv
+
+
+@pytest.mark.parametrize("T,M,k,keep,skew", [(37, 8, 2, 6, 0.0), (100, 16, 3, 12, 1.1),
+                                              (64, 64, 6, 48, 1.1), (5, 4, 4, 4, 0.0),
+                                              (1, 8, 1, 3, 0.0)])
+def test_permutation_matches_brute_force(T, M, k, keep, skew):
+    rng = np.random.default_rng(T + M)
+    cand = sorted(rng.choice(M, keep, replace=False).tolist())
+    idx, _ = W.gen_routing(T, M, k, cand, seed=T * M, skew=skew)
+    seg, perm_src, inv = O.permute(idx, M)
+    bseg, bsrc, binv = _brute_segments(idx, M)
+    assert seg.tolist() == bseg
+    assert perm_src.tolist() == bsrc
+    assert inv.tolist() == binv
+    assert seg[-1] == T * k
+    for e in range(M):
+        if e not in cand:
+            assert seg[e] == seg[e + 1]
+
+
+# ----------------------------------------------------------------------------- experts, Eq. (1)
+
+def test_silu_pins():
+    z = np.linspace(-30, 30, 301)
+    # silu(z) - silu(-z) = z(sigma(z) + sigma(-z)) = z
+    np.testing.assert_allclose(O.silu(z) - O.silu(-z), z, rtol=0, atol=1e-12)
+    assert O.silu(np.array(0.0)) == 0.0
+    np.testing.assert_allclose(O.silu(z), torch.nn.functional.silu(torch.tensor(z)).numpy(),
+                               rtol=1e-14, atol=1e-300)
+
+
+def test_swiglu_gate_and_up_order():
+    c = _load("swiglu_hand.json")
+    y = O.swiglu_expert(np.array(c["x"]), np.array(c["w_gate_up"][0]), np.array(c["w_down"][0]))
+    np.testing.assert_allclose(y[0, 0], value(c["y"]), rtol=1e-14)
+
+
+def _torch_dense_swiglu(x, wgu, wd):
+    H = wd.shape[1]
+    xt, g, u, dn = (torch.tensor(a, dtype=torch.float64) for a in (x, wgu[:H], wgu[H:], wd))
+    f = torch.nn.functional
+    return f.linear(f.silu(f.linear(xt, g)) * f.linear(xt, u), dn).numpy()
+
+
+def test_one_expert_moe_is_dense_ffn():
+    rng = np.random.default_rng(6)
+    T, d, H = 23, 16, 40
+    x = rng.standard_normal((T, d))
+    wgu = rng.standard_normal((1, 2 * H, d)) * 0.3
+    wd = rng.standard_normal((1, d, H)) * 0.3
+    wg, bg, wl, bl = np.zeros((1, d)), np.zeros(1), rng.standard_normal((1, d)), np.zeros(1)
+    idx, w, _ = O.group_gate(x, wg, bg, wl, bl, [1], 1, 1)
+    assert np.all(idx == 0) and np.all(w == 1.0)
+    y = O.moe_forward(x, idx, w, wgu, wd)
+    np.testing.assert_allclose(y, _torch_dense_swiglu(x, wgu[0], wd[0]), rtol=1e-12, atol=1e-12)
+
+
+def test_identical_experts_equal_dense_ffn_for_any_routing():
+    rng = np.random.default_rng(7)
+    T, d, H, M, k = 31, 12, 20, 8, 3
+    x = rng.standard_normal((T, d))
+    one_gu = rng.standard_normal((2 * H, d)) * 0.3
+    one_dn = rng.standard_normal((d, H)) * 0.3
+    wgu = np.stack([one_gu] * M)
+    wd = np.stack([one_dn] * M)
+    idx, w = W.gen_routing(T, M, k, range(M), seed=1, skew=1.1)
+    w = w.astype(np.float64)
+    w /= w.sum(1, keepdims=True)
+    y = O.moe_forward(x, idx, w, wgu, wd)
+    np.testing.assert_allclose(y, _torch_dense_swiglu(x, one_gu, one_dn), rtol=1e-12, atol=1e-12)
+
+
+def test_combine_matches_per_token_sum():
+    """Permutation + expert segments + combine against the definition token by token."""
+    rng = np.random.default_rng(8)
+    T, d, H, M, k = 29, 8, 12, 6, 2
+    x = rng.standard_normal((T, d))
+    wgu = rng.standard_normal((M, 2 * H, d)) * 0.4
+    wd = rng.standard_normal((M, d, H)) * 0.4
+    idx, w = W.gen_routing(T, M, k, [0, 1, 3, 4, 5], seed=2)
+    y = O.moe_forward(x, idx, w, wgu, wd)
+    for t in range(T):
+        ref = sum(float(w[t, j]) * _torch_dense_swiglu(x[t:t + 1], wgu[idx[t, j]], wd[idx[t, j]])[0]
+                  for j in range(k))
+        np.testing.assert_allclose(y[t], ref, rtol=1e-12, atol=1e-12)
+
+
+def test_top1_combine_is_a_gather_and_zero_rows_stay_zero():
+    rng = np.random.default_rng(9)
+    T, d, H, M = 16, 8, 10, 4
+    x = rng.standard_normal((T, d))
+    x[3] = 0.0
+    wgu = rng.standard_normal((M, 2 * H, d))
+    wd = rng.standard_normal((M, d, H))
+    idx, _ = W.gen_routing(T, M, 1, range(M), seed=3)
+    w = np.ones((T, 1))
+    y_perm, seg, perm_src, inv = O.expert_outputs(x, idx, wgu, wd)
+    y = O.combine(y_perm, inv, w)
+    np.testing.assert_array_equal(y, y_perm[inv])
+    assert np.all(y[3] == 0.0)
+
+
+# ----------------------------------------------------------------------------- codec
+
+def test_codec_full_rank_round_trip():
+    """A rank-d orthonormal codec (U, V square orthogonal) reconstructs X exactly
+    (up to rounding): the tiny workload's shape, T=64 tokens, d=128."""
+    cfg = W.CONFIGS["tiny"]
+    x = W.to_f64(W.gen_call(cfg)[0], cfg.dtype)
+    u = W.haar_orthonormal(5, (1,), cfg.n_tokens, cfg.n_tokens)
+    v = W.haar_orthonormal(5, (2,), cfg.d_model, cfg.d_model)
+    z = O.lowrank_encode(x, u, v)
+    xh = O.lowrank_decode(z, u, v)
+    np.testing.assert_allclose(xh, x, rtol=0, atol=1e-14)
+
+
+def test_codec_projection_identities():
+    rng = np.random.default_rng(13)
+    T, d, rh, rw = 48, 80, 12, 20
+    x = rng.standard_normal((T, d))
+    u = W.haar_orthonormal(1, (1,), T, rh)
+    v = W.haar_orthonormal(1, (2,), d, rw)
+    z = O.lowrank_encode(x, u, v)
+    assert z.shape == (rh, rw)
+    xh = O.lowrank_decode(z, u, v)
+    # decode(encode(.)) is the orthogonal projection P_U X P_V: idempotent
+    np.testing.assert_allclose(O.lowrank_decode(O.lowrank_encode(xh, u, v), u, v), xh, atol=1e-12)
+    # Pythagoras: ||Z|| = ||X_hat|| and ||X||^2 = ||X_hat||^2 + ||X - X_hat||^2
+    np.testing.assert_allclose(np.linalg.norm(z), np.linalg.norm(xh), rtol=1e-12)
+    np.testing.assert_allclose(np.sum(x * x), np.sum(xh * xh) + np.sum((x - xh) ** 2), rtol=1e-12)
+    # U = I reduces to the one-sided product X V
+    zi = O.lowrank_encode(x, np.eye(T), v)
+    np.testing.assert_allclose(zi, x @ v, rtol=1e-13, atol=1e-13)
+
+
+def test_codec_eckart_young():
+    """With U, V the top singular vectors of X, the codec error is the tail of the
+    singular values (numpy's SVD)."""
+    rng = np.random.default_rng(14)
+    T, d, r = 40, 70, 9
+    x = rng.standard_normal((T, d)) @ np.diag(np.linspace(3, 0.1, d))
+    uu, s, vt = np.linalg.svd(x, full_matrices=False)
+    z = O.lowrank_encode(x, uu[:, :r], vt[:r].T)
+    np.testing.assert_allclose(np.diag(z), s[:r], rtol=1e-12)
+    xh = O.lowrank_decode(z, uu[:, :r], vt[:r].T)
+    np.testing.assert_allclose(np.sum((x - xh) ** 2), np.sum(s[r:] ** 2), rtol=1e-10)
+
+
+# ----------------------------------------------------------------------------- layer
+
+def test_layer_routes_on_x_and_runs_experts_on_reconstruction():
+    cfg = W.CONFIGS["tiny"]
+    inp = W.gen_layer(cfg)
+    f = inp.f64
+    out = O.layer(f("x"), inp.mask, f("w_global"), inp.b_global, f("w_local"), inp.b_local,
+                  f("w_gate_up"), f("w_down"), f("u"), f("v"), f("u"), f("v"),
+                  cfg.n_groups, cfg.top_k)
+    idx, w, _ = O.group_gate(f("x"), f("w_global"), inp.b_global, f("w_local"), inp.b_local,
+                             inp.mask, cfg.n_groups, cfg.top_k)
+    np.testing.assert_array_equal(out["idx"], idx)
+    xh = f("u") @ (f("u").T @ f("x") @ f("v")) @ f("v").T
+    np.testing.assert_allclose(out["x_hat"], xh, atol=1e-14)
+    assert out["y"].shape == (cfg.n_tokens, cfg.d_model)
+    assert not set(out["idx"].ravel().tolist()) & set(cfg.masked_out)
