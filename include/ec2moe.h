@@ -1,0 +1,208 @@
+/*
+ * ec2moe.h - C ABI of the MI355X (gfx950) library for the data-parallel hot path of
+ * EC2MoE (arXiv 2508.06024): the group-gated Mixture-of-Experts layer forward and the
+ * low-rank encoder/decoder applied to hidden states at the end-cloud pipeline cut.
+ *
+ * Conventions for every call
+ *   - Tensor pointers are DEVICE pointers unless marked [host]. Tensors are dense and
+ *     row-major, 16-byte aligned. Element type: the descriptor's dtype (float32 or
+ *     bfloat16 bit patterns) unless the type says otherwise; biases, gate weights out,
+ *     codec Z and probabilities are always float32; indices are int32.
+ *   - The caller owns every buffer, including the workspace; the library keeps no
+ *     pointer after a call returns and allocates nothing on these paths. Host arrays
+ *     (descriptors, the candidate mask) are read during the call only. Outputs must
+ *     not alias inputs.
+ *   - Calls are stream-ordered and asynchronous on the given hipStream_t (0 = the null
+ *     stream); the library never synchronises. Results are deterministic: the same
+ *     inputs on the same GPU give bit-identical outputs.
+ *   - All validation happens on the host before any launch. On any error nothing is
+ *     launched and no output is written; ec2moe_last_error() returns the detail
+ *     (thread-local). No C++ exception crosses this interface.
+ *   - Supported shapes: d_model and ffn_hidden multiples of 128, 1 <= top_k <= 16,
+ *     n_experts <= 256, n_experts + n_groups <= 320, n_groups dividing n_experts;
+ *     codec ranks r_h, r_w multiples of 16 and at most 256, w a multiple of 128.
+ *     Others return EC2MOE_ERR_UNSUPPORTED. n_tokens == 0 is valid and launches nothing.
+ */
+#ifndef EC2MOE_H
+#define EC2MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { EC2MOE_F32 = 0, EC2MOE_BF16 = 1 } ec2moe_dtype;
+
+typedef enum {
+    EC2MOE_OK = 0,
+    EC2MOE_ERR_INVALID_ARGUMENT = 1,   /* null pointer, bad dimension, misalignment, bad mask bits */
+    EC2MOE_ERR_UNSUPPORTED = 2,        /* valid but outside the supported shapes listed above */
+    EC2MOE_ERR_TOO_FEW_CANDIDATES = 3, /* fewer candidate experts than top_k */
+    EC2MOE_ERR_WORKSPACE_TOO_SMALL = 4,
+    EC2MOE_ERR_HIP = 5                 /* a HIP launch or runtime call failed */
+} ec2moe_status;
+
+/* flags of ec2moe_moe_desc */
+#define EC2MOE_GATE_RENORMALIZE 1u /* selected gate weights are divided by their sum (Eq. 1:
+                                      the gate weights of a token sum to 1); else raw g */
+
+/* Shape of one MoE layer call: T tokens of width d, M experts in K contiguous equal
+ * groups (group k = experts [k*M/K, (k+1)*M/K)), SwiGLU hidden width H, top-k routing. */
+typedef struct {
+    int32_t n_tokens;   /* T */
+    int32_t n_experts;  /* M */
+    int32_t n_groups;   /* K */
+    int32_t d_model;    /* d */
+    int32_t ffn_hidden; /* H */
+    int32_t top_k;      /* k */
+    int32_t dtype;      /* ec2moe_dtype of x, gate weights, expert weights and y */
+    uint32_t flags;     /* EC2MOE_GATE_RENORMALIZE or 0 */
+} ec2moe_moe_desc;
+
+/* Shape of the codec: n_slices blocks X[c] of h x w (h = tokens, w = model width),
+ * projected to r_h x r_w. */
+typedef struct {
+    int32_t n_slices; /* c */
+    int32_t h;
+    int32_t w;
+    int32_t r_h;
+    int32_t r_w;
+    int32_t dtype;    /* ec2moe_dtype of x, x_hat and the projections */
+} ec2moe_codec_desc;
+
+/*
+ * Hardware-aware lightweight group gate (Local Expert Selection, Eq. 4; Lightweight
+ * Group Gate Network, Eq. 5-7) followed by top-k selection.
+ *   cand_mask [host] ceil(M/64) words: bit e of word e/64 set <=> expert e is in the
+ *             candidate set E_local. Bits at or above M must be clear.
+ *   x         [T][d]
+ *   w_global  [K][d], b_global [K] float32 or NULL (zero): stage-1 group gate, Eq. 6
+ *   w_local   [M][d], b_local  [M] float32 or NULL (zero): the K stacked group gates
+ *             W_k (rows k*M/K .. (k+1)*M/K - 1), Eq. 5
+ *   topk_idx  [T][k] int32 out: selected experts, descending fused probability
+ *             g_i = p_group^(k) * p_local,i^(k) (Eq. 7); exact ties -> lower index.
+ *   topk_w    [T][k] float32 out: g of the selected experts, renormalised to sum 1
+ *             when EC2MOE_GATE_RENORMALIZE is set.
+ *   probs     [T][M] float32 out or NULL: the full fused distribution g (0 for
+ *             non-candidates).
+ * Non-candidates get no probability; a group with no candidate leaves the group softmax.
+ * Errors: EC2MOE_ERR_TOO_FEW_CANDIDATES if popcount(mask) < k.
+ */
+ec2moe_status ec2moe_group_gate(const ec2moe_moe_desc* desc, const uint64_t* cand_mask,
+                                const void* x, const void* w_global, const float* b_global,
+                                const void* w_local, const float* b_local,
+                                int32_t* topk_idx, float* topk_w, float* probs,
+                                hipStream_t stream);
+
+/* Workspace bytes needed by ec2moe_permute, ec2moe_expert_ffn and ec2moe_moe_forward
+ * for this descriptor (a superset for all three). */
+ec2moe_status ec2moe_moe_workspace_size(const ec2moe_moe_desc* desc, size_t* bytes /*[host]*/);
+
+/*
+ * Dispatch of tokens to experts (the routing step between the gate and the expert
+ * networks of Eq. 1): assignments a = t*k + j are sorted stably by topk_idx.
+ *   topk_idx    [T][k] int32 in [0, M)
+ *   seg_offsets [M+1] int32 out: expert e owns positions [seg[e], seg[e+1])
+ *   perm_src    [T*k] int32 out: token of each position (ascending inside a segment)
+ *   inv_perm    [T*k] int32 out: position of each assignment
+ *   x, x_perm   [T][d] in, [T*k][d] out: gathered rows; both NULL to skip the gather
+ *   ws          workspace of ec2moe_moe_workspace_size bytes
+ */
+ec2moe_status ec2moe_permute(const ec2moe_moe_desc* desc, const int32_t* topk_idx,
+                             const void* x, int32_t* seg_offsets, int32_t* perm_src,
+                             int32_t* inv_perm, void* x_perm, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/*
+ * The expert networks E_i of Eq. 1 as SwiGLU feed-forward layers,
+ * E(x) = W_down (silu(W_gate x) * (W_up x)), on permuted rows:
+ *   y_perm[p] = E_e(x[perm_src[p]]) for every position p of segment e.
+ *   x [T][d]; seg_offsets [M+1], perm_src [T*k] as from ec2moe_permute;
+ *   w_gate_up [M][2H][d] (rows 0..H-1 gate branch, H..2H-1 up branch); w_down [M][d][H];
+ *   act [T*k][H] out or NULL: silu(gate) * up in the layer dtype;
+ *   y_perm [T*k][d] out.
+ * Intermediates are accumulated in float32 and rounded once to the layer dtype.
+ */
+ec2moe_status ec2moe_expert_ffn(const ec2moe_moe_desc* desc, const void* x,
+                                const int32_t* seg_offsets, const int32_t* perm_src,
+                                const void* w_gate_up, const void* w_down, void* act,
+                                void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Weighted combine, Eq. 1: y[t] = sum_{j<k} topk_w[t][j] * y_perm[inv_perm[t*k+j]],
+ * accumulated in float32 in slot order j = 0..k-1 and rounded once.
+ *   y_perm [T*k][d], inv_perm [T*k] int32, topk_w [T][k] float32, y [T][d] out.
+ */
+ec2moe_status ec2moe_combine(const ec2moe_moe_desc* desc, const void* y_perm,
+                             const int32_t* inv_perm, const float* topk_w, void* y,
+                             hipStream_t stream);
+
+/*
+ * Sparse MoE layer output, Eq. 1, for given routing: permute, expert networks,
+ * combine. y[t] = sum_j topk_w[t][j] * E_{topk_idx[t][j]}(x[t]).
+ *   x [T][d]; topk_idx [T][k] int32 in [0, M); topk_w [T][k] float32;
+ *   w_gate_up [M][2H][d]; w_down [M][d][H]; y [T][d] out; ws of
+ *   ec2moe_moe_workspace_size bytes.
+ * Routing may come from ec2moe_group_gate on other hidden states (the end-cloud split:
+ * route on X, run the experts on the reconstruction X_hat).
+ */
+ec2moe_status ec2moe_moe_forward(const ec2moe_moe_desc* desc, const void* x,
+                                 const int32_t* topk_idx, const float* topk_w,
+                                 const void* w_gate_up, const void* w_down, void* y,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes needed by ec2moe_lowrank_encode and ec2moe_lowrank_decode. */
+ec2moe_status ec2moe_lowrank_workspace_size(const ec2moe_codec_desc* desc,
+                                            size_t* bytes /*[host]*/);
+
+/*
+ * Low-rank encoder (Encoder-Decoder based on Low-Rank Compression): Z = U^T X V per slice.
+ *   x [c][h][w]; u [h][r_h]; v [w][r_w]; z [c][r_h][r_w] float32 out.
+ * X V is accumulated in float32 and kept in float32 for the product with U^T.
+ */
+ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x,
+                                    const void* u, const void* v, float* z, void* ws,
+                                    size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Low-rank decoder: X_hat = U_hat Z V_hat^T per slice, with the decoder's own
+ * ("inverse") projections.
+ *   z [c][r_h][r_w] float32; u_hat [h][r_h]; v_hat [w][r_w]; x_hat [c][h][w] out.
+ * The small product Z V_hat^T is accumulated in float32 and rounded to the layer dtype
+ * before the h x w product, which accumulates in float32.
+ */
+ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* z,
+                                    const void* u_hat, const void* v_hat, void* x_hat,
+                                    void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* ec2moe_status_string(ec2moe_status status);
+
+/* Detail of the last failing call on this thread ("" if none). */
+const char* ec2moe_last_error(void);
+
+/*
+ * Kernel timing. While enabled, every kernel the library launches is bracketed by two
+ * HIP events recorded on its launch stream. ec2moe_profile_collect waits for the
+ * recorded events, writes up to max_entries per-kernel totals (name, launches, total
+ * milliseconds) in first-launch order, sets *n_out, and clears the record.
+ */
+typedef struct {
+    char name[48];
+    int64_t launches;
+    double total_ms;
+} ec2moe_kernel_stat;
+
+ec2moe_status ec2moe_profile_enable(int32_t enable);
+ec2moe_status ec2moe_profile_collect(ec2moe_kernel_stat* out, int32_t max_entries,
+                                     int32_t* n_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EC2MOE_H */

@@ -1,0 +1,497 @@
+// C ABI of the EC2MoE hot path (declarations and contracts in include/ec2moe.h).
+//
+// Every entry point validates its arguments on the host first; on any error it returns
+// before the first HIP call, so nothing is launched and no output is written. The error
+// detail is kept per thread for ec2moe_last_error().
+#include "ec2moe.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace ec2moe {
+namespace {
+
+thread_local std::string g_last_error;
+
+ec2moe_status fail(ec2moe_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+ec2moe_status ok() {
+    g_last_error.clear();
+    return EC2MOE_OK;
+}
+
+ec2moe_status hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) return ok();
+    return fail(EC2MOE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define REQUIRE(cond, st, ...) \
+    do {                       \
+        if (!(cond)) return fail(st, __VA_ARGS__); \
+    } while (0)
+
+#define REQUIRE_PTR(p) REQUIRE((p) != nullptr, EC2MOE_ERR_INVALID_ARGUMENT, "%s is NULL", #p)
+#define REQUIRE_ALIGNED(p) REQUIRE(aligned16(p), EC2MOE_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", #p)
+
+constexpr int kMaxExperts = 256;
+constexpr int kMaxGateRows = 320;
+constexpr int kMaxTopK = 16;
+
+ec2moe_status check_moe_desc(const ec2moe_moe_desc* d) {
+    REQUIRE(d != nullptr, EC2MOE_ERR_INVALID_ARGUMENT, "desc is NULL");
+    REQUIRE(d->dtype == EC2MOE_F32 || d->dtype == EC2MOE_BF16, EC2MOE_ERR_INVALID_ARGUMENT, "unknown dtype %d",
+            d->dtype);
+    REQUIRE(d->n_tokens >= 0, EC2MOE_ERR_INVALID_ARGUMENT, "n_tokens %d < 0", d->n_tokens);
+    REQUIRE(d->n_experts > 0 && d->n_groups > 0 && d->d_model > 0 && d->ffn_hidden > 0 && d->top_k > 0,
+            EC2MOE_ERR_INVALID_ARGUMENT, "n_experts, n_groups, d_model, ffn_hidden and top_k must be positive");
+    REQUIRE(d->n_experts % d->n_groups == 0, EC2MOE_ERR_INVALID_ARGUMENT,
+            "n_groups %d does not divide n_experts %d", d->n_groups, d->n_experts);
+    REQUIRE(d->top_k <= d->n_experts, EC2MOE_ERR_INVALID_ARGUMENT, "top_k %d > n_experts %d", d->top_k,
+            d->n_experts);
+    REQUIRE((d->flags & ~EC2MOE_GATE_RENORMALIZE) == 0, EC2MOE_ERR_INVALID_ARGUMENT, "unknown flags 0x%x",
+            d->flags);
+    REQUIRE(d->n_experts <= kMaxExperts, EC2MOE_ERR_UNSUPPORTED, "n_experts %d > %d", d->n_experts, kMaxExperts);
+    REQUIRE(d->n_experts + d->n_groups <= kMaxGateRows, EC2MOE_ERR_UNSUPPORTED, "n_experts + n_groups > %d",
+            kMaxGateRows);
+    REQUIRE(d->top_k <= kMaxTopK, EC2MOE_ERR_UNSUPPORTED, "top_k %d > %d", d->top_k, kMaxTopK);
+    REQUIRE(d->d_model % 128 == 0, EC2MOE_ERR_UNSUPPORTED, "d_model %d is not a multiple of 128", d->d_model);
+    REQUIRE(d->ffn_hidden % 128 == 0, EC2MOE_ERR_UNSUPPORTED, "ffn_hidden %d is not a multiple of 128",
+            d->ffn_hidden);
+    // 32-bit element offsets inside one operand of the GEMM
+    const int64_t A = static_cast<int64_t>(d->n_tokens) * d->top_k;
+    REQUIRE(A * std::max(d->d_model, d->ffn_hidden) < (int64_t(1) << 32) &&
+                int64_t(2) * d->ffn_hidden * d->d_model < (int64_t(1) << 32),
+            EC2MOE_ERR_UNSUPPORTED, "tensor too large for 32-bit element offsets");
+    return EC2MOE_OK;
+}
+
+// ---------------------------------------------------------------- workspace carving
+constexpr size_t kAlign = 256;
+size_t up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+
+struct MoeWs {
+    size_t counts, seg, perm_src, inv_perm, act, y_perm, total;
+};
+
+MoeWs moe_ws(const ec2moe_moe_desc* d) {
+    const int64_t A = static_cast<int64_t>(d->n_tokens) * d->top_k;
+    const size_t eb = elem_bytes(static_cast<DType>(d->dtype));
+    MoeWs w{};
+    size_t o = 0;
+    w.counts = o; o += up(static_cast<size_t>(std::max(1, perm_chunks(A))) * d->n_experts * 4);
+    w.seg = o; o += up(static_cast<size_t>(d->n_experts + 1) * 4);
+    w.perm_src = o; o += up(static_cast<size_t>(A) * 4);
+    w.inv_perm = o; o += up(static_cast<size_t>(A) * 4);
+    w.act = o; o += up(static_cast<size_t>(A) * d->ffn_hidden * eb);
+    w.y_perm = o; o += up(static_cast<size_t>(A) * d->d_model * eb);
+    w.total = o;
+    return w;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+    return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+ec2moe_status check_ws(void* ws, size_t have, size_t need) {
+    REQUIRE(have >= need, EC2MOE_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, %zu needed", have, need);
+    REQUIRE(need == 0 || ws != nullptr, EC2MOE_ERR_INVALID_ARGUMENT, "ws is NULL");
+    REQUIRE(aligned16(ws), EC2MOE_ERR_INVALID_ARGUMENT, "ws is not 16-byte aligned");
+    return EC2MOE_OK;
+}
+
+// ---------------------------------------------------------------- codec plan
+ec2moe_status check_codec_desc(const ec2moe_codec_desc* d) {
+    REQUIRE(d != nullptr, EC2MOE_ERR_INVALID_ARGUMENT, "desc is NULL");
+    REQUIRE(d->dtype == EC2MOE_F32 || d->dtype == EC2MOE_BF16, EC2MOE_ERR_INVALID_ARGUMENT, "unknown dtype %d",
+            d->dtype);
+    REQUIRE(d->n_slices >= 0 && d->h >= 0, EC2MOE_ERR_INVALID_ARGUMENT, "n_slices and h must be >= 0");
+    REQUIRE(d->w > 0 && d->r_h > 0 && d->r_w > 0, EC2MOE_ERR_INVALID_ARGUMENT, "w, r_h and r_w must be positive");
+    REQUIRE(d->r_h <= d->h || d->h == 0, EC2MOE_ERR_INVALID_ARGUMENT, "r_h %d > h %d", d->r_h, d->h);
+    REQUIRE(d->r_w <= d->w, EC2MOE_ERR_INVALID_ARGUMENT, "r_w %d > w %d", d->r_w, d->w);
+    REQUIRE(d->w % 128 == 0, EC2MOE_ERR_UNSUPPORTED, "w %d is not a multiple of 128", d->w);
+    REQUIRE(d->r_h % 16 == 0 && d->r_w % 16 == 0 && d->r_h <= 256 && d->r_w <= 256, EC2MOE_ERR_UNSUPPORTED,
+            "r_h and r_w must be multiples of 16 and at most 256");
+    REQUIRE(static_cast<int64_t>(d->h) * d->w < (int64_t(1) << 32), EC2MOE_ERR_UNSUPPORTED,
+            "slice too large for 32-bit element offsets");
+    return EC2MOE_OK;
+}
+
+int choose_splits(int M, int N, int K) {
+    const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
+    int s = std::max(1, 512 / std::max(1, tiles));
+    s = std::min(s, std::max(1, K / 64));
+    return std::min(s, 64);
+}
+
+struct CodecWs {
+    // encode
+    size_t vt, p, epart, enc_total;
+    int enc_splits;
+    // decode
+    size_t wt, dpart, dec_total;
+    int dec_splits;
+};
+
+CodecWs codec_ws(const ec2moe_codec_desc* d) {
+    const size_t eb = elem_bytes(static_cast<DType>(d->dtype));
+    CodecWs w{};
+    w.enc_splits = choose_splits(d->r_h, d->r_w, std::max(1, d->h));
+    size_t o = 0;
+    w.vt = o; o += up(static_cast<size_t>(d->r_w) * d->w * eb);
+    w.p = o; o += up(static_cast<size_t>(d->h) * d->r_w * 4);
+    w.epart = o; o += up(static_cast<size_t>(w.enc_splits) * d->r_h * d->r_w * 4);
+    w.enc_total = o;
+    w.dec_splits = choose_splits(d->w, d->r_h, d->r_w);
+    o = 0;
+    w.wt = o; o += up(static_cast<size_t>(d->w) * d->r_h * eb);
+    w.dpart = o; o += up(static_cast<size_t>(w.dec_splits) * d->w * d->r_h * 4);
+    w.dec_total = o;
+    return w;
+}
+
+// ---------------------------------------------------------------- kernel timing
+struct ProfRecord {
+    int name_id;
+    hipEvent_t start, stop;
+};
+
+struct Profiler {
+    std::mutex mu;
+    bool enabled = false;
+    std::vector<std::string> names;
+    std::vector<ProfRecord> records;
+    std::vector<hipEvent_t> pool;
+
+    int name_id(const char* n) {
+        for (size_t i = 0; i < names.size(); ++i)
+            if (names[i] == n) return static_cast<int>(i);
+        names.emplace_back(n);
+        return static_cast<int>(names.size() - 1);
+    }
+    hipEvent_t get() {
+        if (!pool.empty()) {
+            hipEvent_t e = pool.back();
+            pool.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+};
+
+Profiler& prof() {
+    static Profiler p;
+    return p;
+}
+
+}  // namespace
+
+ProfileScope::ProfileScope(const char* name, hipStream_t s) : slot(-1), stream(s) {
+    Profiler& p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    if (!p.enabled) return;
+    ProfRecord r{p.name_id(name), p.get(), p.get()};
+    if (!r.start || !r.stop) return;
+    if (hipEventRecord(r.start, s) != hipSuccess) return;
+    p.records.push_back(r);
+    slot = static_cast<int>(p.records.size() - 1);
+}
+
+ProfileScope::~ProfileScope() {
+    if (slot < 0) return;
+    Profiler& p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    if (slot < static_cast<int>(p.records.size())) (void)hipEventRecord(p.records[slot].stop, stream);
+}
+
+}  // namespace ec2moe
+
+using namespace ec2moe;
+
+extern "C" {
+
+const char* ec2moe_status_string(ec2moe_status s) {
+    switch (s) {
+        case EC2MOE_OK: return "ok";
+        case EC2MOE_ERR_INVALID_ARGUMENT: return "invalid argument";
+        case EC2MOE_ERR_UNSUPPORTED: return "unsupported shape or type";
+        case EC2MOE_ERR_TOO_FEW_CANDIDATES: return "fewer candidate experts than top_k";
+        case EC2MOE_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+        case EC2MOE_ERR_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+const char* ec2moe_last_error(void) { return g_last_error.c_str(); }
+
+ec2moe_status ec2moe_group_gate(const ec2moe_moe_desc* desc, const uint64_t* cand_mask, const void* x,
+                                const void* w_global, const float* b_global, const void* w_local,
+                                const float* b_local, int32_t* topk_idx, float* topk_w, float* probs,
+                                hipStream_t stream) {
+    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    REQUIRE_PTR(cand_mask);
+    const int M = desc->n_experts;
+    const int words = (M + 63) / 64;
+    int pop = 0;
+    for (int i = 0; i < words; ++i) {
+        uint64_t v = cand_mask[i];
+        const int valid_bits = std::min(64, M - 64 * i);
+        if (valid_bits < 64) REQUIRE((v >> valid_bits) == 0, EC2MOE_ERR_INVALID_ARGUMENT,
+                                     "cand_mask has bits set at or above n_experts %d", M);
+        pop += __builtin_popcountll(v);
+    }
+    REQUIRE(pop >= desc->top_k, EC2MOE_ERR_TOO_FEW_CANDIDATES, "%d candidate experts for top-%d", pop,
+            desc->top_k);
+    if (desc->n_tokens == 0) return ok();
+    REQUIRE_PTR(x); REQUIRE_PTR(w_global); REQUIRE_PTR(w_local); REQUIRE_PTR(topk_idx); REQUIRE_PTR(topk_w);
+    REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(w_global); REQUIRE_ALIGNED(w_local);
+    GateArgs a{};
+    a.x = x; a.w_global = w_global; a.b_global = b_global; a.w_local = w_local; a.b_local = b_local;
+    a.topk_idx = topk_idx; a.topk_w = topk_w; a.probs = probs;
+    a.n_tokens = desc->n_tokens; a.d = desc->d_model; a.n_experts = M; a.n_groups = desc->n_groups;
+    a.top_k = desc->top_k; a.renormalize = (desc->flags & EC2MOE_GATE_RENORMALIZE) != 0;
+    for (int i = 0; i < 4; ++i) a.mask[i] = i < words ? cand_mask[i] : 0;
+    return hip_status(launch_gate(static_cast<DType>(desc->dtype), a, stream), "gate launch");
+}
+
+ec2moe_status ec2moe_moe_workspace_size(const ec2moe_moe_desc* desc, size_t* bytes) {
+    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    REQUIRE_PTR(bytes);
+    *bytes = moe_ws(desc).total;
+    return ok();
+}
+
+ec2moe_status ec2moe_permute(const ec2moe_moe_desc* desc, const int32_t* topk_idx, const void* x,
+                             int32_t* seg_offsets, int32_t* perm_src, int32_t* inv_perm, void* x_perm, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    const MoeWs w = moe_ws(desc);
+    if (ec2moe_status st = check_ws(ws, ws_bytes, w.total); st != EC2MOE_OK) return st;
+    REQUIRE_PTR(seg_offsets);
+    REQUIRE((x == nullptr) == (x_perm == nullptr), EC2MOE_ERR_INVALID_ARGUMENT,
+            "x and x_perm must both be given or both be NULL");
+    const int64_t A = static_cast<int64_t>(desc->n_tokens) * desc->top_k;
+    if (A > 0) {
+        REQUIRE_PTR(topk_idx); REQUIRE_PTR(perm_src); REQUIRE_PTR(inv_perm);
+        if (x) { REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(x_perm); }
+    }
+    hipError_t e = launch_permute(topk_idx, A, desc->top_k, desc->n_experts, at<int32_t>(ws, w.counts),
+                                  seg_offsets, perm_src, inv_perm, stream);
+    if (e == hipSuccess && x)
+        e = launch_gather_rows(static_cast<DType>(desc->dtype), x, desc->n_tokens, perm_src,
+                               seg_offsets + desc->n_experts, A, desc->d_model, x_perm, stream);
+    return hip_status(e, "permute launch");
+}
+
+namespace {
+
+hipError_t run_experts(const ec2moe_moe_desc* desc, const void* x, const int32_t* seg, const int32_t* perm_src,
+                       const void* w_gate_up, const void* w_down, void* act, void* y_perm, hipStream_t stream) {
+    const DType dt = static_cast<DType>(desc->dtype);
+    const int64_t A = static_cast<int64_t>(desc->n_tokens) * desc->top_k;
+    const int d = desc->d_model, H = desc->ffn_hidden;
+    GemmArgs g1{};
+    g1.tok = x; g1.row_index = perm_src; g1.w = w_gate_up;
+    g1.w_group_stride = int64_t(2) * H * d; g1.seg = seg; g1.n_groups = desc->n_experts;
+    g1.rows = A; g1.K = d; g1.N = H; g1.out = act; g1.ldo = H;
+    hipError_t e = launch_gemm(dt, Epilogue::SwiGLU, OutType::Same, g1, stream);
+    if (e != hipSuccess) return e;
+    GemmArgs g2{};
+    g2.tok = act; g2.row_index = nullptr; g2.w = w_down;
+    g2.w_group_stride = int64_t(d) * H; g2.seg = seg; g2.n_groups = desc->n_experts;
+    g2.rows = A; g2.K = H; g2.N = d; g2.out = y_perm; g2.ldo = d;
+    return launch_gemm(dt, Epilogue::Store, OutType::Same, g2, stream);
+}
+
+}  // namespace
+
+ec2moe_status ec2moe_expert_ffn(const ec2moe_moe_desc* desc, const void* x, const int32_t* seg_offsets,
+                                const int32_t* perm_src, const void* w_gate_up, const void* w_down, void* act,
+                                void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    const MoeWs w = moe_ws(desc);
+    if (ec2moe_status st = check_ws(ws, ws_bytes, w.total); st != EC2MOE_OK) return st;
+    if (desc->n_tokens == 0) return ok();
+    REQUIRE_PTR(x); REQUIRE_PTR(seg_offsets); REQUIRE_PTR(perm_src); REQUIRE_PTR(w_gate_up); REQUIRE_PTR(w_down);
+    REQUIRE_PTR(y_perm);
+    REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(w_gate_up); REQUIRE_ALIGNED(w_down); REQUIRE_ALIGNED(y_perm);
+    if (act) REQUIRE_ALIGNED(act);
+    void* act_buf = act ? act : at<void>(ws, w.act);
+    return hip_status(run_experts(desc, x, seg_offsets, perm_src, w_gate_up, w_down, act_buf, y_perm, stream),
+                      "expert GEMM launch");
+}
+
+ec2moe_status ec2moe_combine(const ec2moe_moe_desc* desc, const void* y_perm, const int32_t* inv_perm,
+                             const float* topk_w, void* y, hipStream_t stream) {
+    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    if (desc->n_tokens == 0) return ok();
+    REQUIRE_PTR(y_perm); REQUIRE_PTR(inv_perm); REQUIRE_PTR(topk_w); REQUIRE_PTR(y);
+    REQUIRE_ALIGNED(y_perm); REQUIRE_ALIGNED(y);
+    return hip_status(launch_combine(static_cast<DType>(desc->dtype), y_perm, inv_perm, topk_w, desc->n_tokens,
+                                     desc->top_k, desc->d_model, y, stream),
+                      "combine launch");
+}
+
+ec2moe_status ec2moe_moe_forward(const ec2moe_moe_desc* desc, const void* x, const int32_t* topk_idx,
+                                 const float* topk_w, const void* w_gate_up, const void* w_down, void* y, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    const MoeWs w = moe_ws(desc);
+    if (ec2moe_status st = check_ws(ws, ws_bytes, w.total); st != EC2MOE_OK) return st;
+    if (desc->n_tokens == 0) return ok();
+    REQUIRE_PTR(x); REQUIRE_PTR(topk_idx); REQUIRE_PTR(topk_w); REQUIRE_PTR(w_gate_up); REQUIRE_PTR(w_down);
+    REQUIRE_PTR(y);
+    REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(w_gate_up); REQUIRE_ALIGNED(w_down); REQUIRE_ALIGNED(y);
+    const int64_t A = static_cast<int64_t>(desc->n_tokens) * desc->top_k;
+    int32_t* seg = at<int32_t>(ws, w.seg);
+    int32_t* perm_src = at<int32_t>(ws, w.perm_src);
+    int32_t* inv_perm = at<int32_t>(ws, w.inv_perm);
+    void* act = at<void>(ws, w.act);
+    void* y_perm = at<void>(ws, w.y_perm);
+    hipError_t e = launch_permute(topk_idx, A, desc->top_k, desc->n_experts, at<int32_t>(ws, w.counts), seg,
+                                  perm_src, inv_perm, stream);
+    if (e == hipSuccess) e = run_experts(desc, x, seg, perm_src, w_gate_up, w_down, act, y_perm, stream);
+    if (e == hipSuccess)
+        e = launch_combine(static_cast<DType>(desc->dtype), y_perm, inv_perm, topk_w, desc->n_tokens, desc->top_k,
+                           desc->d_model, y, stream);
+    return hip_status(e, "moe_forward launch");
+}
+
+ec2moe_status ec2moe_lowrank_workspace_size(const ec2moe_codec_desc* desc, size_t* bytes) {
+    if (ec2moe_status st = check_codec_desc(desc); st != EC2MOE_OK) return st;
+    REQUIRE_PTR(bytes);
+    const CodecWs w = codec_ws(desc);
+    *bytes = std::max(w.enc_total, w.dec_total);
+    return ok();
+}
+
+ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x, const void* u, const void* v,
+                                    float* z, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (ec2moe_status st = check_codec_desc(desc); st != EC2MOE_OK) return st;
+    const CodecWs w = codec_ws(desc);
+    if (ec2moe_status st = check_ws(ws, ws_bytes, std::max(w.enc_total, w.dec_total)); st != EC2MOE_OK) return st;
+    if (desc->n_slices == 0) return ok();
+    REQUIRE(desc->h > 0, EC2MOE_ERR_INVALID_ARGUMENT, "h must be positive");
+    REQUIRE_PTR(x); REQUIRE_PTR(u); REQUIRE_PTR(v); REQUIRE_PTR(z);
+    REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(u); REQUIRE_ALIGNED(v); REQUIRE_ALIGNED(z);
+    const DType dt = static_cast<DType>(desc->dtype);
+    const size_t eb = elem_bytes(dt);
+    void* vt = at<void>(ws, w.vt);
+    float* p = at<float>(ws, w.p);
+    hipError_t e = launch_transpose(dt, v, desc->w, desc->r_w, vt, stream);
+    for (int c = 0; c < desc->n_slices && e == hipSuccess; ++c) {
+        const char* xc = static_cast<const char*>(x) + static_cast<size_t>(c) * desc->h * desc->w * eb;
+        // P = X V  [h][r_w], float32
+        GemmArgs g{};
+        g.tok = xc; g.row_index = nullptr; g.w = vt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
+        g.rows = desc->h; g.K = desc->w; g.N = desc->r_w; g.out = p; g.ldo = desc->r_w;
+        e = launch_gemm(dt, Epilogue::Store, OutType::F32, g, stream);
+        if (e != hipSuccess) break;
+        // Z = U^T P  [r_h][r_w]: A(m,k) = U[k][m], B(k,n) = P[k][n]
+        SmallGemmArgs s{};
+        s.a = u; s.a_dt = dt; s.a_sm = 1; s.a_sk = desc->r_h;
+        s.b = p; s.b_dt = DType::F32; s.b_sk = desc->r_w; s.b_sn = 1;
+        s.M = desc->r_h; s.N = desc->r_w; s.K = desc->h;
+        s.out = z + static_cast<size_t>(c) * desc->r_h * desc->r_w; s.out_dt = DType::F32;
+        s.part = at<float>(ws, w.epart); s.splits = w.enc_splits;
+        e = launch_small_gemm(s, stream);
+    }
+    return hip_status(e, "lowrank_encode launch");
+}
+
+ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* z, const void* u_hat,
+                                    const void* v_hat, void* x_hat, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (ec2moe_status st = check_codec_desc(desc); st != EC2MOE_OK) return st;
+    const CodecWs w = codec_ws(desc);
+    if (ec2moe_status st = check_ws(ws, ws_bytes, std::max(w.enc_total, w.dec_total)); st != EC2MOE_OK) return st;
+    if (desc->n_slices == 0) return ok();
+    REQUIRE(desc->h > 0, EC2MOE_ERR_INVALID_ARGUMENT, "h must be positive");
+    REQUIRE_PTR(z); REQUIRE_PTR(u_hat); REQUIRE_PTR(v_hat); REQUIRE_PTR(x_hat);
+    REQUIRE_ALIGNED(z); REQUIRE_ALIGNED(u_hat); REQUIRE_ALIGNED(v_hat); REQUIRE_ALIGNED(x_hat);
+    const DType dt = static_cast<DType>(desc->dtype);
+    const size_t eb = elem_bytes(dt);
+    void* wt = at<void>(ws, w.wt);
+    hipError_t e = hipSuccess;
+    for (int c = 0; c < desc->n_slices && e == hipSuccess; ++c) {
+        // Wt = V_hat Z^T  [w][r_h]: A(m,k) = V_hat[m][k], B(k,n) = Z[n][k]; rounded to the layer dtype
+        SmallGemmArgs s{};
+        s.a = v_hat; s.a_dt = dt; s.a_sm = desc->r_w; s.a_sk = 1;
+        s.b = z + static_cast<size_t>(c) * desc->r_h * desc->r_w; s.b_dt = DType::F32; s.b_sk = 1; s.b_sn = desc->r_w;
+        s.M = desc->w; s.N = desc->r_h; s.K = desc->r_w;
+        s.out = wt; s.out_dt = dt;
+        s.part = at<float>(ws, w.dpart); s.splits = w.dec_splits;
+        e = launch_small_gemm(s, stream);
+        if (e != hipSuccess) break;
+        // X_hat = U_hat Wt^T  [h][w]
+        GemmArgs g{};
+        g.tok = u_hat; g.row_index = nullptr; g.w = wt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
+        g.rows = desc->h; g.K = desc->r_h; g.N = desc->w;
+        g.out = static_cast<char*>(x_hat) + static_cast<size_t>(c) * desc->h * desc->w * eb; g.ldo = desc->w;
+        e = launch_gemm(dt, Epilogue::Store, OutType::Same, g, stream);
+    }
+    return hip_status(e, "lowrank_decode launch");
+}
+
+ec2moe_status ec2moe_profile_enable(int32_t enable) {
+    Profiler& p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    p.enabled = enable != 0;
+    return ok();
+}
+
+ec2moe_status ec2moe_profile_collect(ec2moe_kernel_stat* out, int32_t max_entries, int32_t* n_out) {
+    REQUIRE_PTR(n_out);
+    REQUIRE(max_entries >= 0, EC2MOE_ERR_INVALID_ARGUMENT, "max_entries < 0");
+    REQUIRE(max_entries == 0 || out != nullptr, EC2MOE_ERR_INVALID_ARGUMENT, "out is NULL");
+    Profiler& p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    std::vector<int64_t> launches(p.names.size(), 0);
+    std::vector<double> ms(p.names.size(), 0.0);
+    hipError_t err = hipSuccess;
+    for (const ProfRecord& r : p.records) {
+        if (err == hipSuccess) err = hipEventSynchronize(r.stop);
+        float t = 0.f;
+        if (err == hipSuccess) err = hipEventElapsedTime(&t, r.start, r.stop);
+        launches[r.name_id] += 1;
+        ms[r.name_id] += t;
+        p.pool.push_back(r.start);
+        p.pool.push_back(r.stop);
+    }
+    p.records.clear();
+    int n = 0;
+    for (size_t i = 0; i < p.names.size(); ++i) {
+        if (launches[i] == 0) continue;
+        if (n < max_entries) {
+            std::memset(out[n].name, 0, sizeof out[n].name);
+            std::strncpy(out[n].name, p.names[i].c_str(), sizeof out[n].name - 1);
+            out[n].launches = launches[i];
+            out[n].total_ms = ms[i];
+        }
+        ++n;
+    }
+    *n_out = std::min(n, max_entries);
+    return hip_status(err, "profile collect");
+}
+
+}  // extern "C"

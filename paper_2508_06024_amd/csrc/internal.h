@@ -1,0 +1,97 @@
+// Host-side interface between the C ABI (api.cpp) and the kernel launchers (*.hip).
+// Launchers assume validated arguments; they return the HIP error of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ec2moe {
+
+enum class DType : int32_t { F32 = 0, BF16 = 1 };
+
+inline size_t elem_bytes(DType t) { return t == DType::F32 ? 4 : 2; }
+
+// ---------------------------------------------------------------- kernel timing
+// Brackets a launch with events when profiling is on (see ec2moe_profile_enable).
+struct ProfileScope {
+    ProfileScope(const char* name, hipStream_t s);
+    ~ProfileScope();
+    int slot;
+    hipStream_t stream;
+};
+
+// ---------------------------------------------------------------- gate
+struct GateArgs {
+    const void* x;
+    const void* w_global;
+    const float* b_global;
+    const void* w_local;
+    const float* b_local;
+    int32_t* topk_idx;
+    float* topk_w;
+    float* probs;
+    int n_tokens, d, n_experts, n_groups, top_k;
+    bool renormalize;
+    uint64_t mask[4];
+};
+hipError_t launch_gate(DType dt, const GateArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- permutation
+// Work split of the permutation kernels: assignments are processed in chunks of
+// kPermChunk; per-chunk counts live in the workspace.
+constexpr int kPermChunk = 4096;
+inline int perm_chunks(int64_t n_assign) { return static_cast<int>((n_assign + kPermChunk - 1) / kPermChunk); }
+
+hipError_t launch_permute(const int32_t* topk_idx, int64_t n_assign, int top_k, int n_experts,
+                          int32_t* chunk_counts /*[chunks][M]*/, int32_t* seg_offsets,
+                          int32_t* perm_src, int32_t* inv_perm, hipStream_t s);
+// x_perm[r] = x[perm_src[r]] for r < *seg_end (device scalar: the last segment offset); zeros beyond
+hipError_t launch_gather_rows(DType dt, const void* x, int64_t n_src, const int32_t* perm_src,
+                              const int32_t* seg_end, int64_t n_rows, int d, void* x_perm, hipStream_t s);
+
+// ---------------------------------------------------------------- grouped / dense GEMM
+// out[p][n] = sum_k tok[row(p)][k] * w_e[n][k] for every row p of group e, where
+// row(p) = row_index ? row_index[p] : p and w_e = w + e * w_group_stride.
+// SwiGLU mode: weight rows 0..N-1 are the gate branch and N..2N-1 the up branch; the
+// output is silu(gate) * up with N columns.
+enum class Epilogue : int { Store = 0, SwiGLU = 1 };
+enum class OutType : int { Same = 0, F32 = 1 };
+
+struct GemmArgs {
+    const void* tok;          // [rows][K]
+    const int32_t* row_index; // gather map or null
+    const void* w;            // [groups][Nw][K]
+    int64_t w_group_stride;   // elements between consecutive groups' weights
+    const int32_t* seg;       // [groups+1] device segment offsets, or null (dense: one group)
+    int n_groups;
+    int64_t rows;             // total rows (upper bound for grouped; exact for dense)
+    int K;
+    int N;                    // output columns
+    void* out;                // [rows][N]
+    int64_t ldo;              // output row stride (elements)
+};
+hipError_t launch_gemm(DType dt, Epilogue epi, OutType ot, const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- combine
+hipError_t launch_combine(DType dt, const void* y_perm, const int32_t* inv_perm, const float* w,
+                          int n_tokens, int top_k, int d, void* y, hipStream_t s);
+
+// ---------------------------------------------------------------- codec helpers
+// dst[c][r] = src[r][c] for a rows x cols matrix
+hipError_t launch_transpose(DType dt, const void* src, int rows, int cols, void* dst, hipStream_t s);
+
+// C[m][n] = sum_k A(m,k) * B(k,n), float32 accumulation, split over k in `splits`
+// deterministic parts (partials in `part`, [splits][M][N] float32), then reduced in order.
+//   A(m,k) = a[m*a_sm + k*a_sk] (element type a_dt), B(k,n) = b[k*b_sk + n*b_sn] (b_dt).
+// Output element type out_dt (float32 or the layer dtype).
+struct SmallGemmArgs {
+    const void* a; DType a_dt; int64_t a_sm, a_sk;
+    const void* b; DType b_dt; int64_t b_sk, b_sn;
+    int M, N, K;
+    void* out; DType out_dt;
+    float* part; int splits;
+};
+hipError_t launch_small_gemm(const SmallGemmArgs& g, hipStream_t s);
+
+}  // namespace ec2moe

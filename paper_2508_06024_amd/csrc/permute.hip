@@ -1,0 +1,196 @@
+// Dispatch of (token, slot) assignments to per-expert segments, for gfx950.
+//
+// The assignments a = t*k + j are sorted stably by expert id with integer work only:
+//   1. count:   each 4096-assignment chunk builds an LDS histogram over the experts;
+//   2. scan:    one workgroup turns the chunk counts into segment offsets and the
+//               first position of every (chunk, expert) pair;
+//   3. scatter: each wave walks 1024 consecutive assignments 64 at a time; lanes with
+//               the same expert find each other with one ballot per bit of the expert
+//               id, so the rank inside the 64 comes from a popcount and the order of
+//               the input is kept.
+// No floating point and no global atomics: the result is unique and deterministic.
+#include "device_common.h"
+#include "internal.h"
+
+#include <algorithm>
+
+namespace ec2moe {
+namespace {
+
+constexpr int kWaveItems = kPermChunk / 4;  // assignments per wave per chunk
+static_assert(kWaveItems % 64 == 0, "chunk must split into whole wave passes");
+
+__global__ __launch_bounds__(256) void perm_count_kernel(const int32_t* __restrict__ idx, int64_t n,
+                                                         int M, int32_t* __restrict__ counts) {
+    __shared__ int hist[256];
+    for (int e = threadIdx.x; e < M; e += 256) hist[e] = 0;
+    __syncthreads();
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kPermChunk;
+    for (int i = threadIdx.x; i < kPermChunk; i += 256) {
+        const int64_t a = base + i;
+        if (a < n) {
+            const int e = idx[a];
+            if (e >= 0 && e < M) atomicAdd(&hist[e], 1);
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < M; e += 256) counts[static_cast<int64_t>(blockIdx.x) * M + e] = hist[e];
+}
+
+// counts[c][e] -> absolute first position of chunk c's assignments to expert e
+__global__ __launch_bounds__(256) void perm_scan_kernel(int32_t* __restrict__ counts, int n_chunks, int M,
+                                                        int32_t* __restrict__ seg) {
+    __shared__ int total[256];
+    const int e = threadIdx.x;
+    int run = 0;
+    if (e < M) {
+        for (int c = 0; c < n_chunks; ++c) {
+            const int v = counts[static_cast<int64_t>(c) * M + e];
+            counts[static_cast<int64_t>(c) * M + e] = run;
+            run += v;
+        }
+        total[e] = run;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int s = 0;
+        for (int i = 0; i < M; ++i) {
+            const int v = total[i];
+            total[i] = s;
+            s += v;
+        }
+        seg[M] = s;
+    }
+    __syncthreads();
+    if (e < M) {
+        const int start = total[e];
+        seg[e] = start;
+        for (int c = 0; c < n_chunks; ++c) counts[static_cast<int64_t>(c) * M + e] += start;
+    }
+}
+
+__global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __restrict__ idx, int64_t n, int top_k,
+                                                           int M, const int32_t* __restrict__ chunk_base,
+                                                           int32_t* __restrict__ perm_src,
+                                                           int32_t* __restrict__ inv_perm) {
+    __shared__ int wcount[4][256];
+    __shared__ int wpos[4][256];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    for (int i = threadIdx.x; i < 4 * 256; i += 256) (&wcount[0][0])[i] = 0;
+    __syncthreads();
+    const int64_t wbeg = static_cast<int64_t>(blockIdx.x) * kPermChunk + static_cast<int64_t>(wave) * kWaveItems;
+    for (int i = lane; i < kWaveItems; i += 64) {
+        const int64_t a = wbeg + i;
+        if (a < n) {
+            const int e = idx[a];
+            if (e >= 0 && e < M) atomicAdd(&wcount[wave][e], 1);
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < M; e += 256) {
+        int b = chunk_base[static_cast<int64_t>(blockIdx.x) * M + e];
+        for (int w = 0; w < 4; ++w) {
+            wpos[w][e] = b;
+            b += wcount[w][e];
+        }
+    }
+    __syncthreads();
+
+    int nbits = 0;
+    while ((1 << nbits) < M) ++nbits;
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    for (int s = 0; s < kWaveItems; s += 64) {
+        const int64_t a = wbeg + s + lane;
+        int e = -1;
+        if (a < n) {
+            e = idx[a];
+            if (e < 0 || e >= M) {
+                inv_perm[a] = -1;
+                e = -1;
+            }
+        }
+        const bool valid = e >= 0;
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < nbits; ++b) {
+            const bool bit = valid && ((e >> b) & 1);
+            const uint64_t ones = __ballot(bit);
+            peers &= bit ? ones : ~ones;
+        }
+        if (valid) {
+            const int rank = __popcll(peers & lt_mask);
+            const int pos = wpos[wave][e] + rank;
+            perm_src[pos] = static_cast<int32_t>(a / top_k);
+            inv_perm[a] = pos;
+        }
+        // every lane has read its base; the first lane of each expert advances it
+        __builtin_amdgcn_wave_barrier();
+        if (valid && (peers & lt_mask) == 0) wpos[wave][e] += __popcll(peers);
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// Rows past the valid segments (only when some expert ids were out of range) and
+// source ids outside [0, n_src) are written as zeros.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const char* __restrict__ x,
+                                                          const int32_t* __restrict__ perm_src,
+                                                          const int32_t* __restrict__ seg_end, int64_t n_src,
+                                                          int64_t rows, int row_chunks, char* __restrict__ out) {
+    const int64_t total = rows * row_chunks;
+    const int64_t valid_rows = *seg_end;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < total;
+         i += static_cast<int64_t>(gridDim.x) * 256) {
+        const int64_t r = i / row_chunks;
+        const int c = static_cast<int>(i - r * row_chunks);
+        const int64_t src = r < valid_rows ? perm_src[r] : -1;
+        const uint4 v = (src >= 0 && src < n_src) ? ldg16(x + (src * row_chunks + c) * 16) : make_uint4(0, 0, 0, 0);
+        stg16(out + (r * row_chunks + c) * 16, v);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_permute(const int32_t* topk_idx, int64_t n_assign, int top_k, int n_experts,
+                          int32_t* chunk_counts, int32_t* seg_offsets, int32_t* perm_src,
+                          int32_t* inv_perm, hipStream_t s) {
+    const int chunks = perm_chunks(n_assign);
+    if (chunks == 0) {
+        ProfileScope prof("perm_scan", s);
+        hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(256), 0, s, chunk_counts, 0, n_experts, seg_offsets);
+        return hipGetLastError();
+    }
+    {
+        ProfileScope prof("perm_count", s);
+        hipLaunchKernelGGL(perm_count_kernel, dim3(chunks), dim3(256), 0, s, topk_idx, n_assign, n_experts,
+                           chunk_counts);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    {
+        ProfileScope prof("perm_scan", s);
+        hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(256), 0, s, chunk_counts, chunks, n_experts,
+                           seg_offsets);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    {
+        ProfileScope prof("perm_scatter", s);
+        hipLaunchKernelGGL(perm_scatter_kernel, dim3(chunks), dim3(256), 0, s, topk_idx, n_assign, top_k,
+                           n_experts, chunk_counts, perm_src, inv_perm);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(DType dt, const void* x, int64_t n_src, const int32_t* perm_src,
+                              const int32_t* seg_end, int64_t n_rows, int d, void* x_perm, hipStream_t s) {
+    if (n_rows == 0) return hipSuccess;
+    const int row_chunks = static_cast<int>(d * elem_bytes(dt) / 16);
+    const int64_t total = n_rows * row_chunks;
+    const int grid = static_cast<int>(std::min<int64_t>((total + 255) / 256, 8192));
+    ProfileScope prof("gather_rows", s);
+    hipLaunchKernelGGL(gather_rows_kernel, dim3(grid), dim3(256), 0, s, static_cast<const char*>(x), perm_src,
+                       seg_end, n_src, n_rows, row_chunks, static_cast<char*>(x_perm));
+    return hipGetLastError();
+}
+
+}  // namespace ec2moe

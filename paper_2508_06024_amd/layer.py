@@ -1,0 +1,57 @@
+"""One group-gated MoE layer with the low-rank codec at the end-cloud cut, on device.
+
+The step follows the paper's pipeline (EC2MoE Overall Design; HL-GGN then PO-ECC):
+the end side routes the hidden states X with the hardware-aware group gate and
+compresses them, Z = U^T X V; the cloud side reconstructs X_hat = U_hat Z V_hat^T and
+runs the sparse MoE layer of Eq. 1 on X_hat with the end side's routing:
+
+    route = group_gate(X, mask);  Z = encode(X);  X_hat = decode(Z);  y = moe(X_hat, route)
+
+All four are calls into libec2moe; this class only owns the device buffers (allocated
+once) and issues the calls on the current stream.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import ec2moe as E
+
+
+class Ec2moeLayer:
+    def __init__(self, x, mask_words, w_global, b_global, w_local, b_local, w_gate_up, w_down, u, v,
+                 u_hat=None, v_hat=None, n_groups=1, top_k=1, renormalize=True):
+        T, d = x.shape
+        M, H2, _ = w_gate_up.shape
+        dt = x.dtype
+        dev = x.device
+        self.x, self.mask = x, list(mask_words)
+        self.w_global, self.b_global, self.w_local, self.b_local = w_global, b_global, w_local, b_local
+        self.w_gate_up, self.w_down = w_gate_up, w_down
+        self.u, self.v = u, v
+        self.u_hat = u if u_hat is None else u_hat
+        self.v_hat = v if v_hat is None else v_hat
+        self.moe_desc = E.moe_desc(T, M, n_groups, d, H2 // 2, top_k, dt, renormalize)
+        self.codec_desc = E.codec_desc(T, d, u.shape[1], v.shape[1], dt)
+        self.topk_idx = torch.empty((T, top_k), dtype=torch.int32, device=dev)
+        self.topk_w = torch.empty((T, top_k), dtype=torch.float32, device=dev)
+        self.z = torch.empty((u.shape[1], v.shape[1]), dtype=torch.float32, device=dev)
+        self.x_hat = torch.empty((T, d), dtype=dt, device=dev)
+        self.y = torch.empty((T, d), dtype=dt, device=dev)
+        self.moe_ws = E.workspace(E.moe_workspace_size(self.moe_desc), dev)
+        self.codec_ws = E.workspace(E.lowrank_workspace_size(self.codec_desc), dev)
+
+    def set_input(self, x, mask_words=None):
+        """Point the layer at another [T][d] input (and candidate mask) of the same shape."""
+        assert x.shape == self.x.shape and x.dtype == self.x.dtype
+        self.x = x
+        if mask_words is not None:
+            self.mask = list(mask_words)
+
+    def step(self):
+        E.group_gate(self.moe_desc, self.mask, self.x, self.w_global, self.b_global, self.w_local,
+                     self.b_local, self.topk_idx, self.topk_w)
+        E.lowrank_encode_into(self.codec_desc, self.x, self.u, self.v, self.z, self.codec_ws)
+        E.lowrank_decode_into(self.codec_desc, self.z, self.u_hat, self.v_hat, self.x_hat, self.codec_ws)
+        E.moe_forward_into(self.moe_desc, self.x_hat, self.topk_idx, self.topk_w, self.w_gate_up,
+                           self.w_down, self.y, self.moe_ws)
+        return self.y

@@ -1,0 +1,148 @@
+"""The C ABI on the CPU: the library loads without a GPU, exports every entry point the
+header declares, and rejects bad arguments on the host, before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2508_06024_amd import ec2moe as E
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ec2moe.h")
+
+OK, INVALID, UNSUPPORTED, TOO_FEW, WS_SMALL = 0, 1, 2, 3, 4
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:ec2moe_status|const char\s*\*)\s*(ec2moe_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_header_declares_the_expected_calls():
+    names = declared_functions()
+    for n in ("ec2moe_group_gate", "ec2moe_moe_forward", "ec2moe_lowrank_encode", "ec2moe_lowrank_decode",
+              "ec2moe_permute", "ec2moe_combine", "ec2moe_expert_ffn"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(E.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(declared_functions()) == sorted(E.EXPORTS)
+
+
+def test_status_strings():
+    assert E.status_string(0) == "ok"
+    assert "candidate" in E.status_string(3)
+    assert E.status_string(99) == "unknown status"
+
+
+def _desc(**kw):
+    base = dict(n_tokens=64, n_experts=8, n_groups=2, d_model=128, ffn_hidden=256, top_k=2, dtype=E.BF16,
+                renormalize=True)
+    base.update(kw)
+    return E.moe_desc(**base)
+
+
+def _ws_size(desc):
+    n = ctypes.c_size_t(0)
+    st = E._lib.ec2moe_moe_workspace_size(ctypes.byref(desc), ctypes.byref(n))
+    return st, n.value
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_groups=3), INVALID),            # K does not divide M
+    (dict(top_k=9), INVALID),               # k > M
+    (dict(n_tokens=-1), INVALID),
+    (dict(d_model=0), INVALID),
+    (dict(dtype=7), INVALID),
+    (dict(d_model=96), UNSUPPORTED),        # not a multiple of 128
+    (dict(ffn_hidden=200), UNSUPPORTED),
+    (dict(n_experts=512, n_groups=8), UNSUPPORTED),
+    (dict(top_k=17, n_experts=32, n_groups=4), UNSUPPORTED),
+    (dict(), OK),
+])
+def test_descriptor_validation(kw, status):
+    st, n = _ws_size(_desc(**kw))
+    assert st == status, E.last_error()
+    if status == OK:
+        assert n > 0
+    else:
+        assert E.last_error()
+
+
+def test_workspace_size_grows_with_tokens():
+    _, a = _ws_size(_desc(n_tokens=64))
+    _, b = _ws_size(_desc(n_tokens=4096))
+    assert b > a
+    _, z = _ws_size(_desc(n_tokens=0))
+    assert 0 < z < a
+
+
+def _gate(desc, words, ptr=1 << 20):
+    arr = E.mask_array(words)
+    p = ctypes.c_void_p(ptr)
+    return E._lib.ec2moe_group_gate(ctypes.byref(desc), arr, p, p, None, p, None, p, p, None, None)
+
+
+def test_gate_rejects_too_few_candidates_before_launch():
+    assert _gate(_desc(top_k=2), [0b1]) == TOO_FEW
+    assert "candidate" in E.last_error()
+
+
+def test_gate_rejects_mask_bits_beyond_experts():
+    assert _gate(_desc(), [0x1FF]) == INVALID
+
+
+def test_gate_rejects_null_and_misaligned_pointers():
+    words = [0xFF]
+    d = _desc()
+    arr = E.mask_array(words)
+    assert E._lib.ec2moe_group_gate(ctypes.byref(d), arr, None, None, None, None, None, None, None, None,
+                                    None) == INVALID
+    assert _gate(d, words, ptr=(1 << 20) + 4) == INVALID
+    assert "aligned" in E.last_error()
+
+
+def test_gate_with_no_tokens_is_a_no_op():
+    assert _gate(_desc(n_tokens=0), [0xFF]) == OK
+
+
+def test_moe_forward_rejects_small_workspace():
+    d = _desc()
+    _, need = _ws_size(d)
+    p = ctypes.c_void_p(1 << 20)
+    st = E._lib.ec2moe_moe_forward(ctypes.byref(d), p, p, p, p, p, p, p, need - 1, None)
+    assert st == WS_SMALL
+    st = E._lib.ec2moe_moe_forward(ctypes.byref(d), p, p, p, p, p, p, None, need, None)
+    assert st == INVALID
+
+
+def test_permute_requires_x_and_x_perm_together():
+    d = _desc()
+    _, need = _ws_size(d)
+    p = ctypes.c_void_p(1 << 20)
+    st = E._lib.ec2moe_permute(ctypes.byref(d), p, p, p, p, p, None, p, need, None)
+    assert st == INVALID
+
+
+def test_codec_validation():
+    def size(**kw):
+        base = dict(h=64, w=128, r_h=16, r_w=16, dtype=E.F32, n_slices=1)
+        base.update(kw)
+        desc = E.codec_desc(**base)
+        n = ctypes.c_size_t(0)
+        return E._lib.ec2moe_lowrank_workspace_size(ctypes.byref(desc), ctypes.byref(n)), n.value
+
+    assert size()[0] == OK and size()[1] > 0
+    assert size(r_h=80)[0] == INVALID      # r_h > h
+    assert size(r_w=24)[0] == UNSUPPORTED  # not a multiple of 16
+    assert size(w=96)[0] == UNSUPPORTED
+    assert size(r_w=512, w=1024)[0] == UNSUPPORTED
+
+
+def test_profile_collect_without_records():
+    assert E.profile_collect() == {}

@@ -1,0 +1,68 @@
+"""The whole step against the oracle: route on X, compress, reconstruct, experts on X_hat."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2508_06024_amd import workload as W
+from paper_2508_06024_amd.layer import Ec2moeLayer
+from tests.gpu_common import assert_close, check_routing, down, say, tol, up, up_f32
+
+pytestmark = pytest.mark.gpu
+
+
+def build(inp):
+    cfg = inp.cfg
+    dt = cfg.dtype
+    return Ec2moeLayer(up(inp.x, dt), inp.mask, up(inp.w_global, dt), up_f32(inp.b_global), up(inp.w_local, dt),
+                       up_f32(inp.b_local), up(inp.w_gate_up, dt), up(inp.w_down, dt), up(inp.u, dt),
+                       up(inp.v, dt), n_groups=cfg.n_groups, top_k=cfg.top_k)
+
+
+def oracle_sampled(inp, toks):
+    """Oracle layer outputs of the sampled tokens: the gate and the experts act per token;
+    the codec's Z couples all tokens and is computed in full."""
+    cfg = inp.cfg
+    f = inp.f64
+    x, u, v = f("x"), f("u"), f("v")
+    idx, w, g = O.group_gate(x[toks], f("w_global"), inp.b_global, f("w_local"), inp.b_local, inp.mask,
+                             cfg.n_groups, cfg.top_k)
+    z = O.lowrank_encode(x, u, v)
+    xh = O.lowrank_decode(z, u[toks], v)
+    y = np.zeros((len(toks), cfg.d_model))
+    for e in np.unique(idx):
+        gu = W.to_f64(inp.w_gate_up[e], cfg.dtype)
+        dn = W.to_f64(inp.w_down[e], cfg.dtype)
+        rows, slots = np.nonzero(idx == e)
+        y[rows] += w[rows, slots, None] * O.swiglu_expert(xh[rows], gu, dn)
+    return idx, w, g, z, xh, y
+
+
+@pytest.mark.parametrize("name,call,sample", [("tiny", None, 0), ("small", None, 0), ("mixtral", None, 40),
+                                              ("finegrained", None, 40), ("decode", 4, 0), ("decode", 777, 0)])
+def test_layer_step_matches_oracle(name, call, sample):
+    cfg = W.CONFIGS[name]
+    say(f"layer {name} call {call}")
+    torch.cuda.empty_cache()
+    inp = W.gen_layer(cfg, call_seed=call)
+    lay = build(inp)
+    lay.step()
+    torch.cuda.synchronize()
+    T = cfg.n_tokens
+    if sample:
+        rng = np.random.default_rng(1)
+        toks = np.array(sorted(set(rng.choice(T, sample, replace=False).tolist()) | {0, T - 1}))
+    else:
+        toks = np.arange(T)
+    idx, w, g, z, xh, y = oracle_sampled(inp, toks)
+    gidx, gw = down(lay.topk_idx)[toks], down(lay.topk_w)[toks]
+    n_cert = check_routing(gidx, gw, idx, w, g, W.mask_members(inp.mask, cfg.n_experts), cfg.top_k)
+    assert_close(down(lay.z), z, 1e-5, "Z")
+    assert_close(down(lay.x_hat)[toks], xh, tol(cfg.dtype), "X_hat")
+    same = ~(gidx != idx).any(axis=1)
+    e = assert_close(down(lay.y)[toks][same], y[same], tol(cfg.dtype), "y")
+    say(f"  y rel err {e:.2e}; certified near-ties {n_cert}")
+    # same inputs, same bits
+    y1 = lay.y.clone()
+    lay.step()
+    assert torch.equal(lay.y, y1)
