@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""MoE-layer tokens/s of the EC2MoE hot path on one MI355X.
+
+One step is the whole path on one batch: route X with the hardware-aware group gate,
+compress it with the low-rank encoder, reconstruct it with the decoder, and run the
+sparse SwiGLU MoE layer on the reconstruction with the gate's routing (permute,
+grouped expert GEMMs, combine). Inputs are seeded synthetic tensors of the workload's
+shape, resident in HBM before timing. Default workload: the Mixtral-shaped layer
+(T=4096 tokens, d=4096, 8 experts in 2 groups, SwiGLU hidden 14336, top-2, codec
+rank 256).
+
+Prints one JSON line with tokens/s, the per-kernel HIP-event timing of the timed
+region, the roofline of the dominant kernel, and the CPU oracle timed on a bounded
+sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    from paper_2508_06024_amd.workload import CONFIG_ORDER
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 50; 1000 for 'decode')")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mixtral", choices=CONFIG_ORDER)
+    ap.add_argument("--rotate", type=int, default=4, help="distinct copies of X cycled through the steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="after timing, run one plain device copy of this many MiB (counter calibration)")
+    return ap.parse_args()
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = [p["num_threads"] for p in threadpool_info() if p.get("user_api") == "blas"]
+        return max(n) if n else 1
+    except Exception:
+        return 1
+
+
+def cpu_baseline(inp, cfg, target_s):
+    """The oracle's step (gate, encode, decode, experts, combine) on the first S tokens,
+    with U restricted to those rows; weights are upcast to float64 before timing."""
+    import oracle as O
+    from paper_2508_06024_amd import workload as W
+    f = inp.f64
+    x, u, v = f("x"), f("u"), f("v")
+    wg, wl = f("w_global"), f("w_local")
+    gu = [W.to_f64(inp.w_gate_up[e], cfg.dtype) for e in range(cfg.n_experts)]
+    dn = [W.to_f64(inp.w_down[e], cfg.dtype) for e in range(cfg.n_experts)]
+
+    def run(S):
+        t = time.perf_counter()
+        O.layer(x[:S], inp.mask, wg, inp.b_global, wl, inp.b_local, gu, dn, u[:S], v, u[:S], v,
+                cfg.n_groups, cfg.top_k)
+        return time.perf_counter() - t
+
+    T = cfg.n_tokens
+    S0 = min(T, max(cfg.r_h, 64))
+    t0 = run(S0)
+    S = int(min(T, max(S0, S0 * target_s / max(t0, 1e-6))))
+    S = max(cfg.r_h, (S // 64) * 64) if S < T else T
+    t = run(S) if S != S0 else t0
+    return {"value": S / t, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": f"oracle step (gate, encode, decode, experts, combine) on the first {S} of {T} tokens "
+                      f"of the same inputs, U restricted to those rows, float64, {t:.1f} s",
+            "seconds": round(t, 2)}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        log("bench.py measures one GPU: this implementation has no multi-GPU path "
+            "(the token-sharded design is described in DESIGN.md); run with --gpus 1")
+        sys.exit(2)
+
+    import torch
+    from paper_2508_06024_amd import ec2moe as E
+    from paper_2508_06024_amd import roofline as R
+    from paper_2508_06024_amd import workload as W
+    from paper_2508_06024_amd.layer import Ec2moeLayer
+
+    cfg = W.CONFIGS[args.workload]
+    per_call = cfg.mask == "per_call"
+    steps = args.steps or (cfg.n_calls if per_call else 50)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    t_gen = time.perf_counter()
+    inp = W.gen_layer(cfg)
+    log(f"[bench] {cfg.name}: inputs generated in {time.perf_counter() - t_gen:.1f} s")
+
+    def up(a):
+        if cfg.dtype == W.BF16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+    if per_call:
+        calls = [W.gen_call(cfg, s) for s in range(cfg.first_call_seed, cfg.first_call_seed + min(steps, cfg.n_calls))]
+        xs = [up(c[0]) for c in calls]
+        masks = [c[1] for c in calls]
+    else:
+        xs = [up(inp.x) for _ in range(max(1, args.rotate))]
+        masks = [inp.mask]
+    layer = Ec2moeLayer(xs[0], masks[0], up(inp.w_global), f32(inp.b_global), up(inp.w_local), f32(inp.b_local),
+                        up(inp.w_gate_up), up(inp.w_down), up(inp.u), up(inp.v),
+                        n_groups=cfg.n_groups, top_k=cfg.top_k)
+
+    def step(i):
+        layer.set_input(xs[i % len(xs)], masks[i % len(masks)])
+        layer.step()
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # timed region, with the library's per-kernel HIP events on the same stream
+    E.profile_enable(True)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        step(i)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end)
+    stats = E.profile_collect()
+    E.profile_enable(False)
+    ms_step = ms / steps
+    tokens_s = cfg.n_tokens * steps / (ms / 1e3)
+    log(f"[bench] {steps} steps in {ms:.2f} ms: {ms_step:.3f} ms/step, {tokens_s:.4g} tokens/s")
+
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.calibrate_copy_mib} MiB done")
+        del a, b
+
+    # per-kernel algorithmic work at the realised routing
+    idx = layer.topk_idx.cpu().numpy()
+    work = R.kernel_work(cfg, R.expert_rows(idx, cfg.n_experts))
+    group = {"perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
+             "transpose": "encode", "codec_xv": "encode", "codec_utp": "encode", "codec_utp_reduce": "encode",
+             "codec_vzt": "decode", "codec_vzt_reduce": "decode", "codec_uw": "decode"}
+    peak_f = R.PEAK_TFLOPS[cfg.dtype]
+    kernels = {}
+    for name, (n, tot) in stats.items():
+        kernels[name] = {"launches_per_step": n / steps, "avg_us": round(1e3 * tot / n, 2)}
+    rows = {}
+    for name, (n, tot) in stats.items():
+        g = group.get(name, name)
+        rows.setdefault(g, [0.0, 0])
+        rows[g][0] += tot / steps  # ms per step
+        rows[g][1] += n / steps
+    step_roof_ms = 0.0
+    for g, (ms_g, _) in rows.items():
+        if g in work:
+            flop, byt = work[g]
+            t_f = flop / (peak_f * 1e12) * 1e3
+            t_b = byt / (R.PEAK_HBM_GBS * 1e9) * 1e3
+            step_roof_ms += max(t_f, t_b)
+            bound = "mfma" if t_f >= t_b else "hbm"
+            ach = flop / (ms_g * 1e-3) / 1e12 if bound == "mfma" else byt / (ms_g * 1e-3) / 1e9
+            peak = peak_f if bound == "mfma" else R.PEAK_HBM_GBS
+            for name in stats:
+                if group.get(name, name) == g:
+                    kernels[name]["stage"] = g
+            kernels.setdefault(f"stage:{g}", {})
+            kernels[f"stage:{g}"] = {"ms_per_step": round(ms_g, 4), "bound": bound, "achieved": round(ach, 1),
+                                     "unit": "TFLOP/s" if bound == "mfma" else "GB/s", "frac": round(ach / peak, 4)}
+
+    dom = max((n for n in stats if n in work), key=lambda n: stats[n][1])
+    n_l, tot = stats[dom]
+    avg_s = tot / n_l * 1e-3
+    flop, byt = work[dom]
+    bound = "mfma" if flop / (peak_f * 1e12) >= byt / (R.PEAK_HBM_GBS * 1e9) else "hbm"
+    if bound == "mfma":
+        achieved, peak, unit = flop / avg_s / 1e12, peak_f, "TFLOP/s"
+    else:
+        achieved, peak, unit = byt / avg_s / 1e9, R.PEAK_HBM_GBS, "GB/s"
+    traffic = R.measured_traffic(dom, cfg.name)
+    roof = {"kernel": dom, "bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": traffic,
+            "algorithmic": {"flop": flop, "bytes": byt}, "avg_launch_us": round(avg_s * 1e6, 1)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample ...")
+        cpu = cpu_baseline(inp, cfg, args.cpu_seconds)
+        log(f"[bench] oracle: {cpu['value']:.4g} tokens/s on {cpu['cores']} threads")
+
+    out = {
+        "metric": "MoE-layer tokens/s incl. group gate + low-rank codec",
+        "value": round(tokens_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: T={cfg.n_tokens} d={cfg.d_model} experts={cfg.n_experts} "
+                               f"groups={cfg.n_groups} SwiGLU H={cfg.ffn_hidden} top-{cfg.top_k} "
+                               f"codec {cfg.r_h}x{cfg.r_w}, mask={cfg.mask}",
+                   "tokens_per_step": cfg.n_tokens},
+        "roofline": roof,
+        "layer_roofline_frac": round(step_roof_ms / ms_step, 4),
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

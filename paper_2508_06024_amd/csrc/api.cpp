@@ -314,13 +314,13 @@ hipError_t run_experts(const ec2moe_moe_desc* desc, const void* x, const int32_t
     GemmArgs g1{};
     g1.tok = x; g1.row_index = perm_src; g1.w = w_gate_up;
     g1.w_group_stride = int64_t(2) * H * d; g1.seg = seg; g1.n_groups = desc->n_experts;
-    g1.rows = A; g1.K = d; g1.N = H; g1.out = act; g1.ldo = H;
+    g1.rows = A; g1.K = d; g1.N = H; g1.out = act; g1.ldo = H; g1.name = "expert_gate_up";
     hipError_t e = launch_gemm(dt, Epilogue::SwiGLU, OutType::Same, g1, stream);
     if (e != hipSuccess) return e;
     GemmArgs g2{};
     g2.tok = act; g2.row_index = nullptr; g2.w = w_down;
     g2.w_group_stride = int64_t(d) * H; g2.seg = seg; g2.n_groups = desc->n_experts;
-    g2.rows = A; g2.K = H; g2.N = d; g2.out = y_perm; g2.ldo = d;
+    g2.rows = A; g2.K = H; g2.N = d; g2.out = y_perm; g2.ldo = d; g2.name = "expert_down";
     return launch_gemm(dt, Epilogue::Store, OutType::Same, g2, stream);
 }
 
@@ -405,7 +405,7 @@ ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x
         // P = X V  [h][r_w], float32
         GemmArgs g{};
         g.tok = xc; g.row_index = nullptr; g.w = vt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
-        g.rows = desc->h; g.K = desc->w; g.N = desc->r_w; g.out = p; g.ldo = desc->r_w;
+        g.rows = desc->h; g.K = desc->w; g.N = desc->r_w; g.out = p; g.ldo = desc->r_w; g.name = "codec_xv";
         e = launch_gemm(dt, Epilogue::Store, OutType::F32, g, stream);
         if (e != hipSuccess) break;
         // Z = U^T P  [r_h][r_w]: A(m,k) = U[k][m], B(k,n) = P[k][n]
@@ -414,7 +414,7 @@ ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x
         s.b = p; s.b_dt = DType::F32; s.b_sk = desc->r_w; s.b_sn = 1;
         s.M = desc->r_h; s.N = desc->r_w; s.K = desc->h;
         s.out = z + static_cast<size_t>(c) * desc->r_h * desc->r_w; s.out_dt = DType::F32;
-        s.part = at<float>(ws, w.epart); s.splits = w.enc_splits;
+        s.part = at<float>(ws, w.epart); s.splits = w.enc_splits; s.name = "codec_utp";
         e = launch_small_gemm(s, stream);
     }
     return hip_status(e, "lowrank_encode launch");
@@ -440,7 +440,7 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
         s.b = z + static_cast<size_t>(c) * desc->r_h * desc->r_w; s.b_dt = DType::F32; s.b_sk = 1; s.b_sn = desc->r_w;
         s.M = desc->w; s.N = desc->r_h; s.K = desc->r_w;
         s.out = wt; s.out_dt = dt;
-        s.part = at<float>(ws, w.dpart); s.splits = w.dec_splits;
+        s.part = at<float>(ws, w.dpart); s.splits = w.dec_splits; s.name = "codec_vzt";
         e = launch_small_gemm(s, stream);
         if (e != hipSuccess) break;
         // X_hat = U_hat Wt^T  [h][w]
@@ -448,6 +448,7 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
         g.tok = u_hat; g.row_index = nullptr; g.w = wt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
         g.rows = desc->h; g.K = desc->r_h; g.N = desc->w;
         g.out = static_cast<char*>(x_hat) + static_cast<size_t>(c) * desc->h * desc->w * eb; g.ldo = desc->w;
+        g.name = "codec_uw";
         e = launch_gemm(dt, Epilogue::Store, OutType::Same, g, stream);
     }
     return hip_status(e, "lowrank_decode launch");

@@ -10,6 +10,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <string>
 
 namespace ec2moe {
 namespace {
@@ -107,14 +108,15 @@ template <typename TA, typename TB>
 hipError_t small_gemm_t(const SmallGemmArgs& g, hipStream_t s) {
     dim3 grid((g.M + kT - 1) / kT, (g.N + kT - 1) / kT, g.splits);
     {
-        ProfileScope prof("small_gemm", s);
+        ProfileScope prof(g.name ? g.name : "small_gemm", s);
         hipLaunchKernelGGL((small_gemm_kernel<TA, TB>), grid, dim3(256), 0, s, g);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t mn = static_cast<int64_t>(g.M) * g.N;
     const int rgrid = static_cast<int>(std::min<int64_t>((mn + 255) / 256, 4096));
-    ProfileScope prof("split_reduce", s);
+    std::string rname = std::string(g.name ? g.name : "small_gemm") + "_reduce";
+    ProfileScope prof(rname.c_str(), s);
     if (g.out_dt == DType::BF16)
         hipLaunchKernelGGL(split_reduce_kernel<bf16_t>, dim3(rgrid), dim3(256), 0, s, g.part, mn, g.splits,
                            static_cast<bf16_t*>(g.out));

@@ -266,13 +266,13 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
 }
 
 template <typename T, typename TO, int TM, int TN, int WM, int WN, bool SWIGLU>
-hipError_t run(const GemmArgs& a, const char* name, hipStream_t s) {
+hipError_t run(const GemmArgs& a, hipStream_t s) {
     constexpr int NOUT = SWIGLU ? TN / 2 : TN;
     const int ntn = (a.N + NOUT - 1) / NOUT;
     int64_t mtiles = a.seg ? (a.rows + TM - 1) / TM + a.n_groups : (a.rows + TM - 1) / TM;
     const int64_t grid = mtiles * ntn;
     if (grid == 0) return hipSuccess;
-    ProfileScope prof(name, s);
+    ProfileScope prof(a.name ? a.name : "gemm", s);
     hipLaunchKernelGGL((gemm_kernel<T, TO, TM, TN, WM, WN, SWIGLU>), dim3(static_cast<unsigned>(grid)), dim3(256), 0,
                        s, a);
     return hipGetLastError();
@@ -294,11 +294,11 @@ Tile choose_tile(const GemmArgs& a, bool swiglu) {
 }
 
 template <typename T, typename TO, bool SWIGLU>
-hipError_t dispatch(const GemmArgs& a, const char* name, hipStream_t s) {
+hipError_t dispatch(const GemmArgs& a, hipStream_t s) {
     switch (choose_tile(a, SWIGLU)) {
-        case Tile::Big: return run<T, TO, 256, 256, 2, 2, SWIGLU>(a, name, s);
-        case Tile::Mid: return run<T, TO, 128, 128, 2, 2, SWIGLU>(a, name, s);
-        default: return run<T, TO, 32, 128, 1, 4, SWIGLU>(a, name, s);
+        case Tile::Big: return run<T, TO, 256, 256, 2, 2, SWIGLU>(a, s);
+        case Tile::Mid: return run<T, TO, 128, 128, 2, 2, SWIGLU>(a, s);
+        default: return run<T, TO, 32, 128, 1, 4, SWIGLU>(a, s);
     }
 }
 
@@ -307,12 +307,12 @@ hipError_t dispatch(const GemmArgs& a, const char* name, hipStream_t s) {
 hipError_t launch_gemm(DType dt, Epilogue epi, OutType ot, const GemmArgs& a, hipStream_t s) {
     const bool sw = epi == Epilogue::SwiGLU;
     if (dt == DType::BF16) {
-        if (sw) return dispatch<bf16_t, bf16_t, true>(a, "gemm_swiglu", s);
-        if (ot == OutType::F32) return dispatch<bf16_t, float, false>(a, "gemm_f32out", s);
-        return dispatch<bf16_t, bf16_t, false>(a, "gemm", s);
+        if (sw) return dispatch<bf16_t, bf16_t, true>(a, s);
+        if (ot == OutType::F32) return dispatch<bf16_t, float, false>(a, s);
+        return dispatch<bf16_t, bf16_t, false>(a, s);
     }
-    if (sw) return dispatch<float, float, true>(a, "gemm_swiglu", s);
-    return dispatch<float, float, false>(a, "gemm", s);
+    if (sw) return dispatch<float, float, true>(a, s);
+    return dispatch<float, float, false>(a, s);
 }
 
 }  // namespace ec2moe

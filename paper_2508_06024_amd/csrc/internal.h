@@ -70,6 +70,7 @@ struct GemmArgs {
     int N;                    // output columns
     void* out;                // [rows][N]
     int64_t ldo;              // output row stride (elements)
+    const char* name;         // kernel name for the timing record
 };
 hipError_t launch_gemm(DType dt, Epilogue epi, OutType ot, const GemmArgs& a, hipStream_t s);
 
@@ -91,6 +92,7 @@ struct SmallGemmArgs {
     int M, N, K;
     void* out; DType out_dt;
     float* part; int splits;
+    const char* name;         // kernel name for the timing record (the reduction adds "_reduce")
 };
 hipError_t launch_small_gemm(const SmallGemmArgs& g, hipStream_t s);
 

@@ -1,0 +1,63 @@
+"""Algorithmic work of each kernel of the step, and MI355X peaks.
+
+Counts are what the method must compute or move (no padding, no re-reads): bf16 or
+fp32 operands read once, intermediates written once and read once, weights of the
+experts that received at least one row read once.
+"""
+from __future__ import annotations
+
+import hashlib
+import json
+import os
+
+import numpy as np
+
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_ROOT = os.path.dirname(_HERE)
+
+
+def expert_rows(idx: np.ndarray, n_experts: int) -> np.ndarray:
+    return np.bincount(np.asarray(idx).ravel(), minlength=n_experts)
+
+
+def kernel_work(cfg, rows_per_expert: np.ndarray) -> dict:
+    """{kernel: (flop, bytes)} for one step of the layer at this routing."""
+    s = 2 if cfg.dtype == "bf16" else 4
+    T, d, M, K, H, k = cfg.n_tokens, cfg.d_model, cfg.n_experts, cfg.n_groups, cfg.ffn_hidden, cfg.top_k
+    A = T * k
+    act = int(np.count_nonzero(rows_per_expert))
+    rh, rw = cfg.r_h, cfg.r_w
+    return {
+        "gate": (2.0 * T * d * (M + K), T * d * s + (M + K) * d * s + 8.0 * T * k),
+        "expert_gate_up": (4.0 * A * d * H, act * 2.0 * H * d * s + A * d * s + A * H * s),
+        "expert_down": (2.0 * A * H * d, act * 1.0 * d * H * s + A * H * s + A * d * s),
+        "combine": (2.0 * A * d, A * d * s + 8.0 * T * k + T * d * s),
+        "permute": (0.0, 4.0 * A + 12.0 * A),
+        "encode": (2.0 * T * d * rw + 2.0 * rh * rw * T, T * d * s + (T * rh + d * rw) * s + 4.0 * rh * rw),
+        "decode": (2.0 * d * rw * rh + 2.0 * T * rh * d, T * d * s + (T * rh + d * rw) * s + 4.0 * rh * rw),
+    }
+
+
+def source_digest(*names: str) -> str:
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(_HERE, "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch recorded from rocprofv3 counters for this kernel and
+    workload, or None if absent or taken on a different kernel source."""
+    path = os.path.join(_ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_digest") != source_digest(*rec.get("sources", [])):
+        return None
+    return rec.get("hbm_bytes_per_launch")
