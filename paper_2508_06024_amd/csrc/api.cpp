@@ -76,11 +76,12 @@ ec2moe_status check_moe_desc(const ec2moe_moe_desc* d) {
     REQUIRE(d->d_model % 128 == 0, EC2MOE_ERR_UNSUPPORTED, "d_model %d is not a multiple of 128", d->d_model);
     REQUIRE(d->ffn_hidden % 128 == 0, EC2MOE_ERR_UNSUPPORTED, "ffn_hidden %d is not a multiple of 128",
             d->ffn_hidden);
-    // 32-bit element offsets inside one operand of the GEMM
+    // 32-bit byte offsets inside one operand of the GEMM
     const int64_t A = static_cast<int64_t>(d->n_tokens) * d->top_k;
-    REQUIRE(A * std::max(d->d_model, d->ffn_hidden) < (int64_t(1) << 32) &&
-                int64_t(2) * d->ffn_hidden * d->d_model < (int64_t(1) << 32),
-            EC2MOE_ERR_UNSUPPORTED, "tensor too large for 32-bit element offsets");
+    const int64_t eb = d->dtype == EC2MOE_F32 ? 4 : 2;
+    REQUIRE(A * std::max(d->d_model, d->ffn_hidden) * eb < (int64_t(1) << 32) &&
+                int64_t(2) * d->ffn_hidden * d->d_model * eb < (int64_t(1) << 32),
+            EC2MOE_ERR_UNSUPPORTED, "tensor too large for 32-bit byte offsets");
     return EC2MOE_OK;
 }
 
@@ -131,8 +132,8 @@ ec2moe_status check_codec_desc(const ec2moe_codec_desc* d) {
     REQUIRE(d->w % 128 == 0, EC2MOE_ERR_UNSUPPORTED, "w %d is not a multiple of 128", d->w);
     REQUIRE(d->r_h % 16 == 0 && d->r_w % 16 == 0 && d->r_h <= 256 && d->r_w <= 256, EC2MOE_ERR_UNSUPPORTED,
             "r_h and r_w must be multiples of 16 and at most 256");
-    REQUIRE(static_cast<int64_t>(d->h) * d->w < (int64_t(1) << 32), EC2MOE_ERR_UNSUPPORTED,
-            "slice too large for 32-bit element offsets");
+    REQUIRE(static_cast<int64_t>(d->h) * d->w * (d->dtype == EC2MOE_F32 ? 4 : 2) < (int64_t(1) << 32),
+            EC2MOE_ERR_UNSUPPORTED, "slice too large for 32-bit byte offsets");
     return EC2MOE_OK;
 }
 
@@ -315,12 +316,14 @@ hipError_t run_experts(const ec2moe_moe_desc* desc, const void* x, const int32_t
     g1.tok = x; g1.row_index = perm_src; g1.w = w_gate_up;
     g1.w_group_stride = int64_t(2) * H * d; g1.seg = seg; g1.n_groups = desc->n_experts;
     g1.rows = A; g1.K = d; g1.N = H; g1.out = act; g1.ldo = H; g1.name = "expert_gate_up";
+    g1.src_rows = desc->n_tokens; g1.w_rows = int64_t(2) * H;
     hipError_t e = launch_gemm(dt, Epilogue::SwiGLU, OutType::Same, g1, stream);
     if (e != hipSuccess) return e;
     GemmArgs g2{};
     g2.tok = act; g2.row_index = nullptr; g2.w = w_down;
     g2.w_group_stride = int64_t(d) * H; g2.seg = seg; g2.n_groups = desc->n_experts;
     g2.rows = A; g2.K = H; g2.N = d; g2.out = y_perm; g2.ldo = d; g2.name = "expert_down";
+    g2.src_rows = A; g2.w_rows = d;
     return launch_gemm(dt, Epilogue::Store, OutType::Same, g2, stream);
 }
 
@@ -406,6 +409,7 @@ ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x
         GemmArgs g{};
         g.tok = xc; g.row_index = nullptr; g.w = vt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
         g.rows = desc->h; g.K = desc->w; g.N = desc->r_w; g.out = p; g.ldo = desc->r_w; g.name = "codec_xv";
+        g.src_rows = desc->h; g.w_rows = desc->r_w;
         e = launch_gemm(dt, Epilogue::Store, OutType::F32, g, stream);
         if (e != hipSuccess) break;
         // Z = U^T P  [r_h][r_w]: A(m,k) = U[k][m], B(k,n) = P[k][n]
@@ -449,6 +453,7 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
         g.rows = desc->h; g.K = desc->r_h; g.N = desc->w;
         g.out = static_cast<char*>(x_hat) + static_cast<size_t>(c) * desc->h * desc->w * eb; g.ldo = desc->w;
         g.name = "codec_uw";
+        g.src_rows = desc->h; g.w_rows = desc->w;
         e = launch_gemm(dt, Epilogue::Store, OutType::Same, g, stream);
     }
     return hip_status(e, "lowrank_decode launch");

@@ -6,16 +6,27 @@
 // weights), which is the layout the expert networks of Eq. 1 and the codec products use.
 // Groups are the per-expert segments produced by the permutation; their sizes stay on
 // the device. The grid is sized for the upper bound sum_e ceil(n_e / TM) <= ceil(rows/TM)
-// + groups, and every workgroup finds its (expert, m-tile, n-tile) with a wave-parallel
-// prefix sum over the segment table; surplus workgroups exit.
+// + groups; every workgroup counts the real tiles with a wave-parallel prefix sum over
+// the segment table, maps its id to a tile, and surplus workgroups exit.
+//
+// Tile order (XCD-aware): workgroups are dispatched round-robin over the 8 XCDs, each with
+// its own L2. Workgroup p runs logical tile (p % 8) * ceil(tiles / 8) + p / 8, so every XCD
+// walks one contiguous stretch of the logical order, in which the m-tiles of one n-tile
+// (sharing the same weight rows) are consecutive: a weight slab is fetched into one L2
+// and reused there.
 //
 // Workgroup tile: TM token rows x TN weight rows, 4 waves in a WM x WN grid. Each K-step
-// moves one 128-byte slab of every tile row (64 bf16 or 32 fp32 values) global -> LDS,
-// double-buffered so the next slab's loads are in flight during the matrix-core work on
-// the current one. LDS rows are 8 chunks of 16 bytes stored at chunk ^ (row & 7), which
-// keeps both the 16-byte stores and the 16-byte fragment reads free of bank conflicts.
-// Weight rows feed the MFMA A operand and token rows the B operand, so every lane ends
-// with 4 consecutive output columns of one token row (one 8- or 16-byte store).
+// moves one 128-byte slab of every tile row (64 bf16 or 32 fp32 values) into LDS, double
+// buffered. LDS rows are 8 chunks of 16 bytes stored at chunk ^ (row & 7), which keeps
+// the 16-byte fragment reads free of bank conflicts. Weight rows feed the MFMA A operand
+// and token rows the B operand, so every lane ends with 4 consecutive output columns of
+// one token row (one 8- or 16-byte store).
+//
+// Two mainloops:
+//   * gemm_lds_kernel (bf16, K a multiple of 128, 32x32x16 MFMA): buffer loads write the
+//     slabs straight into LDS (no register staging); fragment reads run ahead of the MFMAs;
+//   * gemm_kernel (any K that is a multiple of the 16-byte chunk, bf16 or fp32): loads
+//     through registers, zero-filling chunks past K.
 //
 // SwiGLU epilogue: the weight tile holds TN/2 gate rows followed by the matching TN/2 up
 // rows; each wave owns equal gate and up slices, so silu(gate) * up is formed in registers.
@@ -23,9 +34,20 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace ec2moe {
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+// buffer_load_dwordx4 ... lds: each lane's 16 bytes land at M0 + 16 * lane
+__device__ void raw_buffer_load_lds(i32x4 rsrc, lds_void* lds, int size, int voffset, int soffset, int offset,
+                                    int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+
 namespace {
+
+constexpr int kXcds = 8;
 
 struct TileInfo {
     int group;
@@ -34,21 +56,44 @@ struct TileInfo {
     int nt;        // n-tile index
 };
 
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 // Finds the tile of this workgroup; false if the workgroup has no tile.
 template <int TM>
 __device__ __forceinline__ bool find_tile(const GemmArgs& a, int ntn, TileInfo& ti) {
-    const int bid = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    // real tiles
+    int total;
     if (a.seg == nullptr) {
-        const int64_t mtiles = (a.rows + TM - 1) / TM;
-        if (bid >= mtiles * ntn) return false;
-        const int64_t mt = bid % mtiles;
+        total = static_cast<int>((a.rows + TM - 1) / TM) * ntn;
+    } else {
+        int t = 0;
+        for (int e0 = 0; e0 < a.n_groups; e0 += 64) {
+            const int e = e0 + lane;
+            int cnt = 0;
+            if (e < a.n_groups) cnt = ((a.seg[e + 1] - a.seg[e] + TM - 1) / TM) * ntn;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off);
+            t += cnt;
+        }
+        total = t;
+    }
+    total = uniform(total);
+    const int per_xcd = (total + kXcds - 1) / kXcds;
+    const int p = blockIdx.x;
+    const int j = p / kXcds;
+    const int bid = (p % kXcds) * per_xcd + j;
+    if (j >= per_xcd || bid >= total) return false;
+
+    if (a.seg == nullptr) {
+        const int mtiles = static_cast<int>((a.rows + TM - 1) / TM);
+        const int mt = bid % mtiles;
         ti.group = 0;
-        ti.nt = static_cast<int>(bid / mtiles);
-        ti.row0 = mt * TM;
+        ti.nt = bid / mtiles;
+        ti.row0 = static_cast<int64_t>(mt) * TM;
         ti.valid = static_cast<int>(std::min<int64_t>(TM, a.rows - ti.row0));
         return true;
     }
-    const int lane = threadIdx.x & 63;
     int base = 0;
     for (int e0 = 0; e0 < a.n_groups; e0 += 64) {
         const int e = e0 + lane;
@@ -69,11 +114,11 @@ __device__ __forceinline__ bool find_tile(const GemmArgs& a, int ntn, TileInfo& 
         if (hits) {
             const int src = __ffsll(static_cast<long long>(hits)) - 1;
             const int first = base + __shfl(inc - cnt, src);
-            const int glo = __shfl(lo, src);
-            const int ghi = __shfl(hi, src);
+            const int glo = uniform(__shfl(lo, src));
+            const int ghi = uniform(__shfl(hi, src));
             const int mtiles = (ghi - glo + TM - 1) / TM;
-            const int local = bid - first;
-            ti.group = e0 + src;
+            const int local = uniform(bid - first);
+            ti.group = uniform(e0 + src);
             ti.nt = local / mtiles;
             const int mt = local - ti.nt * mtiles;
             ti.row0 = glo + static_cast<int64_t>(mt) * TM;
@@ -102,6 +147,59 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* dst, f32x4 v) {
     o.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
     *reinterpret_cast<uint2*>(dst) = o;
 }
+
+// LDS row (within the weight part of the tile) of fragment block ni of wave column wn.
+template <int TN, int WN, int NI, bool SWIGLU>
+__device__ __forceinline__ int weight_frag_row(int wn, int ni, int l16) {
+    if (SWIGLU) {
+        constexpr int HALF = NI / 2;
+        const int part = ni < HALF ? 0 : TN / 2;
+        return part + wn * (TN / 2 / WN) + (ni % HALF) * 16 + l16;
+    }
+    return wn * (TN / WN) + ni * 16 + l16;
+}
+
+// Writes the wave's accumulators: lane holds token row wm*(TM/WM) + mi*16 + l16 and weight
+// rows 4*lg .. 4*lg+3 of each 16x16 block.
+template <typename TO, int TM, int TN, int WM, int WN, int MI, int NI, bool SWIGLU>
+__device__ __forceinline__ void write_tile(const GemmArgs& a, const TileInfo& ti, int wm, int wn, int lane,
+                                           const f32x4 (&acc)[NI][MI]) {
+    const int l16 = lane & 15;
+    const int lg = lane >> 4;
+    TO* out = static_cast<TO*>(a.out);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+        const int trow = wm * (TM / WM) + mi * 16 + l16;
+        if (trow >= ti.valid) continue;
+        TO* orow = out + (ti.row0 + trow) * a.ldo;
+        if (SWIGLU) {
+            constexpr int HALF = NI / 2;
+#pragma unroll
+            for (int ni = 0; ni < HALF; ++ni) {
+                const int col = ti.nt * (TN / 2) + wn * (TN / 2 / WN) + ni * 16 + 4 * lg;
+                f32x4 v;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v[i] = silu(acc[ni][mi][i]) * acc[ni + HALF][mi][i];
+                store4<TO>(orow + col, v);
+            }
+        } else {
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+                const int col = ti.nt * TN + wn * (TN / WN) + ni * 16 + 4 * lg;
+                if (col < a.N) store4<TO>(orow + col, acc[ni][mi]);
+            }
+        }
+    }
+}
+
+// Weight row (within the group's weight matrix) of tile row n.
+template <int TN, bool SWIGLU>
+__device__ __forceinline__ int weight_row(const GemmArgs& a, int nt, int n) {
+    if (SWIGLU) return n < TN / 2 ? nt * (TN / 2) + n : a.N + nt * (TN / 2) + (n - TN / 2);
+    return std::min(nt * TN + n, a.N - 1);
+}
+
+// ------------------------------------------------------------------ register-staged mainloop
 
 template <typename T, typename TO, int TM, int TN, int WM, int WN, bool SWIGLU>
 __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
@@ -146,13 +244,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < W_PASSES; ++i) {
-        const int n = rr + 32 * i;
-        int wrow;
-        if (SWIGLU) {
-            wrow = n < TN / 2 ? ti.nt * (TN / 2) + n : a.N + ti.nt * (TN / 2) + (n - TN / 2);
-        } else {
-            wrow = std::min(ti.nt * TN + n, a.N - 1);
-        }
+        const int wrow = weight_row<TN, SWIGLU>(a, ti.nt, rr + 32 * i);
         w_off[i] = static_cast<uint32_t>(static_cast<int64_t>(wrow) * K + c * EPC);
     }
 
@@ -180,7 +272,6 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
         }
     };
 
-    // ---- fragment rows of this wave
     const int l16 = lane & 15;
     const int lg = lane >> 4;
     int frag_t[MI];
@@ -188,17 +279,7 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) frag_t[mi] = wm * (TM / WM) + mi * 16 + l16;
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni) {
-        int wr;
-        if (SWIGLU) {
-            constexpr int HALF = NI / 2;
-            const int part = ni < HALF ? 0 : TN / 2;
-            wr = part + wn * (TN / 2 / WN) + (ni % HALF) * 16 + l16;
-        } else {
-            wr = wn * (TN / WN) + ni * 16 + l16;
-        }
-        frag_w[ni] = TM + wr;
-    }
+    for (int ni = 0; ni < NI; ++ni) frag_w[ni] = TM + weight_frag_row<TN, WN, NI, SWIGLU>(wn, ni, l16);
 
     f32x4 acc[NI][MI];
 #pragma unroll
@@ -237,43 +318,284 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
         __syncthreads();
     }
 
-    // ---- epilogue: lane holds token row frag_t[mi] (col l16 of the MFMA output) and
-    // weight rows 4*lg .. 4*lg+3 of each block
+    write_tile<TO, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+}
+
+// ------------------------------------------------------------------ direct-to-LDS mainloop
+
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t p = reinterpret_cast<uint64_t>(base);
+    i32x4 r;
+    r[0] = uniform(static_cast<int>(static_cast<uint32_t>(p)));
+    r[1] = uniform(static_cast<int>(static_cast<uint32_t>(p >> 32)));
+    r[2] = uniform(static_cast<int>(bytes));
+    r[3] = 0x00020000;  // raw (untyped, unswizzled) buffer of the gfx9 family
+    return r;
+}
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Writes a wave's 32x32-block accumulators. After v_mfma_f32_32x32x16 with weight rows as A
+// and token rows as B, lane l holds token row (l % 32) of the block and, in register r,
+// weight row 8*(r/4) + 4*(l/32) + r%4: four runs of 4 consecutive output columns.
+template <typename TO, int TM, int TN, int WM, int WN, int MI, int NI, bool SWIGLU>
+__device__ __forceinline__ void write_tile32(const GemmArgs& a, const TileInfo& ti, int wm, int wn, int lane,
+                                             const f32x16 (&acc)[NI][MI]) {
+    const int l32 = lane & 31;
+    const int lh = lane >> 5;
     TO* out = static_cast<TO*>(a.out);
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) {
-        const int trow = wm * (TM / WM) + mi * 16 + l16;
+        const int trow = wm * (TM / WM) + mi * 32 + l32;
         if (trow >= ti.valid) continue;
         TO* orow = out + (ti.row0 + trow) * a.ldo;
         if (SWIGLU) {
             constexpr int HALF = NI / 2;
 #pragma unroll
             for (int ni = 0; ni < HALF; ++ni) {
-                const int col = ti.nt * (TN / 2) + wn * (TN / 2 / WN) + ni * 16 + 4 * lg;
-                f32x4 v;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) v[i] = silu(acc[ni][mi][i]) * acc[ni + HALF][mi][i];
-                store4<TO>(orow + col, v);
+                for (int q = 0; q < 4; ++q) {
+                    const int col = ti.nt * (TN / 2) + wn * (TN / 2 / WN) + ni * 32 + 8 * q + 4 * lh;
+                    f32x4 v;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] = silu(acc[ni][mi][4 * q + i]) * acc[ni + HALF][mi][4 * q + i];
+                    store4<TO>(orow + col, v);
+                }
             }
         } else {
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) {
-                const int col = ti.nt * TN + wn * (TN / WN) + ni * 16 + 4 * lg;
-                if (col < a.N) store4<TO>(orow + col, acc[ni][mi]);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int col = ti.nt * TN + wn * (TN / WN) + ni * 32 + 8 * q + 4 * lh;
+                    f32x4 v;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] = acc[ni][mi][4 * q + i];
+                    if (col < a.N) store4<TO>(orow + col, v);
+                }
             }
         }
     }
 }
 
+// bf16 mainloop on 32x32x16 matrix-core blocks (the full-rate bf16 MFMA shape on gfx950).
+//
+// K advances in slabs of 64 (one 128-byte row per tile row) through two LDS stages; the
+// buffer loads of slab ks + 1 fly while slab ks is consumed. Each stage is its own LDS
+// object and the K loop is unrolled by two, so every access names its stage at compile
+// time (fragment reads of one stage then need not wait for loads landing in the other).
+// LDS rows are 8 chunks of 16 bytes, chunk c of row r stored at c ^ ((r >> 1) & 7): a
+// 16-lane group of ds_read_b128 reading one chunk of 16 consecutive rows touches all 64
+// banks once, and the buffer loads write 1 KB contiguous runs.
+// Within a slab of 4 k-steps, fragment reads run one k-step ahead of the MFMAs; the
+// MFMAs of a slab's last k-step are deferred past the next barrier, where they cover the
+// latency of the next slab's first reads.
+template <int TM, int TN, int WM, int WN, bool SWIGLU>
+__global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
+    static_assert(WM * WN == 4, "4 waves per workgroup");
+    constexpr int MI = TM / WM / 32;           // token blocks of 32 per wave
+    constexpr int NI = TN / WN / 32;           // weight blocks of 32 per wave
+    constexpr int NOUT = SWIGLU ? TN / 2 : TN;
+    constexpr int ROWS = TM + TN;
+    constexpr int RB = 128;                    // bytes per tile row per slab (64 bf16)
+    constexpr int STAGE = ROWS * RB;
+    constexpr int WROWS = ROWS / 4;            // tile rows loaded by each wave
+    constexpr int LOADS = WROWS / 8;           // 8-row load instructions per wave per slab
+    static_assert(MI >= 1 && NI >= 1, "wave tile of at least one 32x32 block");
+    static_assert(WROWS % 8 == 0 && TM % WROWS == 0, "each wave loads only token or only weight rows");
+    static_assert(!SWIGLU || NI % 2 == 0, "SwiGLU waves hold matching gate/up blocks");
+
+    __shared__ __attribute__((aligned(1024))) char lds0[STAGE];
+    __shared__ __attribute__((aligned(1024))) char lds1[STAGE];
+
+    const int ntn = (a.N + NOUT - 1) / NOUT;
+    TileInfo ti;
+    if (!find_tile<TM>(a, ntn, ti)) return;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = uniform(tid >> 6);
+    const int wm = wave % WM;
+    const int wn = wave / WM;
+    const int K = a.K;
+    const uint32_t row_bytes = static_cast<uint32_t>(K) * 2u;
+
+    // this wave's rows [wave * WROWS, (wave + 1) * WROWS) are all token rows or all weight rows
+    const bool tok_wave = wave * WROWS < TM;
+    const bf16_t* wgrp = static_cast<const bf16_t*>(a.w) + static_cast<int64_t>(ti.group) * a.w_group_stride;
+    const i32x4 rs = tok_wave ? buffer_rsrc(a.tok, static_cast<uint32_t>(a.src_rows) * row_bytes)
+                              : buffer_rsrc(wgrp, static_cast<uint32_t>(a.w_rows) * row_bytes);
+
+    // one load instruction fills 8 rows: lane -> (row lane / 8, LDS chunk lane % 8), which
+    // holds logical chunk (lane % 8) ^ ((row >> 1) & 7); the swizzle is applied on the
+    // global side
+    uint32_t voff[LOADS];
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+        const int row = wave * WROWS + i * 8 + (lane >> 3);
+        const uint32_t chunk_off = static_cast<uint32_t>(((lane & 7) ^ ((row >> 1) & 7)) * 16);
+        if (tok_wave) {
+            const int r = std::min(row, ti.valid - 1);
+            const int64_t p = ti.row0 + r;
+            const int64_t src = a.row_index ? a.row_index[p] : p;
+            voff[i] = static_cast<uint32_t>(src) * row_bytes + chunk_off;
+        } else {
+            voff[i] = static_cast<uint32_t>(weight_row<TN, SWIGLU>(a, ti.nt, row - TM)) * row_bytes + chunk_off;
+        }
+    }
+    auto issue_slab = [&](int ks, char* stage) {
+        const int soff = ks * RB;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            lds_void* dst = reinterpret_cast<lds_void*>(
+                reinterpret_cast<uintptr_t>(stage + (wave * WROWS + i * 8) * RB));
+            raw_buffer_load_lds(rs, dst, 16, static_cast<int>(voff[i]), soff, 0, 0);
+        }
+    };
+
+    // fragment rows: lane l feeds row (l % 32) of each 32-row block with logical chunk
+    // (2 s + l / 32) of k-step s; blocks start at multiples of 32, so the swizzle depends on
+    // the lane only. Block offsets are compile-time and fold into the read's immediate.
+    const int l32 = lane & 31;
+    const int lh = lane >> 5;
+    const int sw = (l32 >> 1) & 7;
+    constexpr int WTOK = TM / WM;                       // token rows per wave
+    constexpr int WW = SWIGLU ? TN / 2 / WN : TN / WN;  // weight rows per wave (per half)
+    int off_t[4], off_w[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const int ch = ((2 * s + lh) ^ sw) * 16;
+        off_t[s] = (wm * WTOK + l32) * RB + ch;
+        off_w[s] = (TM + wn * WW + l32) * RB + ch;
+    }
+    auto wblk = [](int ni) constexpr {
+        if (SWIGLU) {
+            constexpr int HALF = NI / 2;
+            return (ni < HALF ? 0 : TN / 2) + (ni % HALF) * 32;
+        }
+        return ni * 32;
+    };
+
+    f32x16 acc[NI][MI];
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[ni][mi][r] = 0.f;
+
+    auto mma = [&](const uint4 (&fa)[NI], const uint4 (&fb)[MI]) {
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+                acc[ni][mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[ni]),
+                                                                     __builtin_bit_cast(bf16x8, fb[mi]),
+                                                                     acc[ni][mi], 0, 0, 0);
+    };
+    uint4 pa[NI], pb[MI];  // k-step 3 fragments of the previous slab, consumed after the barrier
+
+    // Program order of a slab: k-step 0 reads, the next slab's buffer loads (other stage),
+    // then [previous slab's k-step 3 | k-step 0 | 1 | 2] MFMAs with reads of k-steps 1, 2, 3
+    // placed one group ahead; k-step 3's MFMAs wait for the next slab.
+    auto slab = [&](const char* base, char* refill, bool prefetch, int ks_next, bool pending) {
+        uint4 fa[3][NI], fb[3][MI];
+        auto read_step = [&](int s, uint4 (&ra)[NI], uint4 (&rb)[MI]) {
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) ra[ni] = *reinterpret_cast<const uint4*>(base + off_w[s] + wblk(ni) * RB);
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi) rb[mi] = *reinterpret_cast<const uint4*>(base + off_t[s] + mi * 32 * RB);
+        };
+        read_step(0, fa[0], fb[0]);
+        if (prefetch) issue_slab(ks_next, refill);
+        read_step(1, fa[1], fb[1]);
+        if (pending) mma(pa, pb);
+        read_step(2, fa[2], fb[2]);
+        mma(fa[0], fb[0]);
+        read_step(3, pa, pb);
+        mma(fa[1], fb[1]);
+        mma(fa[2], fb[2]);
+
+        constexpr int RD = NI + MI;                 // fragment reads per k-step
+        constexpr int MF = NI * MI / RD;            // MFMAs before each read
+        constexpr int REST = NI * MI - MF * RD;
+        static_assert(MF >= 1, "an MFMA for every read of the next k-step");
+        __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
+        if (prefetch) __builtin_amdgcn_sched_group_barrier(0x020, LOADS, 0);
+        if (pending) {
+#pragma unroll
+            for (int i = 0; i < RD; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, MF, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            if (REST) __builtin_amdgcn_sched_group_barrier(0x008, REST, 0);
+        } else {
+            __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
+        }
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+#pragma unroll
+            for (int i = 0; i < RD; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, MF, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            if (REST) __builtin_amdgcn_sched_group_barrier(0x008, REST, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NI * MI, 0);
+    };
+
+    // Before consuming a slab: its loads have landed (vmcnt(0): they are the only ones
+    // outstanding) and this wave's LDS reads have all returned; the barrier then makes every
+    // wave's loads visible and guarantees that no wave still reads the stage about to be
+    // refilled. A bare s_barrier: __syncthreads() would add a fence with the same waits.
+    auto sync = [&]() {
+        __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) expcnt(7) lgkmcnt(0)
+        asm volatile("s_barrier" ::: "memory");
+    };
+
+    const int nk = K / 64;  // even: K is a multiple of 128 on this path
+    issue_slab(0, lds0);
+    sync();
+    slab(lds0, lds1, true, 1, false);
+    for (int ks = 1; ks + 1 < nk; ks += 2) {
+        sync();
+        slab(lds1, lds0, true, ks + 1, true);
+        sync();
+        slab(lds0, lds1, true, ks + 2, true);
+    }
+    sync();
+    slab(lds1, lds0, false, 0, true);
+    mma(pa, pb);
+
+    write_tile32<bf16_t, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+}
+
+// ------------------------------------------------------------------ dispatch
+
+template <int TM, int TN, bool SWIGLU>
+int64_t grid_size(const GemmArgs& a) {
+    constexpr int NOUT = SWIGLU ? TN / 2 : TN;
+    const int64_t ntn = (a.N + NOUT - 1) / NOUT;
+    const int64_t mtiles = a.seg ? (a.rows + TM - 1) / TM + a.n_groups : (a.rows + TM - 1) / TM;
+    return (mtiles * ntn + kXcds - 1) / kXcds * kXcds;
+}
+
 template <typename T, typename TO, int TM, int TN, int WM, int WN, bool SWIGLU>
 hipError_t run(const GemmArgs& a, hipStream_t s) {
-    constexpr int NOUT = SWIGLU ? TN / 2 : TN;
-    const int ntn = (a.N + NOUT - 1) / NOUT;
-    int64_t mtiles = a.seg ? (a.rows + TM - 1) / TM + a.n_groups : (a.rows + TM - 1) / TM;
-    const int64_t grid = mtiles * ntn;
+    const int64_t grid = grid_size<TM, TN, SWIGLU>(a);
     if (grid == 0) return hipSuccess;
     ProfileScope prof(a.name ? a.name : "gemm", s);
-    hipLaunchKernelGGL((gemm_kernel<T, TO, TM, TN, WM, WN, SWIGLU>), dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+    hipLaunchKernelGGL((gemm_kernel<T, TO, TM, TN, WM, WN, SWIGLU>), dim3(static_cast<unsigned>(grid)), dim3(256),
+                       0, s, a);
+    return hipGetLastError();
+}
+
+template <int TM, int TN, int WM, int WN, bool SWIGLU>
+hipError_t run_lds(const GemmArgs& a, hipStream_t s) {
+    const int64_t grid = grid_size<TM, TN, SWIGLU>(a);
+    if (grid == 0) return hipSuccess;
+    ProfileScope prof(a.name ? a.name : "gemm", s);
+    hipLaunchKernelGGL((gemm_lds_kernel<TM, TN, WM, WN, SWIGLU>), dim3(static_cast<unsigned>(grid)), dim3(256), 0,
                        s, a);
     return hipGetLastError();
 }
@@ -295,9 +617,15 @@ Tile choose_tile(const GemmArgs& a, bool swiglu) {
 
 template <typename T, typename TO, bool SWIGLU>
 hipError_t dispatch(const GemmArgs& a, hipStream_t s) {
+    constexpr bool kLdsPath = sizeof(T) == 2 && sizeof(TO) == 2;
+    const bool lds_ok = kLdsPath && a.K % 128 == 0;
     switch (choose_tile(a, SWIGLU)) {
-        case Tile::Big: return run<T, TO, 256, 256, 2, 2, SWIGLU>(a, s);
-        case Tile::Mid: return run<T, TO, 128, 128, 2, 2, SWIGLU>(a, s);
+        case Tile::Big:
+            if (lds_ok) return run_lds<256, 256, 2, 2, SWIGLU>(a, s);
+            return run<T, TO, 256, 256, 2, 2, SWIGLU>(a, s);
+        case Tile::Mid:
+            if (lds_ok) return run_lds<128, 128, 2, 2, SWIGLU>(a, s);
+            return run<T, TO, 128, 128, 2, 2, SWIGLU>(a, s);
         default: return run<T, TO, 32, 128, 1, 4, SWIGLU>(a, s);
     }
 }

@@ -66,6 +66,8 @@ struct GemmArgs {
     const int32_t* seg;       // [groups+1] device segment offsets, or null (dense: one group)
     int n_groups;
     int64_t rows;             // total rows (upper bound for grouped; exact for dense)
+    int64_t src_rows;         // rows of the token matrix `tok` (gather targets are below this)
+    int64_t w_rows;           // rows of one group's weight matrix
     int K;
     int N;                    // output columns
     void* out;                // [rows][N]
