@@ -160,16 +160,23 @@ def main():
     # per-kernel algorithmic work at the realised routing
     idx = layer.topk_idx.cpu().numpy()
     work = R.kernel_work(cfg, R.expert_rows(idx, cfg.n_experts))
-    group = {"perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
-             "transpose": "encode", "codec_xv": "encode", "codec_utp": "encode", "codec_utp_reduce": "encode",
-             "codec_vzt": "decode", "codec_vzt_reduce": "decode", "codec_uw": "decode"}
+    base = {"perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
+            "transpose": "encode", "codec_xv": "encode", "codec_utp": "encode",
+            "codec_vzt": "decode", "codec_uw": "decode"}
+
+    def stage_of(name):
+        # a split-K "<kernel>_tail" / "<kernel>_reduce" launch belongs to its kernel's stage
+        for suf in ("_tail", "_reduce"):
+            if name.endswith(suf):
+                name = name[: -len(suf)]
+        return base.get(name, name)
     peak_f = R.PEAK_TFLOPS[cfg.dtype]
     kernels = {}
     for name, (n, tot) in stats.items():
         kernels[name] = {"launches_per_step": n / steps, "avg_us": round(1e3 * tot / n, 2)}
     rows = {}
     for name, (n, tot) in stats.items():
-        g = group.get(name, name)
+        g = stage_of(name)
         rows.setdefault(g, [0.0, 0])
         rows[g][0] += tot / steps  # ms per step
         rows[g][1] += n / steps
@@ -184,7 +191,7 @@ def main():
             ach = flop / (ms_g * 1e-3) / 1e12 if bound == "mfma" else byt / (ms_g * 1e-3) / 1e9
             peak = peak_f if bound == "mfma" else R.PEAK_HBM_GBS
             for name in stats:
-                if group.get(name, name) == g:
+                if stage_of(name) == g:
                     kernels[name]["stage"] = g
             kernels.setdefault(f"stage:{g}", {})
             kernels[f"stage:{g}"] = {"ms_per_step": round(ms_g, 4), "bound": bound, "achieved": round(ach, 1),

@@ -90,8 +90,11 @@ constexpr size_t kAlign = 256;
 size_t up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
 
 struct MoeWs {
-    size_t counts, seg, perm_src, inv_perm, act, y_perm, total;
+    size_t counts, seg, perm_src, inv_perm, act, y_perm, part, total;
 };
+
+// split-K tail chunks of the large-tile GEMM
+constexpr int kMaxSplit = 8;
 
 MoeWs moe_ws(const ec2moe_moe_desc* d) {
     const int64_t A = static_cast<int64_t>(d->n_tokens) * d->top_k;
@@ -104,6 +107,7 @@ MoeWs moe_ws(const ec2moe_moe_desc* d) {
     w.inv_perm = o; o += up(static_cast<size_t>(A) * 4);
     w.act = o; o += up(static_cast<size_t>(A) * d->ffn_hidden * eb);
     w.y_perm = o; o += up(static_cast<size_t>(A) * d->d_model * eb);
+    w.part = o; o += up(gemm_split_scratch_bytes());
     w.total = o;
     return w;
 }
@@ -145,6 +149,7 @@ int choose_splits(int M, int N, int K) {
 }
 
 struct CodecWs {
+    size_t gpart;  // split-K tail scratch of the matrix-core GEMMs (shared by encode and decode)
     // encode
     size_t vt, p, epart, enc_total;
     int enc_splits;
@@ -158,12 +163,14 @@ CodecWs codec_ws(const ec2moe_codec_desc* d) {
     CodecWs w{};
     w.enc_splits = choose_splits(d->r_h, d->r_w, std::max(1, d->h));
     size_t o = 0;
+    w.gpart = o; o += up(gemm_split_scratch_bytes());
+    const size_t shared = o;
     w.vt = o; o += up(static_cast<size_t>(d->r_w) * d->w * eb);
     w.p = o; o += up(static_cast<size_t>(d->h) * d->r_w * 4);
     w.epart = o; o += up(static_cast<size_t>(w.enc_splits) * d->r_h * d->r_w * 4);
     w.enc_total = o;
     w.dec_splits = choose_splits(d->w, d->r_h, d->r_w);
-    o = 0;
+    o = shared;
     w.wt = o; o += up(static_cast<size_t>(d->w) * d->r_h * eb);
     w.dpart = o; o += up(static_cast<size_t>(w.dec_splits) * d->w * d->r_h * 4);
     w.dec_total = o;
@@ -308,7 +315,8 @@ ec2moe_status ec2moe_permute(const ec2moe_moe_desc* desc, const int32_t* topk_id
 namespace {
 
 hipError_t run_experts(const ec2moe_moe_desc* desc, const void* x, const int32_t* seg, const int32_t* perm_src,
-                       const void* w_gate_up, const void* w_down, void* act, void* y_perm, hipStream_t stream) {
+                       const void* w_gate_up, const void* w_down, void* act, void* y_perm, float* part,
+                       hipStream_t stream) {
     const DType dt = static_cast<DType>(desc->dtype);
     const int64_t A = static_cast<int64_t>(desc->n_tokens) * desc->top_k;
     const int d = desc->d_model, H = desc->ffn_hidden;
@@ -316,14 +324,14 @@ hipError_t run_experts(const ec2moe_moe_desc* desc, const void* x, const int32_t
     g1.tok = x; g1.row_index = perm_src; g1.w = w_gate_up;
     g1.w_group_stride = int64_t(2) * H * d; g1.seg = seg; g1.n_groups = desc->n_experts;
     g1.rows = A; g1.K = d; g1.N = H; g1.out = act; g1.ldo = H; g1.name = "expert_gate_up";
-    g1.src_rows = desc->n_tokens; g1.w_rows = int64_t(2) * H;
+    g1.src_rows = desc->n_tokens; g1.w_rows = int64_t(2) * H; g1.part = part; g1.max_split = kMaxSplit;
     hipError_t e = launch_gemm(dt, Epilogue::SwiGLU, OutType::Same, g1, stream);
     if (e != hipSuccess) return e;
     GemmArgs g2{};
     g2.tok = act; g2.row_index = nullptr; g2.w = w_down;
     g2.w_group_stride = int64_t(d) * H; g2.seg = seg; g2.n_groups = desc->n_experts;
     g2.rows = A; g2.K = H; g2.N = d; g2.out = y_perm; g2.ldo = d; g2.name = "expert_down";
-    g2.src_rows = A; g2.w_rows = d;
+    g2.src_rows = A; g2.w_rows = d; g2.part = part; g2.max_split = kMaxSplit;
     return launch_gemm(dt, Epilogue::Store, OutType::Same, g2, stream);
 }
 
@@ -341,7 +349,8 @@ ec2moe_status ec2moe_expert_ffn(const ec2moe_moe_desc* desc, const void* x, cons
     REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(w_gate_up); REQUIRE_ALIGNED(w_down); REQUIRE_ALIGNED(y_perm);
     if (act) REQUIRE_ALIGNED(act);
     void* act_buf = act ? act : at<void>(ws, w.act);
-    return hip_status(run_experts(desc, x, seg_offsets, perm_src, w_gate_up, w_down, act_buf, y_perm, stream),
+    return hip_status(run_experts(desc, x, seg_offsets, perm_src, w_gate_up, w_down, act_buf, y_perm,
+                                  at<float>(ws, w.part), stream),
                       "expert GEMM launch");
 }
 
@@ -374,7 +383,8 @@ ec2moe_status ec2moe_moe_forward(const ec2moe_moe_desc* desc, const void* x, con
     void* y_perm = at<void>(ws, w.y_perm);
     hipError_t e = launch_permute(topk_idx, A, desc->top_k, desc->n_experts, at<int32_t>(ws, w.counts), seg,
                                   perm_src, inv_perm, stream);
-    if (e == hipSuccess) e = run_experts(desc, x, seg, perm_src, w_gate_up, w_down, act, y_perm, stream);
+    if (e == hipSuccess)
+        e = run_experts(desc, x, seg, perm_src, w_gate_up, w_down, act, y_perm, at<float>(ws, w.part), stream);
     if (e == hipSuccess)
         e = launch_combine(static_cast<DType>(desc->dtype), y_perm, inv_perm, topk_w, desc->n_tokens, desc->top_k,
                            desc->d_model, y, stream);
@@ -409,7 +419,7 @@ ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x
         GemmArgs g{};
         g.tok = xc; g.row_index = nullptr; g.w = vt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
         g.rows = desc->h; g.K = desc->w; g.N = desc->r_w; g.out = p; g.ldo = desc->r_w; g.name = "codec_xv";
-        g.src_rows = desc->h; g.w_rows = desc->r_w;
+        g.src_rows = desc->h; g.w_rows = desc->r_w; g.part = at<float>(ws, w.gpart); g.max_split = kMaxSplit;
         e = launch_gemm(dt, Epilogue::Store, OutType::F32, g, stream);
         if (e != hipSuccess) break;
         // Z = U^T P  [r_h][r_w]: A(m,k) = U[k][m], B(k,n) = P[k][n]
@@ -453,7 +463,7 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
         g.rows = desc->h; g.K = desc->r_h; g.N = desc->w;
         g.out = static_cast<char*>(x_hat) + static_cast<size_t>(c) * desc->h * desc->w * eb; g.ldo = desc->w;
         g.name = "codec_uw";
-        g.src_rows = desc->h; g.w_rows = desc->w;
+        g.src_rows = desc->h; g.w_rows = desc->w; g.part = at<float>(ws, w.gpart); g.max_split = kMaxSplit;
         e = launch_gemm(dt, Epilogue::Store, OutType::Same, g, stream);
     }
     return hip_status(e, "lowrank_decode launch");

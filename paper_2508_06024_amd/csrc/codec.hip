@@ -37,58 +37,75 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ sr
     }
 }
 
-constexpr int kT = 64;   // output tile
-constexpr int kBK = 16;  // k per LDS stage
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
+constexpr int kT = 64;    // output tile (64 x 64 per workgroup, one 32 x 32 block per wave)
+constexpr int kBK = 32;   // k per LDS stage
+constexpr int kPitch = 97;  // LDS row pitch in floats: odd, so 32 consecutive k rows hit distinct banks
+
+// C[m][n] = sum_k A(m,k) B(k,n) on the float32 matrix cores (v_mfma_f32_32x32x2f32).
+// Operands are staged to LDS as [k][m] and [k][n] from any global layout (reads walk the
+// contiguous direction); lane l then feeds row/column l % 32 at k = l / 32 of each step.
 template <typename TA, typename TB>
 __global__ __launch_bounds__(256) void small_gemm_kernel(SmallGemmArgs g) {
-    __shared__ float As[kBK][kT + 4];
-    __shared__ float Bs[kBK][kT + 4];
+    __shared__ float As[kBK * kPitch];
+    __shared__ float Bs[kBK * kPitch];
     const int m0 = blockIdx.x * kT, n0 = blockIdx.y * kT;
     const int split = blockIdx.z;
     const int kper = (g.K + g.splits - 1) / g.splits;
     const int kbeg = split * kper;
     const int kend = std::min(g.K, kbeg + kper);
-    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-    float acc[4][4] = {};
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
     const bool a_k_fast = g.a_sk == 1;
     const bool b_k_fast = g.b_sk == 1;
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    constexpr int PER = kT * kBK / 256;  // elements of each operand per thread per stage
     for (int k0 = kbeg; k0 < kend; k0 += kBK) {
-        for (int i = threadIdx.x; i < kT * kBK; i += 256) {
-            // A tile [kBK][kT]: walk memory-contiguous direction fastest
+        // all loads of the stage first, then the LDS stores
+        float va[PER], vb[PER];
+        int ia[PER], ib[PER];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int e = threadIdx.x + 256 * j;
             int mm, kk;
-            if (a_k_fast) { mm = i / kBK; kk = i % kBK; } else { kk = i / kT; mm = i % kT; }
+            if (a_k_fast) { kk = e % kBK; mm = e / kBK; } else { mm = e % kT; kk = e / kT; }
+            // clamped, unconditional loads (all in flight together); out-of-range lanes select 0
             const int m = m0 + mm, k = k0 + kk;
-            As[kk][mm] = (m < g.M && k < kend) ? ld<TA>(g.a, m * g.a_sm + k * g.a_sk) : 0.f;
+            const float a_v = ld<TA>(g.a, min(m, g.M - 1) * g.a_sm + min(k, kend - 1) * g.a_sk);
+            va[j] = (m < g.M && k < kend) ? a_v : 0.f;
+            ia[j] = kk * kPitch + mm;
             int nn, kb;
-            if (b_k_fast) { nn = i / kBK; kb = i % kBK; } else { kb = i / kT; nn = i % kT; }
+            if (b_k_fast) { kb = e % kBK; nn = e / kBK; } else { nn = e % kT; kb = e / kT; }
             const int n = n0 + nn, kq = k0 + kb;
-            Bs[kb][nn] = (n < g.N && kq < kend) ? ld<TB>(g.b, kq * g.b_sk + n * g.b_sn) : 0.f;
+            const float b_v = ld<TB>(g.b, min(kq, kend - 1) * g.b_sk + min(n, g.N - 1) * g.b_sn);
+            vb[j] = (n < g.N && kq < kend) ? b_v : 0.f;
+            ib[j] = kb * kPitch + nn;
+        }
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            As[ia[j]] = va[j];
+            Bs[ib[j]] = vb[j];
         }
         __syncthreads();
 #pragma unroll
-        for (int kk = 0; kk < kBK; ++kk) {
-            float av[4], bv[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) av[i] = As[kk][ty * 4 + i];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) bv[j] = Bs[kk][tx * 4 + j];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+        for (int kk = 0; kk < kBK; kk += 2) {
+            const float av = As[(kk + (lane >> 5)) * kPitch + wm * 32 + (lane & 31)];
+            const float bv = Bs[(kk + (lane >> 5)) * kPitch + wn * 32 + (lane & 31)];
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
         }
         __syncthreads();
     }
+    // lane l holds C[m0 + wm*32 + 8*(r/4) + 4*(l/32) + r%4][n0 + wn*32 + l%32]
     float* part = g.part + static_cast<int64_t>(split) * g.M * g.N;
+    const int n = n0 + wn * 32 + (lane & 31);
+    if (n < g.N) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = m0 + ty * 4 + i;
-        if (m >= g.M) continue;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int n = n0 + tx * 4 + j;
-            if (n < g.N) part[static_cast<int64_t>(m) * g.N + n] = acc[i][j];
+        for (int r = 0; r < 16; ++r) {
+            const int m = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (m < g.M) part[static_cast<int64_t>(m) * g.N + n] = acc[r];
         }
     }
 }

@@ -1,7 +1,7 @@
 // Weighted combine of the expert outputs, Eq. 1, for gfx950:
 //   y[t] = sum_{j<k} w[t][j] * y_perm[inv_perm[t*k + j]]
-// One workgroup per token; each thread owns 16-byte chunks of the row, accumulates the k
-// slots in float32 in slot order and rounds once. Memory-bound: reads k rows, writes one.
+// One wave per token; each lane owns 16-byte chunks of the row, accumulates the k slots in
+// float32 in slot order and rounds once. Memory-bound: reads k rows, writes one.
 #include "device_common.h"
 #include "internal.h"
 
@@ -9,45 +9,82 @@ namespace ec2moe {
 namespace {
 
 constexpr int kMaxK = 16;
+constexpr int kTokPerBlock = 4;  // one wave per token
 
-template <typename T>
-__global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y_perm,
-                                                      const int32_t* __restrict__ inv_perm,
-                                                      const float* __restrict__ w, int top_k, int d,
+// B chunks of 16 bytes per lane per batch, with all B*k row loads issued before the sums
+template <typename T, int KMAX, int B>
+__global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y_perm, const int32_t* __restrict__ inv_perm,
+                                                      const float* __restrict__ w, int n_tokens, int top_k, int d,
                                                       T* __restrict__ y) {
     constexpr int EPC = Elem<T>::kPerChunk;
-    const int t = blockIdx.x;
-    int pos[kMaxK];
-    float wt[kMaxK];
+    const int lane = threadIdx.x & 63;
+    const int t = blockIdx.x * kTokPerBlock + (threadIdx.x >> 6);
+    if (t >= n_tokens) return;
+    // slot j's position and weight, loaded by lane j and broadcast
+    int my_pos = -1;
+    float my_w = 0.f;
+    if (lane < top_k) {
+        my_pos = inv_perm[static_cast<int64_t>(t) * top_k + lane];
+        my_w = w[static_cast<int64_t>(t) * top_k + lane];
+    }
+    int pos[KMAX];
+    float wt[KMAX];
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-        pos[j] = -1;
-        wt[j] = 0.f;
-        if (j < top_k) {
-            pos[j] = inv_perm[static_cast<int64_t>(t) * top_k + j];
-            wt[j] = w[static_cast<int64_t>(t) * top_k + j];
-        }
+    for (int j = 0; j < KMAX; ++j) {
+        pos[j] = __shfl(my_pos, j);
+        wt[j] = __shfl(my_w, j);
     }
     const int chunks = d / EPC;
-    for (int c = threadIdx.x; c < chunks; c += 256) {
-        float acc[EPC];
+    for (int c0 = lane; c0 < chunks; c0 += 64 * B) {
+        uint4 v[B][KMAX];
 #pragma unroll
-        for (int i = 0; i < EPC; ++i) acc[i] = 0.f;
+        for (int b = 0; b < B; ++b)
 #pragma unroll
-        for (int j = 0; j < kMaxK; ++j) {
-            if (j < top_k && pos[j] >= 0) {
-                const uint4 v = ldg16(y_perm + static_cast<int64_t>(pos[j]) * d + c * EPC);
-                const T* ve = reinterpret_cast<const T*>(&v);
-#pragma unroll
-                for (int i = 0; i < EPC; ++i) acc[i] += wt[j] * Elem<T>::to_f32(ve[i]);
+            for (int j = 0; j < KMAX; ++j) {
+                const int c = c0 + 64 * b;
+                v[b][j] = (j < top_k && pos[j] >= 0 && c < chunks)
+                              ? ldg16(y_perm + static_cast<int64_t>(pos[j]) * d + c * EPC)
+                              : make_uint4(0, 0, 0, 0);
             }
-        }
-        uint4 o;
-        T* oe = reinterpret_cast<T*>(&o);
 #pragma unroll
-        for (int i = 0; i < EPC; ++i) oe[i] = Elem<T>::from_f32(acc[i]);
-        stg16(y + static_cast<int64_t>(t) * d + c * EPC, o);
+        for (int b = 0; b < B; ++b) {
+            const int c = c0 + 64 * b;
+            if (c >= chunks) break;
+            float acc[EPC];
+#pragma unroll
+            for (int i = 0; i < EPC; ++i) acc[i] = 0.f;
+#pragma unroll
+            for (int j = 0; j < KMAX; ++j) {
+                if (j < top_k && pos[j] >= 0) {
+                    const T* ve = reinterpret_cast<const T*>(&v[b][j]);
+#pragma unroll
+                    for (int i = 0; i < EPC; ++i) acc[i] += wt[j] * Elem<T>::to_f32(ve[i]);
+                }
+            }
+            uint4 o;
+            T* oe = reinterpret_cast<T*>(&o);
+#pragma unroll
+            for (int i = 0; i < EPC; ++i) oe[i] = Elem<T>::from_f32(acc[i]);
+            stg16(y + static_cast<int64_t>(t) * d + c * EPC, o);
+        }
     }
+}
+
+template <typename T, int KMAX, int B>
+void launch_k(const void* y_perm, const int32_t* inv_perm, const float* w, int n_tokens, int top_k, int d, void* y,
+              hipStream_t s) {
+    const int grid = (n_tokens + kTokPerBlock - 1) / kTokPerBlock;
+    hipLaunchKernelGGL((combine_kernel<T, KMAX, B>), dim3(grid), dim3(64 * kTokPerBlock), 0, s,
+                       static_cast<const T*>(y_perm), inv_perm, w, n_tokens, top_k, d, static_cast<T*>(y));
+}
+
+template <typename T>
+void launch_t(const void* y_perm, const int32_t* inv_perm, const float* w, int n_tokens, int top_k, int d, void* y,
+              hipStream_t s) {
+    if (top_k <= 2) launch_k<T, 2, 8>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
+    else if (top_k <= 4) launch_k<T, 4, 4>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
+    else if (top_k <= 8) launch_k<T, 8, 2>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
+    else launch_k<T, kMaxK, 1>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
 }
 
 }  // namespace
@@ -57,11 +94,9 @@ hipError_t launch_combine(DType dt, const void* y_perm, const int32_t* inv_perm,
     if (n_tokens == 0) return hipSuccess;
     ProfileScope prof("combine", s);
     if (dt == DType::BF16)
-        hipLaunchKernelGGL(combine_kernel<bf16_t>, dim3(n_tokens), dim3(256), 0, s,
-                           static_cast<const bf16_t*>(y_perm), inv_perm, w, top_k, d, static_cast<bf16_t*>(y));
+        launch_t<bf16_t>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
     else
-        hipLaunchKernelGGL(combine_kernel<float>, dim3(n_tokens), dim3(256), 0, s,
-                           static_cast<const float*>(y_perm), inv_perm, w, top_k, d, static_cast<float*>(y));
+        launch_t<float>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
     return hipGetLastError();
 }
 

@@ -35,129 +35,144 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void gate_kernel(GateArgs p) {
-    extern __shared__ float part[];  // [4 waves][rows][16 tokens], then the sums in wave 0's slot
-    __shared__ float grp_max[4][kMaxGroups];
-    __shared__ float grp_sum[4][kMaxGroups];
-    __shared__ float grp_p[4][kMaxGroups];
+// NRB: blocks of 16 gate rows (M + K <= 16 * NRB); WAVES: waves splitting d.
+template <typename T, int NRB, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
+    extern __shared__ float part[];  // [WAVES][NRB*16 rows][16 tokens], then the sums in wave 0's slot
+    __shared__ float grp_max[WAVES][kMaxGroups];
+    __shared__ float grp_sum[WAVES][kMaxGroups];
+    __shared__ float grp_p[WAVES][kMaxGroups];
 
     constexpr int EPC = Elem<T>::kPerChunk;
     constexpr int SLICE = 4 * EPC;  // k covered by one matrix-core step
+    // k-slices whose loads are issued together: deep for few gate rows, shallow for many
+    constexpr int U = 16 / (NRB + 1) < 1 ? 1 : (16 / (NRB + 1) > 8 ? 8 : 16 / (NRB + 1));
+    constexpr int THREADS = 64 * WAVES;
+    constexpr int TPW = kTok / WAVES;  // tokens per wave in the softmax phase
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int g4 = lane >> 4;
     const int M = p.n_experts, K = p.n_groups, d = p.d;
     const int R = M + K;
-    const int nrb = (R + 15) >> 4;
     const int t0 = blockIdx.x * kTok;
 
-    // ---------------- phase 1: partial logits over this wave's quarter of d
+    // ---------------- phase 1: partial logits over this wave's share of d
     int tok = t0 + (lane & 15);
     if (tok >= p.n_tokens) tok = p.n_tokens - 1;
-    const T* xrow = static_cast<const T*>(p.x) + static_cast<size_t>(tok) * d;
-    const T* wl = static_cast<const T*>(p.w_local);
-    const T* wg = static_cast<const T*>(p.w_global);
-    const int kq = d >> 2;
+    const T* xrow = static_cast<const T*>(p.x) + static_cast<size_t>(tok) * d + g4 * EPC;
+    const T* wrow[NRB];
+    bool wvalid[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+        const int r = rb * 16 + (lane & 15);
+        wvalid[rb] = r < R;
+        const int rr = wvalid[rb] ? r : 0;
+        wrow[rb] = (rr < M ? static_cast<const T*>(p.w_local) + static_cast<size_t>(rr) * d
+                           : static_cast<const T*>(p.w_global) + static_cast<size_t>(rr - M) * d) + g4 * EPC;
+    }
+    const int kq = d / WAVES;
     const int kbeg = wave * kq;
 
-    f32x4 acc[kMaxRowBlocks];
+    f32x4 acc[NRB];
 #pragma unroll
-    for (int rb = 0; rb < kMaxRowBlocks; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int k = kbeg; k < kbeg + kq; k += SLICE) {
-        const uint4 bx = ldg16(xrow + k + g4 * EPC);
+    int k = kbeg;
+    for (; k + U * SLICE <= kbeg + kq; k += U * SLICE) {
+        uint4 bx[U], aw[U][NRB];
 #pragma unroll
-        for (int rb = 0; rb < kMaxRowBlocks; ++rb) {
-            if (rb < nrb) {
-                const int r = rb * 16 + (lane & 15);
-                uint4 aw = make_uint4(0, 0, 0, 0);
-                if (r < R) {
-                    const T* wrow = r < M ? wl + static_cast<size_t>(r) * d
-                                          : wg + static_cast<size_t>(r - M) * d;
-                    aw = ldg16(wrow + k + g4 * EPC);
-                }
-                acc[rb] = Mfma<T>::step(aw, bx, acc[rb]);
-            }
+        for (int u = 0; u < U; ++u) {
+            bx[u] = ldg16(xrow + k + u * SLICE);
+#pragma unroll
+            for (int rb = 0; rb < NRB; ++rb)
+                aw[u][rb] = wvalid[rb] ? ldg16(wrow[rb] + k + u * SLICE) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int rb = 0; rb < NRB; ++rb) acc[rb] = Mfma<T>::step(aw[u][rb], bx[u], acc[rb]);
+    }
+    for (; k < kbeg + kq; k += SLICE) {
+        const uint4 bx = ldg16(xrow + k);
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
+            const uint4 aw = wvalid[rb] ? ldg16(wrow[rb] + k) : make_uint4(0, 0, 0, 0);
+            acc[rb] = Mfma<T>::step(aw, bx, acc[rb]);
         }
     }
 
-    const int rows_pad = nrb * 16;
-    float* mine = part + static_cast<size_t>(wave) * rows_pad * kTok;
+    constexpr int ROWS_PAD = NRB * 16;
+    constexpr int N_EL = ROWS_PAD * kTok;
+    float* mine = part + static_cast<size_t>(wave) * N_EL;
 #pragma unroll
-    for (int rb = 0; rb < kMaxRowBlocks; ++rb) {
-        if (rb < nrb) {
+    for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) mine[(rb * 16 + g4 * 4 + i) * kTok + (lane & 15)] = acc[rb][i];
-        }
+        for (int i = 0; i < 4; ++i) mine[(rb * 16 + g4 * 4 + i) * kTok + (lane & 15)] = acc[rb][i];
+    __syncthreads();
+
+    // ---------------- phase 2: fixed-order sum of the partials
+    for (int i = threadIdx.x; i < N_EL; i += THREADS) {
+        float sum = part[i];
+#pragma unroll
+        for (int w = 1; w < WAVES; ++w) sum += part[w * N_EL + i];
+        part[i] = sum;
     }
     __syncthreads();
 
-    // ---------------- phase 2: fixed-order sum of the four partials
-    const int n_el = rows_pad * kTok;
-    for (int i = threadIdx.x; i < n_el; i += 256) {
-        float s = part[i];
-        s += part[n_el + i];
-        s += part[2 * n_el + i];
-        s += part[3 * n_el + i];
-        part[i] = s;
-    }
-    __syncthreads();
-
-    // ---------------- phase 3: two-stage softmax, fusion, top-k; 4 tokens per wave
+    // ---------------- phase 3: two-stage softmax, fusion, top-k; TPW tokens per wave
     const float* logit = part;  // [row][token]
     const int Mk = M / K;
-    for (int it = 0; it < kTok / 4; ++it) {
-        const int tl = wave * (kTok / 4) + it;
+    for (int it = 0; it < TPW; ++it) {
+        const int tl = wave * TPW + it;
         const int t = t0 + tl;
 
         // stage 2 statistics per group over its candidates: max and sum of exp
-        for (int k = lane; k < K; k += 64) {
+        for (int kk = lane; kk < K; kk += 64) {
             float m = -INFINITY;
-            for (int i = k * Mk; i < (k + 1) * Mk; ++i) {
+            for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) {
                 if (is_cand(p.mask, i)) {
                     const float l = logit[i * kTok + tl] + (p.b_local ? p.b_local[i] : 0.f);
                     m = fmaxf(m, l);
                 }
             }
-            float s = 0.f;
+            float sum = 0.f;
             if (m != -INFINITY) {
-                for (int i = k * Mk; i < (k + 1) * Mk; ++i) {
+                for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) {
                     if (is_cand(p.mask, i)) {
                         const float l = logit[i * kTok + tl] + (p.b_local ? p.b_local[i] : 0.f);
-                        s += expf(l - m);
+                        sum += expf(l - m);
                     }
                 }
             }
-            grp_max[wave][k] = m;
-            grp_sum[wave][k] = s;
+            grp_max[wave][kk] = m;
+            grp_sum[wave][kk] = sum;
         }
         __syncthreads();
 
         // stage 1: softmax over the groups that hold a candidate
         float lmax = -INFINITY;
-        for (int k = lane; k < K; k += 64) {
-            if (grp_max[wave][k] != -INFINITY) {
-                const float lg = logit[(M + k) * kTok + tl] + (p.b_global ? p.b_global[k] : 0.f);
+        for (int kk = lane; kk < K; kk += 64) {
+            if (grp_max[wave][kk] != -INFINITY) {
+                const float lg = logit[(M + kk) * kTok + tl] + (p.b_global ? p.b_global[kk] : 0.f);
                 lmax = fmaxf(lmax, lg);
             }
         }
         const float gmax = wave_max(lmax);
         float lsum = 0.f;
-        for (int k = lane; k < K; k += 64) {
-            if (grp_max[wave][k] != -INFINITY) {
-                const float lg = logit[(M + k) * kTok + tl] + (p.b_global ? p.b_global[k] : 0.f);
+        for (int kk = lane; kk < K; kk += 64) {
+            if (grp_max[wave][kk] != -INFINITY) {
+                const float lg = logit[(M + kk) * kTok + tl] + (p.b_global ? p.b_global[kk] : 0.f);
                 lsum += expf(lg - gmax);
             }
         }
         const float gsum = wave_sum(lsum);
-        for (int k = lane; k < K; k += 64) {
+        for (int kk = lane; kk < K; kk += 64) {
             float pg = 0.f;
-            if (grp_max[wave][k] != -INFINITY) {
-                const float lg = logit[(M + k) * kTok + tl] + (p.b_global ? p.b_global[k] : 0.f);
+            if (grp_max[wave][kk] != -INFINITY) {
+                const float lg = logit[(M + kk) * kTok + tl] + (p.b_global ? p.b_global[kk] : 0.f);
                 pg = expf(lg - gmax) / gsum;
             }
-            grp_p[wave][k] = pg;
+            grp_p[wave][kk] = pg;
         }
         __syncthreads();
 
@@ -168,10 +183,10 @@ __global__ __launch_bounds__(256) void gate_kernel(GateArgs p) {
             const int i = lane + 64 * q;
             gv[q] = -1.f;
             if (i < M && is_cand(p.mask, i)) {
-                const int k = i / Mk;
+                const int kk = i / Mk;
                 const float l = logit[i * kTok + tl] + (p.b_local ? p.b_local[i] : 0.f);
-                const float pl = expf(l - grp_max[wave][k]) / grp_sum[wave][k];
-                gv[q] = grp_p[wave][k] * pl;
+                const float pl = expf(l - grp_max[wave][kk]) / grp_sum[wave][kk];
+                gv[q] = grp_p[wave][kk] * pl;
             }
             if (p.probs && t < p.n_tokens && i < M)
                 p.probs[static_cast<size_t>(t) * M + i] = gv[q] < 0.f ? 0.f : gv[q];
@@ -213,11 +228,11 @@ __global__ __launch_bounds__(256) void gate_kernel(GateArgs p) {
 
         float denom = 1.f;
         if (p.renormalize) {
-            float s = 0.f;
+            float sum = 0.f;
 #pragma unroll
             for (int j = 0; j < kMaxTopK; ++j)
-                if (j < p.top_k) s += sel_g[j];
-            denom = s;
+                if (j < p.top_k) sum += sel_g[j];
+            denom = sum;
         }
         if (t < p.n_tokens) {
 #pragma unroll
@@ -232,22 +247,44 @@ __global__ __launch_bounds__(256) void gate_kernel(GateArgs p) {
     }
 }
 
-template <typename T>
-hipError_t launch_gate_t(const GateArgs& a, hipStream_t s) {
-    const int rows_pad = ((a.n_experts + a.n_groups + 15) / 16) * 16;
-    const size_t lds = static_cast<size_t>(4) * rows_pad * kTok * sizeof(float);
-    static bool attr_set = false;
+template <typename T, int NRB, int WAVES>
+hipError_t launch_waves(const GateArgs& a, hipStream_t s) {
+    const size_t lds = static_cast<size_t>(WAVES) * NRB * 16 * kTok * sizeof(float);
+    static bool attr_set = false;  // once per instantiation: allow the partials beside the static arrays
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gate_kernel<T>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           4 * 320 * kTok * sizeof(float));
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gate_kernel<T, NRB, WAVES>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const int grid = (a.n_tokens + kTok - 1) / kTok;
     ProfileScope prof("gate", s);
-    hipLaunchKernelGGL(gate_kernel<T>, dim3(grid), dim3(256), lds, s, a);
+    hipLaunchKernelGGL((gate_kernel<T, NRB, WAVES>), dim3(grid), dim3(64 * WAVES), lds, s, a);
     return hipGetLastError();
+}
+
+// 8 waves split d when their partial logits fit in 64 KB of LDS and d splits evenly; else 4
+template <typename T, int NRB>
+hipError_t launch_nrb(const GateArgs& a, hipStream_t s) {
+    constexpr int SLICE = 4 * Elem<T>::kPerChunk;
+    if (NRB <= 8 && a.d % (8 * SLICE) == 0) return launch_waves<T, NRB, 8>(a, s);
+    return launch_waves<T, NRB, 4>(a, s);
+}
+
+template <typename T>
+hipError_t launch_gate_t(const GateArgs& a, hipStream_t s) {
+    switch ((a.n_experts + a.n_groups + 15) / 16) {
+        case 1: return launch_nrb<T, 1>(a, s);
+        case 2: return launch_nrb<T, 2>(a, s);
+        case 3: return launch_nrb<T, 3>(a, s);
+        case 4: return launch_nrb<T, 4>(a, s);
+        case 5: return launch_nrb<T, 5>(a, s);
+        case 6: return launch_nrb<T, 6>(a, s);
+        case 7: case 8: return launch_nrb<T, 8>(a, s);
+        case 9: case 10: case 11: case 12: return launch_nrb<T, 12>(a, s);
+        case 13: case 14: case 15: case 16: return launch_nrb<T, 16>(a, s);
+        default: return launch_nrb<T, kMaxRowBlocks>(a, s);
+    }
 }
 
 }  // namespace

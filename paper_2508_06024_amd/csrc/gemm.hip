@@ -34,6 +34,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <string>
 #include <type_traits>
 
 namespace ec2moe {
@@ -48,6 +49,7 @@ __device__ void raw_buffer_load_lds(i32x4 rsrc, lds_void* lds, int size, int vof
 namespace {
 
 constexpr int kXcds = 8;
+constexpr int kMaxSplitChunks = 8;  // K chunks of a split tail tile (the reduction holds this many)
 
 struct TileInfo {
     int group;
@@ -58,33 +60,27 @@ struct TileInfo {
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-// Finds the tile of this workgroup; false if the workgroup has no tile.
+// Number of real tiles (uniform): sum over groups of ceil(rows_e / TM) * ntn.
 template <int TM>
-__device__ __forceinline__ bool find_tile(const GemmArgs& a, int ntn, TileInfo& ti) {
+__device__ __forceinline__ int count_tiles(const GemmArgs& a, int ntn) {
+    if (a.seg == nullptr) return uniform(static_cast<int>((a.rows + TM - 1) / TM) * ntn);
     const int lane = threadIdx.x & 63;
-    // real tiles
-    int total;
-    if (a.seg == nullptr) {
-        total = static_cast<int>((a.rows + TM - 1) / TM) * ntn;
-    } else {
-        int t = 0;
-        for (int e0 = 0; e0 < a.n_groups; e0 += 64) {
-            const int e = e0 + lane;
-            int cnt = 0;
-            if (e < a.n_groups) cnt = ((a.seg[e + 1] - a.seg[e] + TM - 1) / TM) * ntn;
+    int t = 0;
+    for (int e0 = 0; e0 < a.n_groups; e0 += 64) {
+        const int e = e0 + lane;
+        int cnt = 0;
+        if (e < a.n_groups) cnt = ((a.seg[e + 1] - a.seg[e] + TM - 1) / TM) * ntn;
 #pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off);
-            t += cnt;
-        }
-        total = t;
+        for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off);
+        t += cnt;
     }
-    total = uniform(total);
-    const int per_xcd = (total + kXcds - 1) / kXcds;
-    const int p = blockIdx.x;
-    const int j = p / kXcds;
-    const int bid = (p % kXcds) * per_xcd + j;
-    if (j >= per_xcd || bid >= total) return false;
+    return uniform(t);
+}
 
+// Tile with logical index bid (groups in order; within a group, n-tiles in order and the
+// m-tiles of one n-tile adjacent).
+template <int TM>
+__device__ __forceinline__ bool tile_of(const GemmArgs& a, int ntn, int bid, TileInfo& ti) {
     if (a.seg == nullptr) {
         const int mtiles = static_cast<int>((a.rows + TM - 1) / TM);
         const int mt = bid % mtiles;
@@ -94,6 +90,7 @@ __device__ __forceinline__ bool find_tile(const GemmArgs& a, int ntn, TileInfo& 
         ti.valid = static_cast<int>(std::min<int64_t>(TM, a.rows - ti.row0));
         return true;
     }
+    const int lane = threadIdx.x & 63;
     int base = 0;
     for (int e0 = 0; e0 < a.n_groups; e0 += 64) {
         const int e = e0 + lane;
@@ -128,6 +125,42 @@ __device__ __forceinline__ bool find_tile(const GemmArgs& a, int ntn, TileInfo& 
         base += __shfl(inc, 63);
     }
     return false;
+}
+
+// XCD-aware order: workgroup p of a launch of `units` whole tiles runs logical tile
+// (p % 8) * ceil(units / 8) + p / 8; -1 if p has no tile.
+__device__ __forceinline__ int xcd_remap(int p, int units) {
+    const int per_xcd = (units + kXcds - 1) / kXcds;
+    const int j = p / kXcds;
+    const int bid = (p % kXcds) * per_xcd + j;
+    return (j >= per_xcd || bid >= units) ? -1 : bid;
+}
+
+// Finds the tile of this workgroup (whole tiles only); false if it has none.
+template <int TM>
+__device__ __forceinline__ bool find_tile(const GemmArgs& a, int ntn, TileInfo& ti) {
+    const int bid = xcd_remap(blockIdx.x, count_tiles<TM>(a, ntn));
+    return bid >= 0 && tile_of<TM>(a, ntn, bid, ti);
+}
+
+// Split plan of a launch with `total` tiles and `slots` workgroups resident at once: the
+// tiles that fill whole rounds run whole; the tail (fewer than one round) is split into
+// S chunks along K so the last round is about as wide as the machine. Chunks hold an even
+// number of 64-wide slabs.
+struct SplitPlan {
+    int full, tail, S, chunk_slabs;
+};
+
+__device__ __forceinline__ SplitPlan split_plan(int total, int slots, int max_split, int nk) {
+    SplitPlan sp;
+    sp.full = slots > 0 ? total / slots * slots : total;
+    sp.tail = total - sp.full;
+    int S = 1;
+    if (sp.tail > 0 && max_split > 1)
+        S = std::max(1, std::min(std::min(std::min(max_split, kMaxSplitChunks), slots / sp.tail), nk / 2));
+    sp.S = S;
+    sp.chunk_slabs = ((nk + S - 1) / S + 1) / 2 * 2;
+    return sp;
 }
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
@@ -378,6 +411,14 @@ __device__ __forceinline__ void write_tile32(const GemmArgs& a, const TileInfo& 
     }
 }
 
+// Workgroups of the large-tile kernel resident at once on the chip: 256 CUs, and as many
+// workgroups per CU as its LDS stages allow (one 256x256 tile, two 128x128 tiles).
+constexpr int kCUs = 256;
+template <int TM, int TN>
+__host__ __device__ constexpr int gemm_slots() {
+    return kCUs * ((160 * 1024) / (2 * (TM + TN) * 128));
+}
+
 // bf16 mainloop on 32x32x16 matrix-core blocks (the full-rate bf16 MFMA shape on gfx950).
 //
 // K advances in slabs of 64 (one 128-byte row per tile row) through two LDS stages; the
@@ -390,7 +431,7 @@ __device__ __forceinline__ void write_tile32(const GemmArgs& a, const TileInfo& 
 // Within a slab of 4 k-steps, fragment reads run one k-step ahead of the MFMAs; the
 // MFMAs of a slab's last k-step are deferred past the next barrier, where they cover the
 // latency of the next slab's first reads.
-template <int TM, int TN, int WM, int WN, bool SWIGLU>
+template <int TM, int TN, int WM, int WN, bool SWIGLU, typename TO>
 __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
     static_assert(WM * WN == 4, "4 waves per workgroup");
     constexpr int MI = TM / WM / 32;           // token blocks of 32 per wave
@@ -409,15 +450,30 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
     __shared__ __attribute__((aligned(1024))) char lds1[STAGE];
 
     const int ntn = (a.N + NOUT - 1) / NOUT;
+    const int K = a.K;
+    const int nk_all = K / 64;  // even: K is a multiple of 128 on this path
+    const SplitPlan sp = split_plan(count_tiles<TM>(a, ntn), a.part ? gemm_slots<TM, TN>() : 0, a.max_split, nk_all);
+    int bid, chunk = 0;
+    const int p = blockIdx.x;
+    if (p < sp.full) {
+        bid = xcd_remap(p, sp.full);
+    } else {
+        const int u = p - sp.full;
+        if (u >= sp.tail * sp.S) return;
+        bid = sp.full + u / sp.S;
+        chunk = u % sp.S;
+    }
     TileInfo ti;
-    if (!find_tile<TM>(a, ntn, ti)) return;
+    if (bid < 0 || !tile_of<TM>(a, ntn, bid, ti)) return;
+    const bool split = sp.S > 1 && p >= sp.full;
+    const int kb = split ? chunk * sp.chunk_slabs : 0;                  // first slab of this unit
+    const int nk = split ? std::min(nk_all, kb + sp.chunk_slabs) - kb : nk_all;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = uniform(tid >> 6);
     const int wm = wave % WM;
     const int wn = wave / WM;
-    const int K = a.K;
     const uint32_t row_bytes = static_cast<uint32_t>(K) * 2u;
 
     // this wave's rows [wave * WROWS, (wave + 1) * WROWS) are all token rows or all weight rows
@@ -444,7 +500,7 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
         }
     }
     auto issue_slab = [&](int ks, char* stage) {
-        const int soff = ks * RB;
+        const int soff = (kb + ks) * RB;
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
             lds_void* dst = reinterpret_cast<lds_void*>(
@@ -553,21 +609,95 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
         asm volatile("s_barrier" ::: "memory");
     };
 
-    const int nk = K / 64;  // even: K is a multiple of 128 on this path
-    issue_slab(0, lds0);
-    sync();
-    slab(lds0, lds1, true, 1, false);
-    for (int ks = 1; ks + 1 < nk; ks += 2) {
+    if (nk > 0) {  // nk is even (whole chunks of an even number of slabs)
+        issue_slab(0, lds0);
         sync();
-        slab(lds1, lds0, true, ks + 1, true);
+        slab(lds0, lds1, true, 1, false);
+        for (int ks = 1; ks + 1 < nk; ks += 2) {
+            sync();
+            slab(lds1, lds0, true, ks + 1, true);
+            sync();
+            slab(lds0, lds1, true, ks + 2, true);
+        }
         sync();
-        slab(lds0, lds1, true, ks + 2, true);
+        slab(lds1, lds0, false, 0, true);
+        mma(pa, pb);
     }
-    sync();
-    slab(lds1, lds0, false, 0, true);
-    mma(pa, pb);
 
-    write_tile32<bf16_t, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+    if (split) {
+        // raw float32 partial tile [TM][TN] (weight rows in tile order) of this K chunk
+        float* part = a.part + static_cast<int64_t>(p - sp.full) * TM * TN;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+            const int trow = wm * WTOK + mi * 32 + l32;
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+                const int wrow = wn * WW + wblk(ni);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    f32x4 v;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] = acc[ni][mi][4 * q + i];
+                    *reinterpret_cast<f32x4*>(part + trow * TN + wrow + 8 * q + 4 * lh) = v;
+                }
+            }
+        }
+        return;
+    }
+    write_tile32<TO, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+}
+
+// Sums the float32 partial tiles of the split tail in chunk order and applies the
+// epilogue (store, or silu(gate) * up) of the large-tile kernel. One workgroup per
+// (tail tile, 16 rows); every thread owns a run of 4 output columns per pass and issues
+// the loads of all chunks before adding them in order.
+template <int TM, int TN, bool SWIGLU, typename TO>
+__global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs a) {
+    constexpr int NOUT = SWIGLU ? TN / 2 : TN;
+    constexpr int kMaxS = kMaxSplitChunks;
+    const int ntn = (a.N + NOUT - 1) / NOUT;
+    const SplitPlan sp = split_plan(count_tiles<TM>(a, ntn), gemm_slots<TM, TN>(), a.max_split, a.K / 64);
+    if (sp.S <= 1) return;
+    constexpr int ROWS = 16;
+    constexpr int QUADS = NOUT / 4;                  // float4 column runs per row
+    const int t = blockIdx.x / (TM / ROWS);
+    if (t >= sp.tail) return;
+    TileInfo ti;
+    if (!tile_of<TM>(a, ntn, sp.full + t, ti)) return;
+    const float* tile_part = a.part + static_cast<int64_t>(t) * sp.S * TM * TN;
+    const int r0 = (blockIdx.x % (TM / ROWS)) * ROWS;
+    for (int i = threadIdx.x; i < ROWS * QUADS; i += 256) {
+        const int r = r0 + i / QUADS;
+        const int c = (i % QUADS) * 4;
+        if (r >= ti.valid) continue;
+        f32x4 g[kMaxS], u[kMaxS];
+#pragma unroll
+        for (int k = 0; k < kMaxS; ++k) {
+            if (k < sp.S) {
+                const float* src = tile_part + static_cast<int64_t>(k) * TM * TN + r * TN + c;
+                g[k] = *reinterpret_cast<const f32x4*>(src);
+                if (SWIGLU) u[k] = *reinterpret_cast<const f32x4*>(src + TN / 2);
+            }
+        }
+        f32x4 sg = g[0], su = u[0];
+#pragma unroll
+        for (int k = 1; k < kMaxS; ++k) {
+            if (k < sp.S) {
+                sg += g[k];
+                if (SWIGLU) su += u[k];
+            }
+        }
+        TO* orow = static_cast<TO*>(a.out) + (ti.row0 + r) * a.ldo;
+        if (SWIGLU) {
+            f32x4 v;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] = silu(sg[q]) * su[q];
+            store4<TO>(orow + ti.nt * NOUT + c, v);
+        } else {
+            const int col = ti.nt * TN + c;
+            if (col < a.N) store4<TO>(orow + col, sg);
+        }
+    }
 }
 
 // ------------------------------------------------------------------ dispatch
@@ -590,26 +720,52 @@ hipError_t run(const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <int TM, int TN, int WM, int WN, bool SWIGLU>
+template <int TM, int TN, int WM, int WN, bool SWIGLU, typename TO>
 hipError_t run_lds(const GemmArgs& a, hipStream_t s) {
-    const int64_t grid = grid_size<TM, TN, SWIGLU>(a);
+    int64_t grid = grid_size<TM, TN, SWIGLU>(a);
     if (grid == 0) return hipSuccess;
-    ProfileScope prof(a.name ? a.name : "gemm", s);
-    hipLaunchKernelGGL((gemm_lds_kernel<TM, TN, WM, WN, SWIGLU>), dim3(static_cast<unsigned>(grid)), dim3(256), 0,
-                       s, a);
+    const bool can_split = a.part != nullptr && a.max_split > 1;
+    // whole rounds + a split tail of at most `slots` units
+    if (can_split) grid += gemm_slots<TM, TN>();
+    {
+        ProfileScope prof(a.name ? a.name : "gemm", s);
+        hipLaunchKernelGGL((gemm_lds_kernel<TM, TN, WM, WN, SWIGLU, TO>), dim3(static_cast<unsigned>(grid)), dim3(256),
+                           0, s, a);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !can_split) return e;
+    // the tile count of a dense launch is known here: no tail, no reduction
+    if (a.seg == nullptr) {
+        constexpr int NOUT = SWIGLU ? TN / 2 : TN;
+        const int64_t tiles = (a.rows + TM - 1) / TM * ((a.N + NOUT - 1) / NOUT);
+        if (tiles % gemm_slots<TM, TN>() == 0) return hipSuccess;
+    }
+    std::string rname = std::string(a.name ? a.name : "gemm") + "_tail";
+    ProfileScope prof(rname.c_str(), s);
+    hipLaunchKernelGGL((gemm_split_reduce_kernel<TM, TN, SWIGLU, TO>), dim3(gemm_slots<TM, TN>() * (TM / 16)), dim3(256),
+                       0, s, a);
     return hipGetLastError();
 }
 
-// Tile choice: the largest tile that still gives at least two workgroups per CU.
+// Tile choice. The bf16 direct-to-LDS path (K a multiple of 128) takes the largest tile
+// whose rows are mostly occupied; its split-K tail supplies parallelism for few tiles.
+// Otherwise the register-staged kernel, with the largest tile that still gives two
+// workgroups per CU.
 enum class Tile { Big, Mid, Small };
 
-Tile choose_tile(const GemmArgs& a, bool swiglu) {
+Tile choose_tile(const GemmArgs& a, bool swiglu, bool lds) {
     auto tiles = [&](int tm, int tn) {
         const int nout = swiglu ? tn / 2 : tn;
         const int64_t mt = (a.rows + tm - 1) / tm + (a.seg ? a.n_groups : 0);
         return mt * ((a.N + nout - 1) / nout);
     };
     const int64_t avg_rows = a.seg ? a.rows / std::max(1, a.n_groups) : a.rows;
+    if (lds) {
+        // short K (a few slabs per tile) favours two workgroups per CU over big tiles
+        if (avg_rows >= 256 && a.K > 512 && tiles(256, 256) >= gemm_slots<256, 256>()) return Tile::Big;
+        if (avg_rows >= 64) return Tile::Mid;
+        return Tile::Small;
+    }
     if (avg_rows >= 256 && tiles(256, 256) >= 512) return Tile::Big;
     if (avg_rows >= 64 && tiles(128, 128) >= 512) return Tile::Mid;
     return Tile::Small;
@@ -617,20 +773,27 @@ Tile choose_tile(const GemmArgs& a, bool swiglu) {
 
 template <typename T, typename TO, bool SWIGLU>
 hipError_t dispatch(const GemmArgs& a, hipStream_t s) {
-    constexpr bool kLdsPath = sizeof(T) == 2 && sizeof(TO) == 2;
+    constexpr bool kLdsPath = sizeof(T) == 2;
     const bool lds_ok = kLdsPath && a.K % 128 == 0;
-    switch (choose_tile(a, SWIGLU)) {
+    switch (choose_tile(a, SWIGLU, lds_ok)) {
         case Tile::Big:
-            if (lds_ok) return run_lds<256, 256, 2, 2, SWIGLU>(a, s);
+            if constexpr (kLdsPath)
+                if (lds_ok) return run_lds<256, 256, 2, 2, SWIGLU, TO>(a, s);
             return run<T, TO, 256, 256, 2, 2, SWIGLU>(a, s);
         case Tile::Mid:
-            if (lds_ok) return run_lds<128, 128, 2, 2, SWIGLU>(a, s);
+            if constexpr (kLdsPath)
+                if (lds_ok) return run_lds<128, 128, 2, 2, SWIGLU, TO>(a, s);
             return run<T, TO, 128, 128, 2, 2, SWIGLU>(a, s);
         default: return run<T, TO, 32, 128, 1, 4, SWIGLU>(a, s);
     }
 }
 
 }  // namespace
+
+size_t gemm_split_scratch_bytes() {
+    return std::max(static_cast<size_t>(gemm_slots<256, 256>()) * 256 * 256,
+                    static_cast<size_t>(gemm_slots<128, 128>()) * 128 * 128) * sizeof(float);
+}
 
 hipError_t launch_gemm(DType dt, Epilogue epi, OutType ot, const GemmArgs& a, hipStream_t s) {
     const bool sw = epi == Epilogue::SwiGLU;

@@ -40,7 +40,7 @@ hipError_t launch_gate(DType dt, const GateArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- permutation
 // Work split of the permutation kernels: assignments are processed in chunks of
 // kPermChunk; per-chunk counts live in the workspace.
-constexpr int kPermChunk = 4096;
+constexpr int kPermChunk = 1024;
 inline int perm_chunks(int64_t n_assign) { return static_cast<int>((n_assign + kPermChunk - 1) / kPermChunk); }
 
 hipError_t launch_permute(const int32_t* topk_idx, int64_t n_assign, int top_k, int n_experts,
@@ -73,7 +73,15 @@ struct GemmArgs {
     void* out;                // [rows][N]
     int64_t ldo;              // output row stride (elements)
     const char* name;         // kernel name for the timing record
+    // split-K tail (bf16 large-tile path): tiles beyond the last whole round of `slots`
+    // resident workgroups are split along K into at most max_split chunks whose float32
+    // partial tiles go to `part` and are summed in chunk order by a second kernel.
+    // part == nullptr or max_split <= 1 disables the split.
+    float* part;              // [slots][TM][TN] float32 scratch
+    int max_split;
 };
+// Bytes of `part` scratch the large-tile GEMM may use (0 if it cannot split).
+size_t gemm_split_scratch_bytes();
 hipError_t launch_gemm(DType dt, Epilogue epi, OutType ot, const GemmArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- combine
