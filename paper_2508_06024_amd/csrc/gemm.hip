@@ -432,15 +432,16 @@ __host__ __device__ constexpr int gemm_slots() {
 // MFMAs of a slab's last k-step are deferred past the next barrier, where they cover the
 // latency of the next slab's first reads.
 template <int TM, int TN, int WM, int WN, bool SWIGLU, typename TO>
-__global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
-    static_assert(WM * WN == 4, "4 waves per workgroup");
+__global__ __launch_bounds__(64 * WM * WN, 1) void gemm_lds_kernel(GemmArgs a) {
+    constexpr int NW = WM * WN;                // waves per workgroup
+    static_assert(NW == 4 || NW == 8, "4 or 8 waves per workgroup");
     constexpr int MI = TM / WM / 32;           // token blocks of 32 per wave
     constexpr int NI = TN / WN / 32;           // weight blocks of 32 per wave
     constexpr int NOUT = SWIGLU ? TN / 2 : TN;
     constexpr int ROWS = TM + TN;
     constexpr int RB = 128;                    // bytes per tile row per slab (64 bf16)
     constexpr int STAGE = ROWS * RB;
-    constexpr int WROWS = ROWS / 4;            // tile rows loaded by each wave
+    constexpr int WROWS = ROWS / NW;           // tile rows loaded by each wave
     constexpr int LOADS = WROWS / 8;           // 8-row load instructions per wave per slab
     static_assert(MI >= 1 && NI >= 1, "wave tile of at least one 32x32 block");
     static_assert(WROWS % 8 == 0 && TM % WROWS == 0, "each wave loads only token or only weight rows");
@@ -452,30 +453,42 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
     const int ntn = (a.N + NOUT - 1) / NOUT;
     const int K = a.K;
     const int nk_all = K / 64;  // even: K is a multiple of 128 on this path
-    const SplitPlan sp = split_plan(count_tiles<TM>(a, ntn), a.part ? gemm_slots<TM, TN>() : 0, a.max_split, nk_all);
-    int bid, chunk = 0;
+    constexpr int P = gemm_slots<TM, TN>();  // workgroups of the launch, all resident at once
+    constexpr int XW = P / kXcds;            // workgroups on each XCD
+    const SplitPlan sp = split_plan(count_tiles<TM>(a, ntn), P, a.part ? a.max_split : 1, nk_all);
+    const int rounds = sp.full / P;
     const int p = blockIdx.x;
-    if (p < sp.full) {
-        bid = xcd_remap(p, sp.full);
+
+    // Persistent loop. Whole rounds first: workgroup p runs on XCD p % 8, and in round r
+    // takes logical tile (p % 8) * (rounds * XW) + r * XW + p / 8, so the XW workgroups of
+    // one XCD step together through consecutive tiles (m-tiles of one weight slab adjacent)
+    // and share their slabs in that XCD's L2 while they are at the same K. Then at most one
+    // unit of the tail (a whole tile, or one K chunk of a split tile).
+    for (int it = 0; it <= rounds; ++it) {
+    int bid, chunk = 0;
+    bool split = false;
+    if (it < rounds) {
+        bid = (p % kXcds) * (rounds * XW) + it * XW + p / kXcds;
     } else {
-        const int u = p - sp.full;
-        if (u >= sp.tail * sp.S) return;
-        bid = sp.full + u / sp.S;
-        chunk = u % sp.S;
+        if (p >= sp.tail * sp.S) break;
+        bid = sp.full + p / sp.S;
+        chunk = p % sp.S;
+        split = sp.S > 1;
     }
     TileInfo ti;
-    if (bid < 0 || !tile_of<TM>(a, ntn, bid, ti)) return;
-    const bool split = sp.S > 1 && p >= sp.full;
+    if (!tile_of<TM>(a, ntn, bid, ti)) break;
     const int kb = split ? chunk * sp.chunk_slabs : 0;                  // first slab of this unit
     const int nk = split ? std::min(nk_all, kb + sp.chunk_slabs) - kb : nk_all;
 
-    const int tid = threadIdx.x;
+    // Lane-derived addresses are rebuilt every tile from an opaque copy of the thread id:
+    // hoisted out of the tile loop they would stay live through the mainloop and spill.
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
     const int lane = tid & 63;
     const int wave = uniform(tid >> 6);
     const int wm = wave % WM;
     const int wn = wave / WM;
     const uint32_t row_bytes = static_cast<uint32_t>(K) * 2u;
-
     // this wave's rows [wave * WROWS, (wave + 1) * WROWS) are all token rows or all weight rows
     const bool tok_wave = wave * WROWS < TM;
     const bf16_t* wgrp = static_cast<const bf16_t*>(a.w) + static_cast<int64_t>(ti.group) * a.w_group_stride;
@@ -626,7 +639,7 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
 
     if (split) {
         // raw float32 partial tile [TM][TN] (weight rows in tile order) of this K chunk
-        float* part = a.part + static_cast<int64_t>(p - sp.full) * TM * TN;
+        float* part = a.part + static_cast<int64_t>(p) * TM * TN;
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
             const int trow = wm * WTOK + mi * 32 + l32;
@@ -642,9 +655,10 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
                 }
             }
         }
-        return;
+        continue;
     }
     write_tile32<TO, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+    }
 }
 
 // Sums the float32 partial tiles of the split tail in chunk order and applies the
@@ -722,15 +736,14 @@ hipError_t run(const GemmArgs& a, hipStream_t s) {
 
 template <int TM, int TN, int WM, int WN, bool SWIGLU, typename TO>
 hipError_t run_lds(const GemmArgs& a, hipStream_t s) {
-    int64_t grid = grid_size<TM, TN, SWIGLU>(a);
-    if (grid == 0) return hipSuccess;
+    if (grid_size<TM, TN, SWIGLU>(a) == 0) return hipSuccess;
     const bool can_split = a.part != nullptr && a.max_split > 1;
-    // whole rounds + a split tail of at most `slots` units
-    if (can_split) grid += gemm_slots<TM, TN>();
+    // persistent: one workgroup per resident slot, each looping over its tiles
+    const int64_t grid = gemm_slots<TM, TN>();
     {
         ProfileScope prof(a.name ? a.name : "gemm", s);
-        hipLaunchKernelGGL((gemm_lds_kernel<TM, TN, WM, WN, SWIGLU, TO>), dim3(static_cast<unsigned>(grid)), dim3(256),
-                           0, s, a);
+        hipLaunchKernelGGL((gemm_lds_kernel<TM, TN, WM, WN, SWIGLU, TO>), dim3(static_cast<unsigned>(grid)),
+                           dim3(64 * WM * WN), 0, s, a);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !can_split) return e;
@@ -778,7 +791,7 @@ hipError_t dispatch(const GemmArgs& a, hipStream_t s) {
     switch (choose_tile(a, SWIGLU, lds_ok)) {
         case Tile::Big:
             if constexpr (kLdsPath)
-                if (lds_ok) return run_lds<256, 256, 2, 2, SWIGLU, TO>(a, s);
+                if (lds_ok) return run_lds<256, 256, 4, 2, SWIGLU, TO>(a, s);
             return run<T, TO, 256, 256, 2, 2, SWIGLU>(a, s);
         case Tile::Mid:
             if constexpr (kLdsPath)
