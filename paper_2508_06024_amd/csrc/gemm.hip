@@ -5,28 +5,29 @@
 // Both operands are K-contiguous (token rows of the activations, rows of nn.Linear-style
 // weights), which is the layout the expert networks of Eq. 1 and the codec products use.
 // Groups are the per-expert segments produced by the permutation; their sizes stay on
-// the device. The grid is sized for the upper bound sum_e ceil(n_e / TM) <= ceil(rows/TM)
-// + groups; every workgroup counts the real tiles with a wave-parallel prefix sum over
-// the segment table, maps its id to a tile, and surplus workgroups exit.
+// the device. Every workgroup counts the real tiles with a wave-parallel prefix sum over
+// the segment table and maps logical tile ids to (group, m-tile, n-tile).
 //
 // Tile order (XCD-aware): workgroups are dispatched round-robin over the 8 XCDs, each with
-// its own L2. Workgroup p runs logical tile (p % 8) * ceil(tiles / 8) + p / 8, so every XCD
-// walks one contiguous stretch of the logical order, in which the m-tiles of one n-tile
-// (sharing the same weight rows) are consecutive: a weight slab is fetched into one L2
-// and reused there.
+// its own L2. Within a group, m-tiles go in bands of at most 8 and a band's n-tiles run in
+// order with its m-tiles adjacent, so a run of consecutive logical tiles shares a few
+// weight and token slabs. Each XCD walks one contiguous stretch of the logical order.
 //
-// Workgroup tile: TM token rows x TN weight rows, 4 waves in a WM x WN grid. Each K-step
+// Workgroup tile: TM token rows x TN weight rows, waves in a WM x WN grid. Each K-step
 // moves one 128-byte slab of every tile row (64 bf16 or 32 fp32 values) into LDS, double
-// buffered. LDS rows are 8 chunks of 16 bytes stored at chunk ^ (row & 7), which keeps
-// the 16-byte fragment reads free of bank conflicts. Weight rows feed the MFMA A operand
-// and token rows the B operand, so every lane ends with 4 consecutive output columns of
-// one token row (one 8- or 16-byte store).
+// buffered. Weight rows feed the MFMA A operand and token rows the B operand, so every
+// lane ends with 4 consecutive output columns of one token row (one 8- or 16-byte store).
 //
 // Two mainloops:
-//   * gemm_lds_kernel (bf16, K a multiple of 128, 32x32x16 MFMA): buffer loads write the
-//     slabs straight into LDS (no register staging); fragment reads run ahead of the MFMAs;
+//   * gemm_lds_kernel (bf16, K a multiple of 128, 32x32x16 MFMA): persistent (one
+//     workgroup per resident slot, each XCD's workgroups stepping through consecutive
+//     tiles together); buffer loads write the slabs straight into LDS (no register
+//     staging); the 256x256 tile runs 8 waves so that every SIMD holds two; the last
+//     partial round of tiles is split along K (float32 partials, summed in order by a
+//     second kernel);
 //   * gemm_kernel (any K that is a multiple of the 16-byte chunk, bf16 or fp32): loads
-//     through registers, zero-filling chunks past K.
+//     through registers, zero-filling chunks past K; one workgroup per tile, the
+//     workgroup-to-tile map rotated over the XCDs.
 //
 // SwiGLU epilogue: the weight tile holds TN/2 gate rows followed by the matching TN/2 up
 // rows; each wave owns equal gate and up slices, so silu(gate) * up is formed in registers.
@@ -77,15 +78,31 @@ __device__ __forceinline__ int count_tiles(const GemmArgs& a, int ntn) {
     return uniform(t);
 }
 
-// Tile with logical index bid (groups in order; within a group, n-tiles in order and the
-// m-tiles of one n-tile adjacent).
+// Position of tile `local` within one group of mtiles x ntn tiles: m-tiles go in
+// ceil(mtiles / 8) bands of near-equal size (4 to 8 m-tiles when there are enough); a
+// band's n-tiles run in order with the band's m-tiles adjacent. A run of 32 consecutive
+// tiles (one XCD's workgroups) then covers b m-tiles x 32/b n-tiles, which share
+// b + 32/b slabs (11 to 12 of 64) in that XCD's L2.
+__device__ __forceinline__ void band_decode(int local, int mtiles, int ntn, int& mt, int& nt) {
+    const int nbands = (mtiles + 7) / 8;
+    const int bsz = (mtiles + nbands - 1) / nbands;
+    const int band = local / (bsz * ntn);
+    const int m0 = band * bsz;
+    const int bm = std::min(bsz, mtiles - m0);  // m-tiles in this band
+    const int r = local - band * bsz * ntn;
+    nt = r / bm;
+    mt = m0 + (r - nt * bm);
+}
+
+// Tile with logical index bid (groups in order; within a group, banded as above).
 template <int TM>
 __device__ __forceinline__ bool tile_of(const GemmArgs& a, int ntn, int bid, TileInfo& ti) {
     if (a.seg == nullptr) {
         const int mtiles = static_cast<int>((a.rows + TM - 1) / TM);
-        const int mt = bid % mtiles;
+        int mt, nt;
+        band_decode(bid, mtiles, ntn, mt, nt);
         ti.group = 0;
-        ti.nt = bid / mtiles;
+        ti.nt = nt;
         ti.row0 = static_cast<int64_t>(mt) * TM;
         ti.valid = static_cast<int>(std::min<int64_t>(TM, a.rows - ti.row0));
         return true;
@@ -116,8 +133,9 @@ __device__ __forceinline__ bool tile_of(const GemmArgs& a, int ntn, int bid, Til
             const int mtiles = (ghi - glo + TM - 1) / TM;
             const int local = uniform(bid - first);
             ti.group = uniform(e0 + src);
-            ti.nt = local / mtiles;
-            const int mt = local - ti.nt * mtiles;
+            int mt, nt;
+            band_decode(local, mtiles, ntn, mt, nt);
+            ti.nt = nt;
             ti.row0 = glo + static_cast<int64_t>(mt) * TM;
             ti.valid = std::min(TM, ghi - static_cast<int>(ti.row0));
             return true;
