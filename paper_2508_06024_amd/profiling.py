@@ -5,8 +5,9 @@
         --kernel <substring> --copy-mib N --workload NAME --command "<cmd>" [-o out.json]
 
 HBM bytes of a kernel come from FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
-scaled by the ratio of the known bytes of a plain device copy (the benchmark's
---calibrate-copy-mib) to what the same counter reads for that copy.
+scaled by the ratio of the known bytes of a plain elementwise pass over N MiB (the
+benchmark's --calibrate-copy-mib: it reads N MiB and writes N MiB) to what the same
+counter reads for that pass.
 """
 from __future__ import annotations
 
@@ -76,9 +77,15 @@ def traffic(fetch_csv: str, write_csv: str, kernel: str, copy_mib: int):
         vals = [v for k in ks for v in d[k]]
         return sum(vals) / len(vals), len(vals)
 
+    def calib(d):
+        # the calibration kernel: the largest elementwise dispatch of the run
+        vals = [v for k in d if "elementwise" in k for v in d[k]]
+        if not vals:
+            raise KeyError("no elementwise calibration dispatch")
+        return max(vals)
+
     copy_kib = copy_mib * 1024.0
-    f_copy, _ = pick(fetch, "copyBuffer") if any("copyBuffer" in k for k in fetch) else pick(fetch, "elementwise")
-    w_copy, _ = pick(write, "copyBuffer") if any("copyBuffer" in k for k in write) else pick(write, "elementwise")
+    f_copy, w_copy = calib(fetch), calib(write)
     f_kib, nf = pick(fetch, kernel)
     w_kib, nw = pick(write, kernel)
     f_scale, w_scale = copy_kib / f_copy, copy_kib / w_copy
@@ -93,6 +100,8 @@ def main(argv=None):
     s = sub.add_parser("stats")
     s.add_argument("csv")
     s.add_argument("--command", required=True)
+    s.add_argument("--bench-json", help="the bench.py JSON line of the same run: its HIP-event "
+                                        "averages are listed beside the profiler's")
     s.add_argument("-o", "--out")
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
@@ -107,6 +116,16 @@ def main(argv=None):
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         text = stats_summary(a.csv, a.command)
+        if a.bench_json:
+            rec = json.loads(open(a.bench_json).read().strip().splitlines()[-1])
+            text += ("\nThe same run's bench.py line (library HIP events on the launch stream, timed "
+                     "region only):\n\n| library kernel name | launches per step | avg us |\n|---|---|---|\n")
+            for name, k in rec.get("kernels", {}).items():
+                if not name.startswith("stage:"):
+                    text += f"| {name} | {k['launches_per_step']:g} | {k['avg_us']} |\n"
+            text += (f"\nbench: {rec['value']} {rec['unit']}, {rec['ms_per_step']} ms/step; roofline kernel "
+                     f"{rec['roofline']['kernel']}: {rec['roofline']['achieved']} {rec['roofline']['unit']} "
+                     f"({rec['roofline']['frac']:.1%} of peak)\n")
     else:
         rec = traffic(a.fetch, a.write, a.kernel, a.copy_mib)
         rec.update({"kernel": a.name, "workload": a.workload, "command": a.command, "sources": a.sources,
