@@ -200,6 +200,12 @@ typedef struct {
 ec2moe_status ec2moe_profile_enable(int32_t enable);
 ec2moe_status ec2moe_profile_collect(ec2moe_kernel_stat* out, int32_t max_entries,
                                      int32_t* n_out);
+/*
+ * Restrict the timing to kernels named `name` (the names ec2moe_profile_collect
+ * reports, e.g. "expert_gate_up"); NULL records every kernel again. The string is
+ * copied. Lets a caller time one kernel without event records around the others.
+ */
+ec2moe_status ec2moe_profile_select(const char* name);
 
 #ifdef __cplusplus
 }

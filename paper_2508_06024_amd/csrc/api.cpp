@@ -186,6 +186,7 @@ struct ProfRecord {
 struct Profiler {
     std::mutex mu;
     bool enabled = false;
+    std::string only;  // record only kernels of this name (empty: all)
     std::vector<std::string> names;
     std::vector<ProfRecord> records;
     std::vector<hipEvent_t> pool;
@@ -218,7 +219,7 @@ Profiler& prof() {
 ProfileScope::ProfileScope(const char* name, hipStream_t s) : slot(-1), stream(s) {
     Profiler& p = prof();
     std::lock_guard<std::mutex> lk(p.mu);
-    if (!p.enabled) return;
+    if (!p.enabled || (!p.only.empty() && p.only != name)) return;
     ProfRecord r{p.name_id(name), p.get(), p.get()};
     if (!r.start || !r.stop) return;
     if (hipEventRecord(r.start, s) != hipSuccess) return;
@@ -473,6 +474,13 @@ ec2moe_status ec2moe_profile_enable(int32_t enable) {
     Profiler& p = prof();
     std::lock_guard<std::mutex> lk(p.mu);
     p.enabled = enable != 0;
+    return ok();
+}
+
+ec2moe_status ec2moe_profile_select(const char* name) {
+    Profiler& p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    p.only = name ? name : "";
     return ok();
 }
 

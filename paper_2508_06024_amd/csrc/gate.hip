@@ -1,7 +1,7 @@
 // Hardware-aware lightweight group gate (Local Expert Selection, Eq. 4; Lightweight
 // Group Gate Network, Eq. 5-7) and top-k selection, for gfx950.
 //
-// One workgroup (4 waves) takes 16 tokens. Phase 1 computes the M local and K group
+// One workgroup (4 or 8 waves) takes 16 tokens. Phase 1 computes the M local and K group
 // logits of those tokens with the matrix cores: gate-weight rows are the A operand,
 // token rows the B operand, and each wave contracts a quarter of d. Phase 2 adds the
 // four partial sums in a fixed order (deterministic). Phase 3 gives each wave four
@@ -17,6 +17,7 @@ namespace {
 constexpr int kTok = 16;           // tokens per workgroup
 constexpr int kMaxRowBlocks = 20;  // M + K <= 320 gate rows
 constexpr int kMaxGroups = 160;
+constexpr int kMaxExperts = 256;
 constexpr int kMaxTopK = 16;
 
 __device__ __forceinline__ bool is_cand(const uint64_t* mask, int e) {
@@ -42,6 +43,9 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     __shared__ float grp_max[WAVES][kMaxGroups];
     __shared__ float grp_sum[WAVES][kMaxGroups];
     __shared__ float grp_p[WAVES][kMaxGroups];
+    __shared__ float loc[WAVES][kMaxExperts];  // a wave's biased local logits, -inf off the candidate set
+    __shared__ float s_bl[kMaxExperts];        // b_local (0 if absent)
+    __shared__ float s_bg[kMaxGroups];         // b_global (0 if absent)
 
     constexpr int EPC = Elem<T>::kPerChunk;
     constexpr int SLICE = 4 * EPC;  // k covered by one matrix-core step
@@ -55,6 +59,10 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     const int M = p.n_experts, K = p.n_groups, d = p.d;
     const int R = M + K;
     const int t0 = blockIdx.x * kTok;
+
+    // biases staged once (read by the softmax phase; the barrier after phase 1 orders them)
+    for (int i = threadIdx.x; i < M; i += 64 * WAVES) s_bl[i] = p.b_local ? p.b_local[i] : 0.f;
+    for (int i = threadIdx.x; i < K; i += 64 * WAVES) s_bg[i] = p.b_global ? p.b_global[i] : 0.f;
 
     // ---------------- phase 1: partial logits over this wave's share of d
     int tok = t0 + (lane & 15);
@@ -119,62 +127,59 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     }
     __syncthreads();
 
-    // ---------------- phase 3: two-stage softmax, fusion, top-k; TPW tokens per wave
+    // ---------------- phase 3: two-stage softmax, fusion, top-k; TPW tokens per wave.
+    // Each wave works on its own LDS rows (loc, grp_*): wave-level ordering suffices.
     const float* logit = part;  // [row][token]
     const int Mk = M / K;
+    auto wave_sync = [] {
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+        __builtin_amdgcn_wave_barrier();
+    };
     for (int it = 0; it < TPW; ++it) {
         const int tl = wave * TPW + it;
         const int t = t0 + tl;
 
+        // biased local logits of the candidates (lane owns experts lane + 64 q)
+        float lv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = lane + 64 * q;
+            lv[q] = -INFINITY;
+            if (i < M && is_cand(p.mask, i)) lv[q] = logit[i * kTok + tl] + s_bl[i];
+            if (i < M) loc[wave][i] = lv[q];
+        }
+        wave_sync();
+
         // stage 2 statistics per group over its candidates: max and sum of exp
         for (int kk = lane; kk < K; kk += 64) {
             float m = -INFINITY;
-            for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) {
-                if (is_cand(p.mask, i)) {
-                    const float l = logit[i * kTok + tl] + (p.b_local ? p.b_local[i] : 0.f);
-                    m = fmaxf(m, l);
-                }
-            }
+            for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) m = fmaxf(m, loc[wave][i]);
             float sum = 0.f;
-            if (m != -INFINITY) {
+            if (m != -INFINITY)
                 for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) {
-                    if (is_cand(p.mask, i)) {
-                        const float l = logit[i * kTok + tl] + (p.b_local ? p.b_local[i] : 0.f);
-                        sum += expf(l - m);
-                    }
+                    const float l = loc[wave][i];
+                    if (l != -INFINITY) sum += expf(l - m);
                 }
-            }
             grp_max[wave][kk] = m;
             grp_sum[wave][kk] = sum;
         }
-        __syncthreads();
+        wave_sync();
 
         // stage 1: softmax over the groups that hold a candidate
         float lmax = -INFINITY;
-        for (int kk = lane; kk < K; kk += 64) {
-            if (grp_max[wave][kk] != -INFINITY) {
-                const float lg = logit[(M + kk) * kTok + tl] + (p.b_global ? p.b_global[kk] : 0.f);
-                lmax = fmaxf(lmax, lg);
-            }
-        }
+        for (int kk = lane; kk < K; kk += 64)
+            if (grp_max[wave][kk] != -INFINITY) lmax = fmaxf(lmax, logit[(M + kk) * kTok + tl] + s_bg[kk]);
         const float gmax = wave_max(lmax);
         float lsum = 0.f;
-        for (int kk = lane; kk < K; kk += 64) {
-            if (grp_max[wave][kk] != -INFINITY) {
-                const float lg = logit[(M + kk) * kTok + tl] + (p.b_global ? p.b_global[kk] : 0.f);
-                lsum += expf(lg - gmax);
-            }
-        }
+        for (int kk = lane; kk < K; kk += 64)
+            if (grp_max[wave][kk] != -INFINITY) lsum += expf(logit[(M + kk) * kTok + tl] + s_bg[kk] - gmax);
         const float gsum = wave_sum(lsum);
         for (int kk = lane; kk < K; kk += 64) {
             float pg = 0.f;
-            if (grp_max[wave][kk] != -INFINITY) {
-                const float lg = logit[(M + kk) * kTok + tl] + (p.b_global ? p.b_global[kk] : 0.f);
-                pg = expf(lg - gmax) / gsum;
-            }
+            if (grp_max[wave][kk] != -INFINITY) pg = expf(logit[(M + kk) * kTok + tl] + s_bg[kk] - gmax) / gsum;
             grp_p[wave][kk] = pg;
         }
-        __syncthreads();
+        wave_sync();
 
         // fusion, Eq. 7: g_i = p_group^(k) * p_local,i^(k); -1 marks a non-candidate
         float gv[4];
@@ -182,10 +187,9 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
         for (int q = 0; q < 4; ++q) {
             const int i = lane + 64 * q;
             gv[q] = -1.f;
-            if (i < M && is_cand(p.mask, i)) {
+            if (lv[q] != -INFINITY) {
                 const int kk = i / Mk;
-                const float l = logit[i * kTok + tl] + (p.b_local ? p.b_local[i] : 0.f);
-                const float pl = expf(l - grp_max[wave][kk]) / grp_sum[wave][kk];
+                const float pl = expf(lv[q] - grp_max[wave][kk]) / grp_sum[wave][kk];
                 gv[q] = grp_p[wave][kk] * pl;
             }
             if (p.probs && t < p.n_tokens && i < M)
@@ -243,7 +247,7 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
                 }
             }
         }
-        __syncthreads();
+        wave_sync();  // the next token rewrites this wave's rows
     }
 }
 

@@ -181,7 +181,12 @@ __device__ __forceinline__ SplitPlan split_plan(int total, int slots, int max_sp
     return sp;
 }
 
-__device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
+// silu(g) = g / (1 + e^-g) with the hardware 2^x and reciprocal (each within about 1 ulp),
+// e^-g = 2^(-g log2 e); a very negative g gives e^-g = inf and a zero reciprocal.
+__device__ __forceinline__ float silu(float g) {
+    const float e = __builtin_amdgcn_exp2f(-g * 1.4426950408889634f);
+    return g * __builtin_amdgcn_rcpf(1.0f + e);
+}
 
 template <typename TO>
 __device__ __forceinline__ void store4(TO* dst, f32x4 v);

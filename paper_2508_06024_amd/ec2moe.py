@@ -70,6 +70,7 @@ _SIGS = {
     "ec2moe_last_error": [],
     "ec2moe_profile_enable": [ctypes.c_int32],
     "ec2moe_profile_collect": [ctypes.POINTER(KernelStat), ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)],
+    "ec2moe_profile_select": [ctypes.c_char_p],
 }
 for _name, _args in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -305,6 +306,11 @@ def lowrank_decode(z, u_hat, v_hat, ws=None):
 
 def profile_enable(on: bool = True):
     _check(_lib.ec2moe_profile_enable(1 if on else 0))
+
+
+def profile_select(name=None):
+    """Time only the kernels called `name` (None: all)."""
+    _check(_lib.ec2moe_profile_select(name.encode() if name else None))
 
 
 def profile_collect(max_entries: int = 64):
