@@ -143,7 +143,7 @@ ec2moe_status check_codec_desc(const ec2moe_codec_desc* d) {
 
 int choose_splits(int M, int N, int K) {
     const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
-    int s = std::max(1, 512 / std::max(1, tiles));
+    int s = std::max(1, 256 / std::max(1, tiles));  // about one workgroup per CU
     s = std::min(s, std::max(1, K / 64));
     return std::min(s, 64);
 }

@@ -20,20 +20,37 @@ __device__ __forceinline__ float ld(const void* p, int64_t i) {
     return Elem<T>::to_f32(static_cast<const T*>(p)[i]);
 }
 
+// dst[c][r] = src[r][c] through 64x64 tiles in LDS; 16-byte global loads and stores
+// (rows and cols multiples of 16 / sizeof(T), both pointers 16-byte aligned). The LDS row
+// pitch is an odd number of 4-byte words, so a column walk hits distinct banks.
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ src, int rows, int cols,
                                                         T* __restrict__ dst) {
-    __shared__ T tile[32][33];
-    const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
-    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
-    for (int i = ty; i < 32; i += 8) {
-        const int r = r0 + i, c = c0 + tx;
-        if (r < rows && c < cols) tile[i][tx] = src[static_cast<int64_t>(r) * cols + c];
+    constexpr int EPC = 16 / static_cast<int>(sizeof(T));  // elements per 16-byte chunk
+    constexpr int CPR = 64 / EPC;                           // chunks per 64-element tile row
+    __shared__ T tile[64][64 + 4 / sizeof(T)];
+    const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+    for (int i = threadIdx.x; i < 64 * CPR; i += 256) {
+        const int r = i / CPR, ch = i % CPR;
+        const int gr = r0 + r, gc = c0 + ch * EPC;
+        if (gr < rows && gc < cols) {
+            const uint4 v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(gr) * cols + gc);
+            const T* e = reinterpret_cast<const T*>(&v);
+#pragma unroll
+            for (int j = 0; j < EPC; ++j) tile[r][ch * EPC + j] = e[j];
+        }
     }
     __syncthreads();
-    for (int i = ty; i < 32; i += 8) {
-        const int c = c0 + i, r = r0 + tx;
-        if (r < rows && c < cols) dst[static_cast<int64_t>(c) * rows + r] = tile[tx][i];
+    for (int i = threadIdx.x; i < 64 * CPR; i += 256) {
+        const int oc = i / CPR, ch = i % CPR;  // output row c0 + oc, output columns r0 + ch * EPC ..
+        const int gc = c0 + oc, gr = r0 + ch * EPC;
+        if (gc < cols && gr < rows) {
+            uint4 v;
+            T* e = reinterpret_cast<T*>(&v);
+#pragma unroll
+            for (int j = 0; j < EPC; ++j) e[j] = tile[ch * EPC + j][oc];
+            *reinterpret_cast<uint4*>(dst + static_cast<int64_t>(gc) * rows + gr) = v;
+        }
     }
 }
 
@@ -111,13 +128,29 @@ __global__ __launch_bounds__(256) void small_gemm_kernel(SmallGemmArgs g) {
 }
 
 template <typename TO>
+__device__ __forceinline__ void put4(TO* dst, f32x4 v) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dst[i] = Elem<TO>::from_f32(v[i]);
+}
+
+// out[i] = sum over p of part[p][i], in p order (deterministic); four elements per thread
+// (mn a multiple of 4), the loads of up to 8 partials in flight at once.
+template <typename TO>
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part, int64_t mn, int splits,
                                                            TO* __restrict__ out) {
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < mn;
-         i += static_cast<int64_t>(gridDim.x) * 256) {
-        float s = part[i];
-        for (int p = 1; p < splits; ++p) s += part[p * mn + i];
-        out[i] = Elem<TO>::from_f32(s);
+    for (int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4; i < mn;
+         i += static_cast<int64_t>(gridDim.x) * 256 * 4) {
+        f32x4 s = *reinterpret_cast<const f32x4*>(part + i);
+        for (int p0 = 1; p0 < splits; p0 += 8) {
+            f32x4 v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (p0 + j < splits) v[j] = *reinterpret_cast<const f32x4*>(part + (p0 + j) * mn + i);
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (p0 + j < splits) s += v[j];
+        }
+        put4<TO>(out + i, s);
     }
 }
 
@@ -131,7 +164,7 @@ hipError_t small_gemm_t(const SmallGemmArgs& g, hipStream_t s) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t mn = static_cast<int64_t>(g.M) * g.N;
-    const int rgrid = static_cast<int>(std::min<int64_t>((mn + 255) / 256, 4096));
+    const int rgrid = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 4096));
     std::string rname = std::string(g.name ? g.name : "small_gemm") + "_reduce";
     ProfileScope prof(rname.c_str(), s);
     if (g.out_dt == DType::BF16)
@@ -146,7 +179,7 @@ hipError_t small_gemm_t(const SmallGemmArgs& g, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_transpose(DType dt, const void* src, int rows, int cols, void* dst, hipStream_t s) {
-    dim3 grid((cols + 31) / 32, (rows + 31) / 32);
+    dim3 grid((cols + 63) / 64, (rows + 63) / 64);
     ProfileScope prof("transpose", s);
     if (dt == DType::BF16)
         hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, dim3(256), 0, s, static_cast<const bf16_t*>(src), rows,

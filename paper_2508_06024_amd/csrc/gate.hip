@@ -4,10 +4,10 @@
 // One workgroup (4 or 8 waves) takes 16 tokens. Phase 1 computes the M local and K group
 // logits of those tokens with the matrix cores: gate-weight rows are the A operand,
 // token rows the B operand, and each wave contracts a quarter of d. Phase 2 adds the
-// four partial sums in a fixed order (deterministic). Phase 3 gives each wave four
-// tokens: masked group softmax (stage 1), masked in-group softmax (stage 2), the
-// product g_i = p_group^(k) * p_local,i^(k), top-k by wave shuffles with ties to the
-// lower expert index, and renormalisation of the selected weights.
+// partial sums in a fixed order (deterministic). Phase 3 gives each wave its tokens:
+// masked group softmax (stage 1), masked in-group softmax (stage 2), the product
+// g_i = p_group^(k) * p_local,i^(k), top-k by rank (ties to the lower expert index), and
+// renormalisation of the selected weights.
 #include "device_common.h"
 #include "internal.h"
 
@@ -24,17 +24,16 @@ __device__ __forceinline__ bool is_cand(const uint64_t* mask, int e) {
     return (mask[e >> 6] >> (e & 63)) & 1ull;
 }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+// Keeps a kernel-argument value in a scalar register: left alone, the compiler may reload
+// it from the argument segment at every use, and each reload waits on that memory.
+template <typename V>
+__device__ __forceinline__ V pin(V v) {
+    asm volatile("" : "+s"(v));
     return v;
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-    return v;
-}
+// e^x with the hardware 2^x (within about 1 ulp); the gate's probabilities are float32
+__device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
 
 // NRB: blocks of 16 gate rows (M + K <= 16 * NRB); WAVES: waves splitting d.
 template <typename T, int NRB, int WAVES>
@@ -42,31 +41,45 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     extern __shared__ float part[];  // [WAVES][NRB*16 rows][16 tokens], then the sums in wave 0's slot
     __shared__ float grp_max[WAVES][kMaxGroups];
     __shared__ float grp_sum[WAVES][kMaxGroups];
-    __shared__ float grp_p[WAVES][kMaxGroups];
-    __shared__ float loc[WAVES][kMaxExperts];  // a wave's biased local logits, -inf off the candidate set
+    __shared__ float grp_lg[WAVES][kMaxGroups];  // a wave's biased group logits
+    __shared__ float loc[WAVES][kMaxExperts];  // a wave's biased local logits (-inf off the candidate set), then g
+    __shared__ float sel_g[WAVES][kMaxTopK];
+    __shared__ int sel_i[WAVES][kMaxTopK];
     __shared__ float s_bl[kMaxExperts];        // b_local (0 if absent)
     __shared__ float s_bg[kMaxGroups];         // b_global (0 if absent)
+    __shared__ unsigned char s_cand[kMaxExperts];  // candidate flags of the mask
 
     constexpr int EPC = Elem<T>::kPerChunk;
     constexpr int SLICE = 4 * EPC;  // k covered by one matrix-core step
     // k-slices whose loads are issued together: deep for few gate rows, shallow for many
-    constexpr int U = 16 / (NRB + 1) < 1 ? 1 : (16 / (NRB + 1) > 8 ? 8 : 16 / (NRB + 1));
+    // (U (NRB + 1) uint4 registers; the budget shrinks with more waves per SIMD)
+    constexpr int UB = WAVES <= 8 ? 40 : 16;
+    constexpr int U = UB / (NRB + 1) < 1 ? 1 : (UB / (NRB + 1) > 8 ? 8 : UB / (NRB + 1));
     constexpr int THREADS = 64 * WAVES;
     constexpr int TPW = kTok / WAVES;  // tokens per wave in the softmax phase
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int g4 = lane >> 4;
-    const int M = p.n_experts, K = p.n_groups, d = p.d;
+    const int M = pin(p.n_experts), K = pin(p.n_groups), d = pin(p.d);
+    const int KT = pin(p.top_k);
+    const int n_tokens = pin(p.n_tokens);
+    const bool renormalize = pin(static_cast<int>(p.renormalize)) != 0;
+    float* const probs = pin(p.probs);
+    int32_t* const topk_idx = pin(p.topk_idx);
+    float* const topk_w = pin(p.topk_w);
     const int R = M + K;
     const int t0 = blockIdx.x * kTok;
 
     // biases staged once (read by the softmax phase; the barrier after phase 1 orders them)
-    for (int i = threadIdx.x; i < M; i += 64 * WAVES) s_bl[i] = p.b_local ? p.b_local[i] : 0.f;
+    for (int i = threadIdx.x; i < M; i += 64 * WAVES) {
+        s_bl[i] = p.b_local ? p.b_local[i] : 0.f;
+        s_cand[i] = is_cand(p.mask, i) ? 1 : 0;
+    }
     for (int i = threadIdx.x; i < K; i += 64 * WAVES) s_bg[i] = p.b_global ? p.b_global[i] : 0.f;
 
     // ---------------- phase 1: partial logits over this wave's share of d
     int tok = t0 + (lane & 15);
-    if (tok >= p.n_tokens) tok = p.n_tokens - 1;
+    if (tok >= n_tokens) tok = n_tokens - 1;
     const T* xrow = static_cast<const T*>(p.x) + static_cast<size_t>(tok) * d + g4 * EPC;
     const T* wrow[NRB];
     bool wvalid[NRB];
@@ -128,58 +141,56 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     __syncthreads();
 
     // ---------------- phase 3: two-stage softmax, fusion, top-k; TPW tokens per wave.
-    // Each wave works on its own LDS rows (loc, grp_*): wave-level ordering suffices.
+    // Each wave works on its own LDS rows with wave-level ordering only. Values every lane
+    // needs (group softmax, the rank order) are read back from LDS by all lanes in the
+    // same order instead of cross-lane shuffles, whose latency chains dominated.
     const float* logit = part;  // [row][token]
     const int Mk = M / K;
+    const int Mpad = (M + 3) & ~3;
     auto wave_sync = [] {
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS traffic is done
         __builtin_amdgcn_wave_barrier();
     };
     for (int it = 0; it < TPW; ++it) {
         const int tl = wave * TPW + it;
         const int t = t0 + tl;
+        float* gl = loc[wave];
 
-        // biased local logits of the candidates (lane owns experts lane + 64 q)
+        // biased logits: local ones of the candidates (lane owns experts lane + 64 q), group ones
         float lv[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int i = lane + 64 * q;
             lv[q] = -INFINITY;
-            if (i < M && is_cand(p.mask, i)) lv[q] = logit[i * kTok + tl] + s_bl[i];
-            if (i < M) loc[wave][i] = lv[q];
+            if (i < M && s_cand[i]) lv[q] = logit[i * kTok + tl] + s_bl[i];
+            if (i < M) gl[i] = lv[q];
         }
+        for (int kk = lane; kk < K; kk += 64) grp_lg[wave][kk] = logit[(M + kk) * kTok + tl] + s_bg[kk];
         wave_sync();
 
         // stage 2 statistics per group over its candidates: max and sum of exp
         for (int kk = lane; kk < K; kk += 64) {
             float m = -INFINITY;
-            for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) m = fmaxf(m, loc[wave][i]);
+            for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) m = fmaxf(m, gl[i]);
             float sum = 0.f;
             if (m != -INFINITY)
                 for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) {
-                    const float l = loc[wave][i];
-                    if (l != -INFINITY) sum += expf(l - m);
+                    const float l = gl[i];
+                    if (l != -INFINITY) sum += fast_exp(l - m);
                 }
             grp_max[wave][kk] = m;
             grp_sum[wave][kk] = sum;
         }
         wave_sync();
 
-        // stage 1: softmax over the groups that hold a candidate
-        float lmax = -INFINITY;
-        for (int kk = lane; kk < K; kk += 64)
-            if (grp_max[wave][kk] != -INFINITY) lmax = fmaxf(lmax, logit[(M + kk) * kTok + tl] + s_bg[kk]);
-        const float gmax = wave_max(lmax);
-        float lsum = 0.f;
-        for (int kk = lane; kk < K; kk += 64)
-            if (grp_max[wave][kk] != -INFINITY) lsum += expf(logit[(M + kk) * kTok + tl] + s_bg[kk] - gmax);
-        const float gsum = wave_sum(lsum);
-        for (int kk = lane; kk < K; kk += 64) {
-            float pg = 0.f;
-            if (grp_max[wave][kk] != -INFINITY) pg = expf(logit[(M + kk) * kTok + tl] + s_bg[kk] - gmax) / gsum;
-            grp_p[wave][kk] = pg;
-        }
-        wave_sync();
+        // stage 1: softmax over the groups that hold a candidate (every lane, group order)
+        float gmax = -INFINITY;
+        for (int kk = 0; kk < K; ++kk)
+            if (grp_max[wave][kk] != -INFINITY) gmax = fmaxf(gmax, grp_lg[wave][kk]);
+        float gsum = 0.f;
+        for (int kk = 0; kk < K; ++kk)
+            if (grp_max[wave][kk] != -INFINITY) gsum += fast_exp(grp_lg[wave][kk] - gmax);
+        const float rgsum = __builtin_amdgcn_rcpf(gsum);
 
         // fusion, Eq. 7: g_i = p_group^(k) * p_local,i^(k); -1 marks a non-candidate
         float gv[4];
@@ -189,63 +200,50 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
             gv[q] = -1.f;
             if (lv[q] != -INFINITY) {
                 const int kk = i / Mk;
-                const float pl = expf(lv[q] - grp_max[wave][kk]) / grp_sum[wave][kk];
-                gv[q] = grp_p[wave][kk] * pl;
+                const float pg = fast_exp(grp_lg[wave][kk] - gmax) * rgsum;
+                const float pl = fast_exp(lv[q] - grp_max[wave][kk]) * __builtin_amdgcn_rcpf(grp_sum[wave][kk]);
+                gv[q] = pg * pl;
             }
-            if (p.probs && t < p.n_tokens && i < M)
-                p.probs[static_cast<size_t>(t) * M + i] = gv[q] < 0.f ? 0.f : gv[q];
+            if (probs && t < n_tokens && i < M) probs[static_cast<size_t>(t) * M + i] = gv[q] < 0.f ? 0.f : gv[q];
         }
+        wave_sync();  // every lane is done with the local logits
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = lane + 64 * q;
+            if (i < Mpad) gl[i] = i < M ? gv[q] : -1.f;
+        }
+        wave_sync();
 
-        // top-k: k rounds of a wave argmax on (g, -index)
-        int sel_i[kMaxTopK];
-        float sel_g[kMaxTopK];
+        // top-k by rank: a larger g, or an equal g at a lower index, ranks first
 #pragma unroll
-        for (int j = 0; j < kMaxTopK; ++j) {
-            sel_i[j] = 0;
-            sel_g[j] = 0.f;
-            if (j < p.top_k) {
-                float bv = -3.f;
-                int bi = 0x7fffffff;
+        for (int q = 0; q < 4; ++q) {
+            const int i = lane + 64 * q;
+            if (gv[q] >= 0.f) {
+                const float g = gv[q];
+                int r = 0;
+                for (int j = 0; j < Mpad; j += 4) {
+                    const f32x4 o = *reinterpret_cast<const f32x4*>(gl + j);
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    if (gv[q] > bv) {  // ascending index: strict > keeps the lower index on ties
-                        bv = gv[q];
-                        bi = lane + 64 * q;
-                    }
+                    for (int u = 0; u < 4; ++u) r += (o[u] > g || (o[u] == g && j + u < i)) ? 1 : 0;
                 }
-#pragma unroll
-                for (int off = 32; off >= 1; off >>= 1) {
-                    const float ov = __shfl_xor(bv, off);
-                    const int oi = __shfl_xor(bi, off);
-                    if (ov > bv || (ov == bv && oi < bi)) {
-                        bv = ov;
-                        bi = oi;
-                    }
+                if (r < KT) {
+                    sel_g[wave][r] = g;
+                    sel_i[wave][r] = i;
                 }
-                sel_i[j] = bi;
-                sel_g[j] = bv;
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    if (lane + 64 * q == bi) gv[q] = -2.f;
             }
         }
+        wave_sync();
 
+        // slot j of the output (lane j); renormalised by the sum in slot order
         float denom = 1.f;
-        if (p.renormalize) {
+        if (renormalize) {
             float sum = 0.f;
-#pragma unroll
-            for (int j = 0; j < kMaxTopK; ++j)
-                if (j < p.top_k) sum += sel_g[j];
+            for (int j = 0; j < KT; ++j) sum += sel_g[wave][j];
             denom = sum;
         }
-        if (t < p.n_tokens) {
-#pragma unroll
-            for (int j = 0; j < kMaxTopK; ++j) {
-                if (j < p.top_k && lane == j) {
-                    p.topk_idx[static_cast<size_t>(t) * p.top_k + j] = sel_i[j];
-                    p.topk_w[static_cast<size_t>(t) * p.top_k + j] = p.renormalize ? sel_g[j] / denom : sel_g[j];
-                }
-            }
+        if (t < n_tokens && lane < KT) {
+            topk_idx[static_cast<size_t>(t) * KT + lane] = sel_i[wave][lane];
+            topk_w[static_cast<size_t>(t) * KT + lane] = renormalize ? sel_g[wave][lane] / denom : sel_g[wave][lane];
         }
         wave_sync();  // the next token rewrites this wave's rows
     }
@@ -267,10 +265,15 @@ hipError_t launch_waves(const GateArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-// 8 waves split d when their partial logits fit in 64 KB of LDS and d splits evenly; else 4
+// 8 waves split d when their partial logits fit in 64 KB of LDS and d splits evenly, else
+// 4; with fewer token blocks than CUs (small batches) 16 waves shorten each wave's walk
+// over d.
 template <typename T, int NRB>
 hipError_t launch_nrb(const GateArgs& a, hipStream_t s) {
     constexpr int SLICE = 4 * Elem<T>::kPerChunk;
+    const int blocks = (a.n_tokens + kTok - 1) / kTok;
+    if constexpr (NRB <= 6)
+        if (blocks < 256 && a.d % (16 * SLICE) == 0) return launch_waves<T, NRB, 16>(a, s);
     if (NRB <= 8 && a.d % (8 * SLICE) == 0) return launch_waves<T, NRB, 8>(a, s);
     return launch_waves<T, NRB, 4>(a, s);
 }
