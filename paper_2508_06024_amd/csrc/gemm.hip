@@ -18,13 +18,16 @@
 // buffered. Weight rows feed the MFMA A operand and token rows the B operand, so every
 // lane ends with 4 consecutive output columns of one token row (one 8- or 16-byte store).
 //
-// Two mainloops:
-//   * gemm_lds_kernel (bf16, K a multiple of 128, 32x32x16 MFMA): persistent (one
-//     workgroup per resident slot, each XCD's workgroups stepping through consecutive
-//     tiles together); buffer loads write the slabs straight into LDS (no register
-//     staging); the 256x256 tile runs 8 waves so that every SIMD holds two; the last
-//     partial round of tiles is split along K (float32 partials, summed in order by a
-//     second kernel);
+// Three mainloops:
+//   * gemm_pp_kernel (bf16 256x256 tiles, K a multiple of 128, 32x32x16 MFMA): persistent
+//     (one workgroup per CU, each XCD's workgroups stepping through consecutive tiles
+//     together); buffer loads write the slabs straight into LDS (no register staging);
+//     8 waves in two groups of one wave per SIMD that alternate between a phase of
+//     matrix-core work and a phase of memory work, so every SIMD always has a wave
+//     issuing MFMAs; the last partial round of tiles is split along K (float32 partials,
+//     summed in order by a second kernel);
+//   * gemm_lds_kernel (bf16 128x128 tiles, same loads and split): 4 waves that each
+//     interleave their own loads, fragment reads and MFMAs;
 //   * gemm_kernel (any K that is a multiple of the 16-byte chunk, bf16 or fp32): loads
 //     through registers, zero-filling chunks past K; one workgroup per tile, the
 //     workgroup-to-tile map rotated over the XCDs.
@@ -684,6 +687,213 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_lds_kernel(GemmArgs a) {
     }
 }
 
+// 8-wave ping-pong mainloop for the 256x256 tile. Waves 0-3 (group 0, token loaders) and
+// waves 4-7 (group 1, weight loaders) sit one per SIMD each; the groups alternate between a
+// compute phase (all 32 MFMAs of one slab from registers, at raised priority) and a memory
+// phase (fragment reads of the next slab, buffer loads), with a workgroup barrier between
+// phases, so on every SIMD one wave issues MFMAs while the other waits on memory.
+//   group 0, slab s: issue token rows of slab s+1 | read slab s | barrier | MFMA slab s |
+//                    wait own loads | barrier
+//   group 1, slab s: MFMA slab s-1 | barrier | read slab s, then issue weight rows of slab
+//                    s+2 into the same stage | wait loads of slab s+1 | barrier
+template <bool SWIGLU, typename TO>
+__global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
+    constexpr int TM = 256, TN = 256, WM = 4, WN = 2, NW = 8;
+    constexpr int MI = TM / WM / 32;           // 2
+    constexpr int NI = TN / WN / 32;           // 4
+    constexpr int NOUT = SWIGLU ? TN / 2 : TN;
+    constexpr int ROWS = TM + TN;
+    constexpr int RB = 128;
+    constexpr int STAGE = ROWS * RB;
+    constexpr int WROWS = ROWS / NW;           // 64
+    constexpr int LOADS = WROWS / 8;           // 8
+    static_assert(LOADS < 16, "vmcnt immediate");
+
+    __shared__ __attribute__((aligned(1024))) char lds0[STAGE];
+    __shared__ __attribute__((aligned(1024))) char lds1[STAGE];
+
+    const int ntn = (a.N + NOUT - 1) / NOUT;
+    const int K = a.K;
+    const int nk_all = K / 64;
+    constexpr int P = gemm_slots<TM, TN>();
+    constexpr int XW = P / kXcds;
+    const SplitPlan sp = split_plan(count_tiles<TM>(a, ntn), P, a.part ? a.max_split : 1, nk_all);
+    const int rounds = sp.full / P;
+    const int p = blockIdx.x;
+
+    for (int it = 0; it <= rounds; ++it) {
+    int bid, chunk = 0;
+    bool split = false;
+    if (it < rounds) {
+        bid = (p % kXcds) * (rounds * XW) + it * XW + p / kXcds;
+    } else {
+        if (p >= sp.tail * sp.S) break;
+        bid = sp.full + p / sp.S;
+        chunk = p % sp.S;
+        split = sp.S > 1;
+    }
+    TileInfo ti;
+    if (!tile_of<TM>(a, ntn, bid, ti)) break;
+    const int kb = split ? chunk * sp.chunk_slabs : 0;
+    const int nk = split ? std::min(nk_all, kb + sp.chunk_slabs) - kb : nk_all;
+
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63;
+    const int wave = uniform(tid >> 6);
+    const int wm = wave % WM;
+    const int wn = wave / WM;                 // also the group
+    const uint32_t row_bytes = static_cast<uint32_t>(K) * 2u;
+    const bool tok_wave = wave * WROWS < TM;  // group 0
+    const bf16_t* wgrp = static_cast<const bf16_t*>(a.w) + static_cast<int64_t>(ti.group) * a.w_group_stride;
+    const i32x4 rs = tok_wave ? buffer_rsrc(a.tok, static_cast<uint32_t>(a.src_rows) * row_bytes)
+                              : buffer_rsrc(wgrp, static_cast<uint32_t>(a.w_rows) * row_bytes);
+    uint32_t voff[LOADS];
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+        const int row = wave * WROWS + i * 8 + (lane >> 3);
+        const uint32_t chunk_off = static_cast<uint32_t>(((lane & 7) ^ ((row >> 1) & 7)) * 16);
+        if (tok_wave) {
+            const int r = std::min(row, ti.valid - 1);
+            const int64_t pr = ti.row0 + r;
+            const int64_t src = a.row_index ? a.row_index[pr] : pr;
+            voff[i] = static_cast<uint32_t>(src) * row_bytes + chunk_off;
+        } else {
+            voff[i] = static_cast<uint32_t>(weight_row<TN, SWIGLU>(a, ti.nt, row - TM)) * row_bytes + chunk_off;
+        }
+    }
+    auto issue_slab = [&](int ks, char* stage) {
+        const int soff = (kb + ks) * RB;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            lds_void* dst = reinterpret_cast<lds_void*>(
+                reinterpret_cast<uintptr_t>(stage + (wave * WROWS + i * 8) * RB));
+            raw_buffer_load_lds(rs, dst, 16, static_cast<int>(voff[i]), soff, 0, 0);
+        }
+    };
+
+    const int l32 = lane & 31;
+    const int lh = lane >> 5;
+    const int sw = (l32 >> 1) & 7;
+    constexpr int WTOK = TM / WM;
+    constexpr int WW = SWIGLU ? TN / 2 / WN : TN / WN;
+    int off_t[4], off_w[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const int ch = ((2 * s + lh) ^ sw) * 16;
+        off_t[s] = (wm * WTOK + l32) * RB + ch;
+        off_w[s] = (TM + wn * WW + l32) * RB + ch;
+    }
+    auto wblk = [](int ni) constexpr {
+        if (SWIGLU) {
+            constexpr int HALF = NI / 2;
+            return (ni < HALF ? 0 : TN / 2) + (ni % HALF) * 32;
+        }
+        return ni * 32;
+    };
+
+    f32x16 acc[NI][MI];
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[ni][mi][r] = 0.f;
+
+    uint4 fa[4][NI], fb[4][MI];  // one slab of fragments
+    auto read_slab = [&](const char* base) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) fa[s][ni] = *reinterpret_cast<const uint4*>(base + off_w[s] + wblk(ni) * RB);
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi) fb[s][mi] = *reinterpret_cast<const uint4*>(base + off_t[s] + mi * 32 * RB);
+        }
+    };
+    auto mma_slab = [&]() {
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+                for (int mi = 0; mi < MI; ++mi)
+                    acc[ni][mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[s][ni]),
+                                                                         __builtin_bit_cast(bf16x8, fb[s][mi]),
+                                                                         acc[ni][mi], 0, 0, 0);
+        __builtin_amdgcn_s_setprio(0);
+    };
+    auto barrier = [&]() {
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_barrier" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    if (nk > 0) {  // nk is even and the same for every wave
+        issue_slab(0, lds0);
+        issue_slab(1, lds1);
+        __builtin_amdgcn_s_waitcnt(0x0070 | LOADS);  // own rows of slab 0 landed
+        barrier();
+        if (tok_wave) {
+            auto slab0 = [&](const char* cur, char* nxt, int s) {
+                if (s >= 1 && s + 1 < nk) issue_slab(s + 1, nxt);
+                read_slab(cur);
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+                barrier();
+                mma_slab();
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_waitcnt(0x0070);  // token rows of slab s+1 landed
+                barrier();
+            };
+            for (int s = 0; s < nk; s += 2) {
+                slab0(lds0, lds1, s);
+                slab0(lds1, lds0, s + 1);
+            }
+        } else {
+            auto slab1 = [&](char* cur, int s) {
+                if (s > 0) mma_slab();
+                barrier();
+                read_slab(cur);
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this stage's reads done
+                if (s + 2 < nk) {
+                    issue_slab(s + 2, cur);
+                    __builtin_amdgcn_s_waitcnt(0x0070 | LOADS);  // weight rows of slab s+1 landed
+                } else {
+                    __builtin_amdgcn_s_waitcnt(0x0070);
+                }
+                barrier();
+            };
+            for (int s = 0; s < nk; s += 2) {
+                slab1(lds0, s);
+                slab1(lds1, s + 1);
+            }
+            mma_slab();
+        }
+    }
+
+    if (split) {
+        float* part = a.part + static_cast<int64_t>(p) * TM * TN;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+            const int trow = wm * WTOK + mi * 32 + l32;
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+                const int wrow = wn * WW + wblk(ni);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    f32x4 v;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] = acc[ni][mi][4 * q + i];
+                    *reinterpret_cast<f32x4*>(part + trow * TN + wrow + 8 * q + 4 * lh) = v;
+                }
+            }
+        }
+        continue;
+    }
+    write_tile32<TO, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+    }
+}
+
 // Sums the float32 partial tiles of the split tail in chunk order and applies the
 // epilogue (store, or silu(gate) * up) of the large-tile kernel. One workgroup per
 // (tail tile, 16 rows); every thread owns a run of 4 output columns per pass and issues
@@ -765,8 +975,11 @@ hipError_t run_lds(const GemmArgs& a, hipStream_t s) {
     const int64_t grid = gemm_slots<TM, TN>();
     {
         ProfileScope prof(a.name ? a.name : "gemm", s);
-        hipLaunchKernelGGL((gemm_lds_kernel<TM, TN, WM, WN, SWIGLU, TO>), dim3(static_cast<unsigned>(grid)),
-                           dim3(64 * WM * WN), 0, s, a);
+        if constexpr (TM == 256 && TN == 256 && WM * WN == 8)
+            hipLaunchKernelGGL((gemm_pp_kernel<SWIGLU, TO>), dim3(static_cast<unsigned>(grid)), dim3(512), 0, s, a);
+        else
+            hipLaunchKernelGGL((gemm_lds_kernel<TM, TN, WM, WN, SWIGLU, TO>), dim3(static_cast<unsigned>(grid)),
+                               dim3(64 * WM * WN), 0, s, a);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !can_split) return e;
