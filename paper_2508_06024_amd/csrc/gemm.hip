@@ -239,7 +239,7 @@ __device__ __forceinline__ void write_tile(const GemmArgs& a, const TileInfo& ti
                 f32x4 v;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) v[i] = silu(acc[ni][mi][i]) * acc[ni + HALF][mi][i];
-                store4<TO>(orow + col, v);
+                if (col < a.N) store4<TO>(orow + col, v);
             }
         } else {
 #pragma unroll
@@ -393,6 +393,7 @@ __device__ __forceinline__ i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
 }
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 // Writes a wave's 32x32-block accumulators. After v_mfma_f32_32x32x16 with weight rows as A
 // and token rows as B, lane l holds token row (l % 32) of the block and, in register r,
@@ -418,7 +419,7 @@ __device__ __forceinline__ void write_tile32(const GemmArgs& a, const TileInfo& 
                     f32x4 v;
 #pragma unroll
                     for (int i = 0; i < 4; ++i) v[i] = silu(acc[ni][mi][4 * q + i]) * acc[ni + HALF][mi][4 * q + i];
-                    store4<TO>(orow + col, v);
+                    if (col < a.N) store4<TO>(orow + col, v);
                 }
             }
         } else {
@@ -890,7 +891,58 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
         }
         continue;
     }
-    write_tile32<TO, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+    if constexpr (sizeof(TO) == 4) {
+        write_tile32<TO, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+    } else {
+        // The finished tile is staged in LDS as bf16 rows (both stages are free after the last
+        // slab) so that the global stores are whole rows: 16 bytes per lane, 128-byte lines.
+        // Staged row r holds its 16-byte chunk c at c ^ (r % OCH).
+        constexpr int OROW = NOUT * 2;   // bytes per staged row
+        constexpr int OCH = OROW / 16;   // 16-byte chunks per row
+        constexpr int RPS = STAGE / OROW;  // rows per LDS stage (all 256 for SwiGLU, 128 otherwise)
+        static_assert(TM <= 2 * RPS && WTOK <= RPS && RPS % WTOK == 0, "staged tile fits the two stages");
+        // this wave's rows wm * 64 .. wm * 64 + 63 lie in one stage
+        char* wst = (wm * WTOK < RPS ? lds0 : lds1) + (wm * WTOK % RPS) * OROW;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) {
+            const int r = mi * 32 + l32;  // row within this wave's 64
+            const int sr = wm * WTOK + r;  // row within the tile (swizzle key)
+            constexpr int NB = SWIGLU ? NI / 2 : NI;
+#pragma unroll
+            for (int ni = 0; ni < NB; ++ni) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        v[e] = SWIGLU ? silu(acc[ni][mi][4 * q + e]) * acc[ni + NB][mi][4 * q + e] : acc[ni][mi][4 * q + e];
+                    bf16x4 o;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(v[e]);
+                    const int col = wn * (NOUT / WN) + ni * 32 + 8 * q;  // first column of the 8-column chunk
+                    const int ch = (col / 8) ^ (sr % OCH);
+                    *reinterpret_cast<bf16x4*>(wst + r * OROW + ch * 16 + lh * 8) = o;
+                }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+        barrier();
+        // whole rows back out: ROWS_PER_INSTR rows of OCH lanes per instruction
+        constexpr int RPI = 64 / OCH;
+        constexpr int NINSTR = TM / NW / RPI;
+        TO* out = static_cast<TO*>(a.out);
+#pragma unroll
+        for (int j = 0; j < NINSTR; ++j) {
+            const int r = wave * (TM / NW) + j * RPI + lane / OCH;  // tile row
+            const int c = lane % OCH;
+            const char* src = (r < RPS ? lds0 : lds1) + (r % RPS) * OROW + ((c ^ (r % OCH)) * 16);
+            const uint4 v = *reinterpret_cast<const uint4*>(src);
+            const int col = ti.nt * NOUT + c * 8;
+            if (r < ti.valid && col < a.N) *reinterpret_cast<uint4*>(out + (ti.row0 + r) * a.ldo + col) = v;
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): staged rows read before the stages refill
+        barrier();
+    }
     }
 }
 
@@ -939,7 +991,7 @@ __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs a) {
             f32x4 v;
 #pragma unroll
             for (int q = 0; q < 4; ++q) v[q] = silu(sg[q]) * su[q];
-            store4<TO>(orow + ti.nt * NOUT + c, v);
+            if (ti.nt * NOUT + c < a.N) store4<TO>(orow + ti.nt * NOUT + c, v);
         } else {
             const int col = ti.nt * TN + c;
             if (col < a.N) store4<TO>(orow + col, sg);
