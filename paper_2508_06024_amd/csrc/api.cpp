@@ -141,38 +141,39 @@ ec2moe_status check_codec_desc(const ec2moe_codec_desc* d) {
     return EC2MOE_OK;
 }
 
-int choose_splits(int M, int N, int K) {
-    const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
-    int s = std::max(1, 256 / std::max(1, tiles));  // about one workgroup per CU
-    s = std::min(s, std::max(1, K / 64));
-    return std::min(s, 64);
-}
-
 struct CodecWs {
     size_t gpart;  // split-K tail scratch of the matrix-core GEMMs (shared by encode and decode)
-    // encode
+    // encode: V^T, P = X V (float32), per-chunk partial sums of U^T P
     size_t vt, p, epart, enc_total;
-    int enc_splits;
-    // decode
-    size_t wt, dpart, dec_total;
-    int dec_splits;
+    int tc;  // tokens per chunk of the U^T P contraction
+    // decode: Z rounded to the layer dtype (bf16 only), W = V_hat Z^T
+    size_t zb, wt, dec_total;
 };
+
+// Token chunk of the U^T P contraction: about one workgroup per CU over (chunk, 64-column
+// block) pairs, in multiples of 4 tokens.
+int utp_chunk(int h, int r_w) {
+    const int col_blocks = (r_w + 63) / 64;
+    const int target = std::max(1, 256 / col_blocks);
+    const int tc = (std::max(1, h) + target - 1) / target;
+    return (tc + 3) & ~3;
+}
 
 CodecWs codec_ws(const ec2moe_codec_desc* d) {
     const size_t eb = elem_bytes(static_cast<DType>(d->dtype));
     CodecWs w{};
-    w.enc_splits = choose_splits(d->r_h, d->r_w, std::max(1, d->h));
+    w.tc = utp_chunk(d->h, d->r_w);
+    const size_t chunks = (static_cast<size_t>(std::max(1, d->h)) + w.tc - 1) / w.tc;
     size_t o = 0;
     w.gpart = o; o += up(gemm_split_scratch_bytes());
     const size_t shared = o;
     w.vt = o; o += up(static_cast<size_t>(d->r_w) * d->w * eb);
     w.p = o; o += up(static_cast<size_t>(d->h) * d->r_w * 4);
-    w.epart = o; o += up(static_cast<size_t>(w.enc_splits) * d->r_h * d->r_w * 4);
+    w.epart = o; o += up(chunks * d->r_h * d->r_w * 4);
     w.enc_total = o;
-    w.dec_splits = choose_splits(d->w, d->r_h, d->r_w);
     o = shared;
+    w.zb = o; o += up(static_cast<size_t>(d->r_h) * d->r_w * eb);
     w.wt = o; o += up(static_cast<size_t>(d->w) * d->r_h * eb);
-    w.dpart = o; o += up(static_cast<size_t>(w.dec_splits) * d->w * d->r_h * 4);
     w.dec_total = o;
     return w;
 }
@@ -423,14 +424,11 @@ ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x
         g.src_rows = desc->h; g.w_rows = desc->r_w; g.part = at<float>(ws, w.gpart); g.max_split = kMaxSplit;
         e = launch_gemm(dt, Epilogue::Store, OutType::F32, g, stream);
         if (e != hipSuccess) break;
-        // Z = U^T P  [r_h][r_w]: A(m,k) = U[k][m], B(k,n) = P[k][n]
-        SmallGemmArgs s{};
-        s.a = u; s.a_dt = dt; s.a_sm = 1; s.a_sk = desc->r_h;
-        s.b = p; s.b_dt = DType::F32; s.b_sk = desc->r_w; s.b_sn = 1;
-        s.M = desc->r_h; s.N = desc->r_w; s.K = desc->h;
-        s.out = z + static_cast<size_t>(c) * desc->r_h * desc->r_w; s.out_dt = DType::F32;
-        s.part = at<float>(ws, w.epart); s.splits = w.enc_splits; s.name = "codec_utp";
-        e = launch_small_gemm(s, stream);
+        // Z = U^T P  [r_h][r_w], float32 over token chunks, reduced in chunk order
+        UtpArgs s{};
+        s.u = u; s.p = p; s.T = desc->h; s.rh = desc->r_h; s.rw = desc->r_w; s.tc = w.tc;
+        s.part = at<float>(ws, w.epart); s.z = z + static_cast<size_t>(c) * desc->r_h * desc->r_w;
+        e = launch_utp(dt, s, stream);
     }
     return hip_status(e, "lowrank_encode launch");
 }
@@ -449,14 +447,21 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
     void* wt = at<void>(ws, w.wt);
     hipError_t e = hipSuccess;
     for (int c = 0; c < desc->n_slices && e == hipSuccess; ++c) {
-        // Wt = V_hat Z^T  [w][r_h]: A(m,k) = V_hat[m][k], B(k,n) = Z[n][k]; rounded to the layer dtype
-        SmallGemmArgs s{};
-        s.a = v_hat; s.a_dt = dt; s.a_sm = desc->r_w; s.a_sk = 1;
-        s.b = z + static_cast<size_t>(c) * desc->r_h * desc->r_w; s.b_dt = DType::F32; s.b_sk = 1; s.b_sn = desc->r_w;
-        s.M = desc->w; s.N = desc->r_h; s.K = desc->r_w;
-        s.out = wt; s.out_dt = dt;
-        s.part = at<float>(ws, w.dpart); s.splits = w.dec_splits; s.name = "codec_vzt";
-        e = launch_small_gemm(s, stream);
+        // Wt = V_hat Z^T  [w][r_h]: both operands are K-contiguous rows (V_hat [w][r_w], Z [r_h][r_w]).
+        // In bf16 layers Z is rounded to bf16 first (the product runs on the bf16 matrix cores;
+        // Wt itself is rounded to bf16 anyway).
+        const float* zc = z + static_cast<size_t>(c) * desc->r_h * desc->r_w;
+        const void* zop = zc;
+        if (dt == DType::BF16) {
+            e = launch_f32_to_bf16(zc, static_cast<int64_t>(desc->r_h) * desc->r_w, at<void>(ws, w.zb), stream);
+            if (e != hipSuccess) break;
+            zop = at<void>(ws, w.zb);
+        }
+        GemmArgs gw{};
+        gw.tok = v_hat; gw.row_index = nullptr; gw.w = zop; gw.w_group_stride = 0; gw.seg = nullptr; gw.n_groups = 1;
+        gw.rows = desc->w; gw.K = desc->r_w; gw.N = desc->r_h; gw.out = wt; gw.ldo = desc->r_h; gw.name = "codec_vzt";
+        gw.src_rows = desc->w; gw.w_rows = desc->r_h; gw.part = at<float>(ws, w.gpart); gw.max_split = kMaxSplit;
+        e = launch_gemm(dt, Epilogue::Store, OutType::Same, gw, stream);
         if (e != hipSuccess) break;
         // X_hat = U_hat Wt^T  [h][w]
         GemmArgs g{};

@@ -1,11 +1,8 @@
 // Helpers of the low-rank codec (Encoder-Decoder based on Low-Rank Compression) for
-// gfx950: a tiled transpose, and a float32-accumulating GEMM for the small products
-// whose operands must stay in float32 (U^T (X V) with X V in float32, Z V_hat^T with Z
-// in float32). The large products X V and U_hat W run on the matrix-core GEMM.
-//
-// small_gemm: C[m][n] = sum_k A(m,k) B(k,n) with arbitrary element strides, 64x64 output
-// tile per workgroup, 4x4 outputs per thread, k split into `splits` parts written to a
-// float32 partial buffer and summed in part order by a second kernel (deterministic).
+// gfx950: a tiled transpose, the float32 contraction Z = U^T P of the encoder (P = X V in
+// float32, so Z keeps float32 accuracy), its in-order reduction over token chunks, and the
+// float32 -> bfloat16 rounding of Z for the decoder. The large products X V, V_hat Z^T and
+// U_hat W^T run on the matrix-core GEMM.
 #include "device_common.h"
 #include "internal.h"
 
@@ -54,76 +51,127 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ sr
     }
 }
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+constexpr int kUtpT = 64;   // tokens per LDS stage
+constexpr int kUtpC = 64;   // columns of P per workgroup
+constexpr int kUtpUP = 272;  // LDS pitch of the staged U rows (floats; 272 % 64 = 16: the four
+                             // 16-lane groups of a read fall on disjoint banks)
+constexpr int kUtpPP = 80;   // LDS pitch of the staged P rows (80 % 64 = 16)
 
-constexpr int kT = 64;    // output tile (64 x 64 per workgroup, one 32 x 32 block per wave)
-constexpr int kBK = 32;   // k per LDS stage
-constexpr int kPitch = 97;  // LDS row pitch in floats: odd, so 32 consecutive k rows hit distinct banks
-
-// C[m][n] = sum_k A(m,k) B(k,n) on the float32 matrix cores (v_mfma_f32_32x32x2f32).
-// Operands are staged to LDS as [k][m] and [k][n] from any global layout (reads walk the
-// contiguous direction); lane l then feeds row/column l % 32 at k = l / 32 of each step.
-template <typename TA, typename TB>
-__global__ __launch_bounds__(256) void small_gemm_kernel(SmallGemmArgs g) {
-    __shared__ float As[kBK * kPitch];
-    __shared__ float Bs[kBK * kPitch];
-    const int m0 = blockIdx.x * kT, n0 = blockIdx.y * kT;
-    const int split = blockIdx.z;
-    const int kper = (g.K + g.splits - 1) / g.splits;
-    const int kbeg = split * kper;
-    const int kend = std::min(g.K, kbeg + kper);
+// One token chunk of Z = U^T P: part[s][r][c] = sum over t in chunk s of U[t][r] P[t][c], for
+// the 64 columns c0.. of this workgroup and all r_h <= 256 rows, on the float32 matrix cores
+// (v_mfma_f32_16x16x4f32: lane l feeds A[l % 16][l / 16] and B[l / 16][l % 16] and holds
+// D[4 (l / 16) + i][l % 16]). Each stage loads 64 token rows of U (converted to float32) and of
+// P with 16-byte loads into LDS; rows past the chunk are zero. Wave w owns rows w*64 .. w*64+63.
+template <typename TU>
+__global__ __launch_bounds__(256) void utp_kernel(UtpArgs g) {
+    __shared__ float Us[kUtpT * kUtpUP];
+    __shared__ float Ps[kUtpT * kUtpPP];
+    constexpr int EPC = 16 / static_cast<int>(sizeof(TU));
+    const int c0 = blockIdx.x * kUtpC;
+    const int tb = blockIdx.y * g.tc;
+    const int te = min(g.T, tb + g.tc);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
-    const bool a_k_fast = g.a_sk == 1;
-    const bool b_k_fast = g.b_sk == 1;
-    f32x16 acc;
+    const int l16 = lane & 15, lg = lane >> 4;
+    const int rbase = wave * 64;
+    // U columns r_h .. 255 stay zero: a wave's blocks past r_h (and P columns past r_w) multiply
+    // zeros, which keeps the matrix-core sequence free of branches; their outputs are not stored
+    for (int i = threadIdx.x; i < kUtpT * (256 - g.rh); i += 256) {
+        const int r = i / (256 - g.rh), c = g.rh + i % (256 - g.rh);
+        Us[r * kUtpUP + c] = 0.f;
+    }
+    f32x4 acc[4][4];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-    constexpr int PER = kT * kBK / 256;  // elements of each operand per thread per stage
-    for (int k0 = kbeg; k0 < kend; k0 += kBK) {
-        // all loads of the stage first, then the LDS stores
-        float va[PER], vb[PER];
-        int ia[PER], ib[PER];
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            const int e = threadIdx.x + 256 * j;
-            int mm, kk;
-            if (a_k_fast) { kk = e % kBK; mm = e / kBK; } else { mm = e % kT; kk = e / kT; }
-            // clamped, unconditional loads (all in flight together); out-of-range lanes select 0
-            const int m = m0 + mm, k = k0 + kk;
-            const float a_v = ld<TA>(g.a, min(m, g.M - 1) * g.a_sm + min(k, kend - 1) * g.a_sk);
-            va[j] = (m < g.M && k < kend) ? a_v : 0.f;
-            ia[j] = kk * kPitch + mm;
-            int nn, kb;
-            if (b_k_fast) { kb = e % kBK; nn = e / kBK; } else { nn = e % kT; kb = e / kT; }
-            const int n = n0 + nn, kq = k0 + kb;
-            const float b_v = ld<TB>(g.b, min(kq, kend - 1) * g.b_sk + min(n, g.N - 1) * g.b_sn);
-            vb[j] = (n < g.N && kq < kend) ? b_v : 0.f;
-            ib[j] = kb * kPitch + nn;
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const TU* u = static_cast<const TU*>(g.u);
+    for (int t0 = tb; t0 < te; t0 += kUtpT) {
+        const int nt = min(kUtpT, te - t0);
+        // U rows (rh / EPC chunks per row, at most 8 chunks per thread) and P rows (16 chunks
+        // of 4 floats per row, 4 per thread): all loads of the stage issue before the LDS stores
+        const int ucpr = g.rh / EPC;
+        constexpr int UPT = kUtpT * (256 / EPC) / 256;
+        uint4 uq[UPT];
+#pragma unroll
+        for (int j = 0; j < UPT; ++j) {
+            const int i = threadIdx.x + 256 * j;
+            const int r = i / ucpr, ch = i % ucpr;
+            uq[j] = make_uint4(0, 0, 0, 0);
+            if (i < kUtpT * ucpr && r < nt)
+                uq[j] = *reinterpret_cast<const uint4*>(u + static_cast<int64_t>(t0 + r) * g.rh + ch * EPC);
+        }
+        constexpr int PPT = kUtpT * 16 / 256;
+        f32x4 pq[PPT];
+#pragma unroll
+        for (int j = 0; j < PPT; ++j) {
+            const int i = threadIdx.x + 256 * j;
+            const int r = i / 16, c = c0 + (i % 16) * 4;
+            pq[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (r < nt && c < g.rw) pq[j] = *reinterpret_cast<const f32x4*>(g.p + static_cast<int64_t>(t0 + r) * g.rw + c);
         }
 #pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            As[ia[j]] = va[j];
-            Bs[ib[j]] = vb[j];
+        for (int j = 0; j < UPT; ++j) {
+            const int i = threadIdx.x + 256 * j;
+            if (i < kUtpT * ucpr) {
+                const int r = i / ucpr, ch = i % ucpr;
+                const TU* e = reinterpret_cast<const TU*>(&uq[j]);
+#pragma unroll
+                for (int q = 0; q < EPC; q += 4)
+                    *reinterpret_cast<f32x4*>(Us + r * kUtpUP + ch * EPC + q) =
+                        f32x4{Elem<TU>::to_f32(e[q]), Elem<TU>::to_f32(e[q + 1]), Elem<TU>::to_f32(e[q + 2]),
+                              Elem<TU>::to_f32(e[q + 3])};
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < PPT; ++j) {
+            const int i = threadIdx.x + 256 * j;
+            *reinterpret_cast<f32x4*>(Ps + (i / 16) * kUtpPP + (i % 16) * 4) = pq[j];
         }
         __syncthreads();
+        auto kstep = [&](int k) {
+            float a[4], b[4];
 #pragma unroll
-        for (int kk = 0; kk < kBK; kk += 2) {
-            const float av = As[(kk + (lane >> 5)) * kPitch + wm * 32 + (lane & 31)];
-            const float bv = Bs[(kk + (lane >> 5)) * kPitch + wn * 32 + (lane & 31)];
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
+            for (int rb = 0; rb < 4; ++rb) a[rb] = Us[(k + lg) * kUtpUP + rbase + rb * 16 + l16];
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) b[cb] = Ps[(k + lg) * kUtpPP + cb * 16 + l16];
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                for (int cb = 0; cb < 4; ++cb)
+                    acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[rb], b[cb], acc[rb][cb], 0, 0, 0);
+        };
+        if (nt == kUtpT) {
+#pragma unroll
+            for (int k = 0; k < kUtpT; k += 4) kstep(k);
+        } else {
+            const int nk = (nt + 3) & ~3;
+            for (int k = 0; k < nk; k += 4) kstep(k);
         }
         __syncthreads();
     }
-    // lane l holds C[m0 + wm*32 + 8*(r/4) + 4*(l/32) + r%4][n0 + wn*32 + l%32]
-    float* part = g.part + static_cast<int64_t>(split) * g.M * g.N;
-    const int n = n0 + wn * 32 + (lane & 31);
-    if (n < g.N) {
+    float* part = g.part + static_cast<int64_t>(blockIdx.y) * g.rh * g.rw;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int m = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            if (m < g.M) part[static_cast<int64_t>(m) * g.N + n] = acc[r];
-        }
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = rbase + rb * 16 + 4 * lg + i;
+                const int c = c0 + cb * 16 + l16;
+                if (r < g.rh && c < g.rw) part[static_cast<int64_t>(r) * g.rw + c] = acc[rb][cb][i];
+            }
+}
+
+// dst[i] = round-to-nearest-even bfloat16 of src[i], four elements per thread (n a multiple of 4)
+__global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ src, int64_t n,
+                                                          bf16_t* __restrict__ dst) {
+    for (int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4; i < n;
+         i += static_cast<int64_t>(gridDim.x) * 256 * 4) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(src + i);
+        uint2 o;
+        o.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+        o.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+        *reinterpret_cast<uint2*>(dst + i) = o;
     }
 }
 
@@ -133,47 +181,35 @@ __device__ __forceinline__ void put4(TO* dst, f32x4 v) {
     for (int i = 0; i < 4; ++i) dst[i] = Elem<TO>::from_f32(v[i]);
 }
 
-// out[i] = sum over p of part[p][i], in p order (deterministic); four elements per thread
-// (mn a multiple of 4), the loads of up to 8 partials in flight at once.
+// out[i] = sum over p of part[p][i] (deterministic): four groups of threads each add a quarter
+// of the partials in order with up to 16 loads in flight, and the group sums are added in
+// group order. A workgroup owns 64 runs of four consecutive elements (mn a multiple of 4).
 template <typename TO>
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part, int64_t mn, int splits,
                                                            TO* __restrict__ out) {
-    for (int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4; i < mn;
-         i += static_cast<int64_t>(gridDim.x) * 256 * 4) {
-        f32x4 s = *reinterpret_cast<const f32x4*>(part + i);
-        for (int p0 = 1; p0 < splits; p0 += 8) {
-            f32x4 v[8];
+    __shared__ f32x4 grp[4][64];
+    const int col = threadIdx.x & 63, g = threadIdx.x >> 6;
+    const int per = (splits + 3) / 4;
+    const int p0 = g * per, p1 = min(splits, p0 + per);
+    for (int64_t base = static_cast<int64_t>(blockIdx.x) * 256; base < mn; base += static_cast<int64_t>(gridDim.x) * 256) {
+        const int64_t i = base + col * 4;
+        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (i < mn) {
+            for (int q = p0; q < p1; q += 16) {
+                f32x4 v[16];
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (p0 + j < splits) v[j] = *reinterpret_cast<const f32x4*>(part + (p0 + j) * mn + i);
+                for (int j = 0; j < 16; ++j)
+                    if (q + j < p1) v[j] = *reinterpret_cast<const f32x4*>(part + (q + j) * mn + i);
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (p0 + j < splits) s += v[j];
+                for (int j = 0; j < 16; ++j)
+                    if (q + j < p1) s += v[j];
+            }
         }
-        put4<TO>(out + i, s);
+        grp[g][col] = s;
+        __syncthreads();
+        if (g == 0 && i < mn) put4<TO>(out + i, ((grp[0][col] + grp[1][col]) + grp[2][col]) + grp[3][col]);
+        __syncthreads();
     }
-}
-
-template <typename TA, typename TB>
-hipError_t small_gemm_t(const SmallGemmArgs& g, hipStream_t s) {
-    dim3 grid((g.M + kT - 1) / kT, (g.N + kT - 1) / kT, g.splits);
-    {
-        ProfileScope prof(g.name ? g.name : "small_gemm", s);
-        hipLaunchKernelGGL((small_gemm_kernel<TA, TB>), grid, dim3(256), 0, s, g);
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int64_t mn = static_cast<int64_t>(g.M) * g.N;
-    const int rgrid = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 4096));
-    std::string rname = std::string(g.name ? g.name : "small_gemm") + "_reduce";
-    ProfileScope prof(rname.c_str(), s);
-    if (g.out_dt == DType::BF16)
-        hipLaunchKernelGGL(split_reduce_kernel<bf16_t>, dim3(rgrid), dim3(256), 0, s, g.part, mn, g.splits,
-                           static_cast<bf16_t*>(g.out));
-    else
-        hipLaunchKernelGGL(split_reduce_kernel<float>, dim3(rgrid), dim3(256), 0, s, g.part, mn, g.splits,
-                           static_cast<float*>(g.out));
-    return hipGetLastError();
 }
 
 }  // namespace
@@ -190,12 +226,28 @@ hipError_t launch_transpose(DType dt, const void* src, int rows, int cols, void*
     return hipGetLastError();
 }
 
-hipError_t launch_small_gemm(const SmallGemmArgs& g, hipStream_t s) {
-    const bool ab = g.a_dt == DType::BF16, bb = g.b_dt == DType::BF16;
-    if (ab && bb) return small_gemm_t<bf16_t, bf16_t>(g, s);
-    if (ab) return small_gemm_t<bf16_t, float>(g, s);
-    if (bb) return small_gemm_t<float, bf16_t>(g, s);
-    return small_gemm_t<float, float>(g, s);
+hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s) {
+    const int chunks = (g.T + g.tc - 1) / g.tc;
+    dim3 grid((g.rw + kUtpC - 1) / kUtpC, chunks);
+    {
+        ProfileScope prof("codec_utp", s);
+        if (udt == DType::BF16) hipLaunchKernelGGL(utp_kernel<bf16_t>, grid, dim3(256), 0, s, g);
+        else hipLaunchKernelGGL(utp_kernel<float>, grid, dim3(256), 0, s, g);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t mn = static_cast<int64_t>(g.rh) * g.rw;
+    const int rgrid = static_cast<int>(std::min<int64_t>((mn + 255) / 256, 4096));
+    ProfileScope prof("codec_utp_reduce", s);
+    hipLaunchKernelGGL(split_reduce_kernel<float>, dim3(rgrid), dim3(256), 0, s, g.part, mn, chunks, g.z);
+    return hipGetLastError();
+}
+
+hipError_t launch_f32_to_bf16(const float* src, int64_t n, void* dst, hipStream_t s) {
+    const int grid = static_cast<int>(std::min<int64_t>((n / 4 + 255) / 256, 4096));
+    ProfileScope prof("codec_z_bf16", s);
+    hipLaunchKernelGGL(f32_to_bf16_kernel, dim3(grid), dim3(256), 0, s, src, n, static_cast<bf16_t*>(dst));
+    return hipGetLastError();
 }
 
 }  // namespace ec2moe

@@ -53,8 +53,9 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     constexpr int SLICE = 4 * EPC;  // k covered by one matrix-core step
     // k-slices whose loads are issued together: deep for few gate rows, shallow for many
     // (U (NRB + 1) uint4 registers; the budget shrinks with more waves per SIMD)
+    // (one batch covers a wave's whole share of d = 4096 with 8 waves and one row block)
     constexpr int UB = WAVES <= 8 ? 40 : 16;
-    constexpr int U = UB / (NRB + 1) < 1 ? 1 : (UB / (NRB + 1) > 8 ? 8 : UB / (NRB + 1));
+    constexpr int U = UB / (NRB + 1) < 1 ? 1 : (UB / (NRB + 1) > 16 ? 16 : UB / (NRB + 1));
     constexpr int THREADS = 64 * WAVES;
     constexpr int TPW = kTok / WAVES;  // tokens per wave in the softmax phase
     const int lane = threadIdx.x & 63;

@@ -92,18 +92,19 @@ hipError_t launch_combine(DType dt, const void* y_perm, const int32_t* inv_perm,
 // dst[c][r] = src[r][c] for a rows x cols matrix
 hipError_t launch_transpose(DType dt, const void* src, int rows, int cols, void* dst, hipStream_t s);
 
-// C[m][n] = sum_k A(m,k) * B(k,n), float32 accumulation, split over k in `splits`
-// deterministic parts (partials in `part`, [splits][M][N] float32), then reduced in order.
-//   A(m,k) = a[m*a_sm + k*a_sk] (element type a_dt), B(k,n) = b[k*b_sk + n*b_sn] (b_dt).
-// Output element type out_dt (float32 or the layer dtype).
-struct SmallGemmArgs {
-    const void* a; DType a_dt; int64_t a_sm, a_sk;
-    const void* b; DType b_dt; int64_t b_sk, b_sn;
-    int M, N, K;
-    void* out; DType out_dt;
-    float* part; int splits;
-    const char* name;         // kernel name for the timing record (the reduction adds "_reduce")
+// Z[r][c] = sum_t U[t][r] P[t][c] (r < rh, c < rw, t < T): float32 partial sums over token
+// chunks of tc rows go to part ([ceil(T / tc)][rh][rw] float32), then are added in chunk
+// order into z (deterministic). U has the layer dtype, P and Z are float32. rh <= 256;
+// rh and rw are multiples of 16; every row is 16-byte aligned.
+struct UtpArgs {
+    const void* u;
+    const float* p;
+    int T, rh, rw, tc;
+    float* part;
+    float* z;
 };
-hipError_t launch_small_gemm(const SmallGemmArgs& g, hipStream_t s);
+hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s);
+// dst = bfloat16(src) with round-to-nearest-even, n a multiple of 4
+hipError_t launch_f32_to_bf16(const float* src, int64_t n, void* dst, hipStream_t s);
 
 }  // namespace ec2moe

@@ -8,6 +8,7 @@
 //               the same expert find each other with one ballot per bit of the expert
 //               id, so the rank inside the 64 comes from a popcount and the order of
 //               the input is kept.
+// Up to 65536 assignments the three steps run in one workgroup (one launch instead of three).
 // No floating point and no global atomics: the result is unique and deterministic.
 #include "device_common.h"
 #include "internal.h"
@@ -130,6 +131,133 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
     }
 }
 
+// The three steps in one workgroup of 16 waves, for up to kSmallMax assignments: wave w
+// takes the w-th of 16 consecutive ranges, so the input order is kept across waves as it is
+// across chunks above; the segment offsets come from a wave-level scan over the experts.
+constexpr int kSmallWaves = 16;
+constexpr int64_t kSmallMax = 65536;
+
+__global__ __launch_bounds__(64 * kSmallWaves) void perm_small_kernel(const int32_t* __restrict__ idx, int64_t n,
+                                                                      int top_k, int M, int32_t* __restrict__ seg,
+                                                                      int32_t* __restrict__ perm_src,
+                                                                      int32_t* __restrict__ inv_perm) {
+    __shared__ int wpos[kSmallWaves][256];  // counts per (wave, expert), then first positions
+    __shared__ int total[256];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    for (int i = threadIdx.x; i < kSmallWaves * 256; i += 64 * kSmallWaves) (&wpos[0][0])[i] = 0;
+    __syncthreads();
+    const int64_t per = (n + kSmallWaves - 1) / kSmallWaves;
+    const int64_t wbeg = wave * per;
+    const int64_t wend = std::min<int64_t>(n, wbeg + per);
+    // the wave's expert ids are read 8 passes of 64 at a time (loads in flight together)
+    constexpr int U = 8;
+    for (int64_t s0 = wbeg; s0 < wend; s0 += 64 * U) {
+        int ev[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t a = s0 + 64 * u + lane;
+            ev[u] = a < wend ? idx[a] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ev[u] >= 0 && ev[u] < M) atomicAdd(&wpos[wave][ev[u]], 1);
+    }
+    __syncthreads();
+    // per expert: offsets of the waves' runs inside its segment, and its total
+    if (threadIdx.x < M) {
+        const int e = threadIdx.x;
+        int c[kSmallWaves];
+#pragma unroll
+        for (int w = 0; w < kSmallWaves; ++w) c[w] = wpos[w][e];
+        int run = 0;
+#pragma unroll
+        for (int w = 0; w < kSmallWaves; ++w) {
+            wpos[w][e] = run;
+            run += c[w];
+        }
+        total[e] = run;
+    }
+    __syncthreads();
+    // exclusive scan of the totals over experts: lane l of wave 0 owns experts 4 l .. 4 l + 3
+    if (wave == 0) {
+        int v[4], sum = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = 4 * lane + q;
+            v[q] = e < M ? total[e] : 0;
+            sum += v[q];
+        }
+        int inc = sum;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int t = __shfl_up(inc, off);
+            if (lane >= off) inc += t;
+        }
+        int run = inc - sum;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = 4 * lane + q;
+            if (e < M) {
+                total[e] = run;
+                seg[e] = run;
+            }
+            run += v[q];
+        }
+        if (lane == 63) seg[M] = inc;
+    }
+    __syncthreads();
+    if (threadIdx.x < M) {
+        const int e = threadIdx.x;
+        const int start = total[e];
+#pragma unroll
+        for (int w = 0; w < kSmallWaves; ++w) wpos[w][e] += start;
+    }
+    __syncthreads();
+
+    int nbits = 0;
+    while ((1 << nbits) < M) ++nbits;
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    for (int64_t s1 = wbeg; s1 < wend; s1 += 64 * U) {
+    int ev[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t a = s1 + 64 * u + lane;
+        ev[u] = a < wend ? idx[a] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t s0 = s1 + 64 * u;
+        if (s0 >= wend) break;
+        const int64_t a = s0 + lane;
+        int e = -1;
+        if (a < wend) {
+            e = ev[u];
+            if (e < 0 || e >= M) {
+                inv_perm[a] = -1;
+                e = -1;
+            }
+        }
+        const bool valid = e >= 0;
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < nbits; ++b) {
+            const bool bit = valid && ((e >> b) & 1);
+            const uint64_t ones = __ballot(bit);
+            peers &= bit ? ones : ~ones;
+        }
+        if (valid) {
+            const int rank = __popcll(peers & lt_mask);
+            const int pos = wpos[wave][e] + rank;
+            perm_src[pos] = static_cast<int32_t>(a / top_k);
+            inv_perm[a] = pos;
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (valid && (peers & lt_mask) == 0) wpos[wave][e] += __popcll(peers);
+        __builtin_amdgcn_wave_barrier();
+    }
+    }
+}
+
 // Rows past the valid segments (only when some expert ids were out of range) and
 // source ids outside [0, n_src) are written as zeros.
 __global__ __launch_bounds__(256) void gather_rows_kernel(const char* __restrict__ x,
@@ -153,6 +281,12 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const char* __restrict
 hipError_t launch_permute(const int32_t* topk_idx, int64_t n_assign, int top_k, int n_experts,
                           int32_t* chunk_counts, int32_t* seg_offsets, int32_t* perm_src,
                           int32_t* inv_perm, hipStream_t s) {
+    if (n_assign <= kSmallMax) {
+        ProfileScope prof("perm_small", s);
+        hipLaunchKernelGGL(perm_small_kernel, dim3(1), dim3(64 * kSmallWaves), 0, s, topk_idx, n_assign, top_k,
+                           n_experts, seg_offsets, perm_src, inv_perm);
+        return hipGetLastError();
+    }
     const int chunks = perm_chunks(n_assign);
     if (chunks == 0) {
         ProfileScope prof("perm_scan", s);
