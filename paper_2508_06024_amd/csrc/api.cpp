@@ -94,7 +94,7 @@ struct MoeWs {
 };
 
 // split-K tail chunks of the large-tile GEMM
-constexpr int kMaxSplit = 8;
+constexpr int kMaxSplit = 32;
 
 MoeWs moe_ws(const ec2moe_moe_desc* d) {
     const int64_t A = static_cast<int64_t>(d->n_tokens) * d->top_k;

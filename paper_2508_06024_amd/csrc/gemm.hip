@@ -53,7 +53,7 @@ __device__ void raw_buffer_load_lds(i32x4 rsrc, lds_void* lds, int size, int vof
 namespace {
 
 constexpr int kXcds = 8;
-constexpr int kMaxSplitChunks = 8;  // K chunks of a split tail tile (the reduction holds this many)
+constexpr int kMaxSplitChunks = 32;  // K chunks of a split tail tile
 
 struct TileInfo {
     int group;
@@ -953,7 +953,6 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
 template <int TM, int TN, bool SWIGLU, typename TO>
 __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs a) {
     constexpr int NOUT = SWIGLU ? TN / 2 : TN;
-    constexpr int kMaxS = kMaxSplitChunks;
     const int ntn = (a.N + NOUT - 1) / NOUT;
     const SplitPlan sp = split_plan(count_tiles<TM>(a, ntn), gemm_slots<TM, TN>(), a.max_split, a.K / 64);
     if (sp.S <= 1) return;
@@ -969,21 +968,24 @@ __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs a) {
         const int r = r0 + i / QUADS;
         const int c = (i % QUADS) * 4;
         if (r >= ti.valid) continue;
-        f32x4 g[kMaxS], u[kMaxS];
+        // chunks in order, 8 loads in flight at a time
+        f32x4 sg = f32x4{0.f, 0.f, 0.f, 0.f}, su = sg;
+        for (int k0 = 0; k0 < sp.S; k0 += 8) {
+            f32x4 g[8], u[8];
 #pragma unroll
-        for (int k = 0; k < kMaxS; ++k) {
-            if (k < sp.S) {
-                const float* src = tile_part + static_cast<int64_t>(k) * TM * TN + r * TN + c;
-                g[k] = *reinterpret_cast<const f32x4*>(src);
-                if (SWIGLU) u[k] = *reinterpret_cast<const f32x4*>(src + TN / 2);
+            for (int k = 0; k < 8; ++k) {
+                if (k0 + k < sp.S) {
+                    const float* src = tile_part + static_cast<int64_t>(k0 + k) * TM * TN + r * TN + c;
+                    g[k] = *reinterpret_cast<const f32x4*>(src);
+                    if (SWIGLU) u[k] = *reinterpret_cast<const f32x4*>(src + TN / 2);
+                }
             }
-        }
-        f32x4 sg = g[0], su = u[0];
 #pragma unroll
-        for (int k = 1; k < kMaxS; ++k) {
-            if (k < sp.S) {
-                sg += g[k];
-                if (SWIGLU) su += u[k];
+            for (int k = 0; k < 8; ++k) {
+                if (k0 + k < sp.S) {
+                    sg = k0 + k == 0 ? g[k] : sg + g[k];
+                    if (SWIGLU) su = k0 + k == 0 ? u[k] : su + u[k];
+                }
             }
         }
         TO* orow = static_cast<TO*>(a.out) + (ti.row0 + r) * a.ldo;
@@ -1065,6 +1067,9 @@ Tile choose_tile(const GemmArgs& a, bool swiglu, bool lds) {
         // the 256x256 tile whenever it fills at least one round of the machine (short K
         // included: the codec's rank-r products run 1.6x faster on it than on 128x128 tiles)
         if (avg_rows >= 256 && tiles(256, 256) >= gemm_slots<256, 256>()) return Tile::Big;
+        // long K and only a few 128x128 tiles (the encoder's X V for a handful of tokens): the
+        // split-K tail of the 128x128 kernel spreads K over up to 32 workgroups per tile
+        if (tiles(128, 128) * 4 <= gemm_slots<128, 128>() && a.K >= 2048) return Tile::Mid;
         // a few slabs of K and too few big tiles (the decoder's V_hat Z^T): the small
         // register-staged tile fills the machine without a split (2.5x faster than a split
         // 128x128 tile there)

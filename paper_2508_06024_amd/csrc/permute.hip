@@ -8,7 +8,7 @@
 //               the same expert find each other with one ballot per bit of the expert
 //               id, so the rank inside the 64 comes from a popcount and the order of
 //               the input is kept.
-// Up to 65536 assignments the three steps run in one workgroup (one launch instead of three).
+// Up to 8192 assignments the three steps run in one workgroup (one launch instead of three).
 // No floating point and no global atomics: the result is unique and deterministic.
 #include "device_common.h"
 #include "internal.h"
@@ -38,35 +38,65 @@ __global__ __launch_bounds__(256) void perm_count_kernel(const int32_t* __restri
     for (int e = threadIdx.x; e < M; e += 256) counts[static_cast<int64_t>(blockIdx.x) * M + e] = hist[e];
 }
 
-// counts[c][e] -> absolute first position of chunk c's assignments to expert e
+// counts[c][e] -> absolute first position of chunk c's assignments to expert e. Each expert's
+// column is walked 8 chunks at a time (loads in flight together); the expert totals are
+// scanned by one wave (lane l owns experts 4 l .. 4 l + 3).
 __global__ __launch_bounds__(256) void perm_scan_kernel(int32_t* __restrict__ counts, int n_chunks, int M,
                                                         int32_t* __restrict__ seg) {
     __shared__ int total[256];
     const int e = threadIdx.x;
+    const int lane = threadIdx.x & 63;
     int run = 0;
     if (e < M) {
-        for (int c = 0; c < n_chunks; ++c) {
-            const int v = counts[static_cast<int64_t>(c) * M + e];
-            counts[static_cast<int64_t>(c) * M + e] = run;
-            run += v;
+        for (int c0 = 0; c0 < n_chunks; c0 += 8) {
+            int v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = c0 + j < n_chunks ? counts[static_cast<int64_t>(c0 + j) * M + e] : 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (c0 + j < n_chunks) {
+                    counts[static_cast<int64_t>(c0 + j) * M + e] = run;
+                    run += v[j];
+                }
         }
         total[e] = run;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int s = 0;
-        for (int i = 0; i < M; ++i) {
-            const int v = total[i];
-            total[i] = s;
-            s += v;
+    if (threadIdx.x < 64) {
+        int v[4], sum = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int x = 4 * lane + q;
+            v[q] = x < M ? total[x] : 0;
+            sum += v[q];
         }
-        seg[M] = s;
+        int inc = sum;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int t = __shfl_up(inc, off);
+            if (lane >= off) inc += t;
+        }
+        int r = inc - sum;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int x = 4 * lane + q;
+            if (x < M) total[x] = r;
+            r += v[q];
+        }
+        if (lane == 63) seg[M] = inc;
     }
     __syncthreads();
     if (e < M) {
         const int start = total[e];
         seg[e] = start;
-        for (int c = 0; c < n_chunks; ++c) counts[static_cast<int64_t>(c) * M + e] += start;
+        for (int c0 = 0; c0 < n_chunks; c0 += 8) {
+            int v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = c0 + j < n_chunks ? counts[static_cast<int64_t>(c0 + j) * M + e] : 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (c0 + j < n_chunks) counts[static_cast<int64_t>(c0 + j) * M + e] = v[j] + start;
+        }
     }
 }
 
@@ -135,7 +165,7 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
 // takes the w-th of 16 consecutive ranges, so the input order is kept across waves as it is
 // across chunks above; the segment offsets come from a wave-level scan over the experts.
 constexpr int kSmallWaves = 16;
-constexpr int64_t kSmallMax = 65536;
+constexpr int64_t kSmallMax = 8192;
 
 __global__ __launch_bounds__(64 * kSmallWaves) void perm_small_kernel(const int32_t* __restrict__ idx, int64_t n,
                                                                       int top_k, int M, int32_t* __restrict__ seg,

@@ -18,12 +18,13 @@ PERM_CASES = [
     # T, M, k, n_keep, skew
     (64, 8, 2, 6, 0.0),
     (1024, 16, 2, 12, 0.0),
-    (8192, 64, 6, 48, 1.1),     # 49152 assignments in one workgroup, Zipf-skewed
+    (8192, 64, 6, 48, 1.1),     # 49152 assignments, chunked kernels, Zipf-skewed
     (4097, 8, 2, 8, 0.0),       # ragged last chunk
     (1, 4, 1, 4, 0.0),
     (3000, 256, 16, 256, 0.5),  # maximum experts and top-k
     (32, 64, 8, 16, 0.0),
-    (65536, 8, 1, 8, 0.0),      # largest single-workgroup input
+    (8192, 8, 1, 8, 0.0),       # largest single-workgroup input
+    (4097, 16, 2, 12, 0.0),     # 8194 assignments: smallest chunked input
     (40000, 64, 2, 48, 1.1),    # 80000 assignments: chunked count / scan / scatter kernels
     (20001, 256, 6, 200, 0.5),  # ragged last chunk of the chunked kernels
 ]
