@@ -26,10 +26,15 @@ Readings where the paper is silent (each is also listed with the design notes):
     applied to the sparse gate) unless renormalize=False;
   * the expert network is a SwiGLU feed-forward layer without biases:
     E(x) = W_down (silu(W_gate x) * (W_up x)), silu(z) = z / (1 + exp(-z));
+    or, for the paper's own setting (a Switch Transformer base model,
+    Experimental Setup), a two-layer ReLU feed-forward layer without biases:
+    E(x) = W_down relu(W_in x);
   * tokens are permuted into per-expert segments by a stable sort on the expert
     id of each (token, slot) assignment a = t*k + j;
   * the codec acts on the [T][d] block of hidden states (h = tokens, w = model
-    width, one slice), and U_hat, V_hat are inputs of their own.
+    width, one slice), and U_hat, V_hat are inputs of their own; with c slices
+    (X in R^{h x w x c}, one slice per sequence of a batch) every slice
+    X[s] = rows s*h .. (s+1)*h - 1 is coded with the same U, V.
 """
 from __future__ import annotations
 
@@ -160,9 +165,20 @@ def swiglu_expert(x_rows, w_gate_up_e, w_down_e):
     return act @ np.asarray(w_down_e, np.float64).T
 
 
-def expert_outputs(x, idx, w_gate_up, w_down):
+def relu_expert(x_rows, w_in_e, w_down_e):
+    """E(x) = W_down relu(W_in x) for a block of rows (the Switch Transformer FFN)."""
+    h = np.asarray(x_rows, np.float64) @ np.asarray(w_in_e, np.float64).T
+    return np.maximum(h, 0.0) @ np.asarray(w_down_e, np.float64).T
+
+
+EXPERTS = {"swiglu": swiglu_expert, "relu": relu_expert}
+
+
+def expert_outputs(x, idx, w_gate_up, w_down, activation="swiglu"):
     """Y_perm [T*k][d]: every assignment's expert output, in segment order.
-    w_gate_up[e] / w_down[e] may be any per-expert indexable of 2-D arrays."""
+    w_gate_up[e] / w_down[e] may be any per-expert indexable of 2-D arrays; for ReLU
+    experts w_gate_up[e] is W_in [H][d]."""
+    expert = EXPERTS[activation]
     M = len(w_gate_up)
     seg, perm_src, inv_perm = permute(idx, M)
     x = np.asarray(x, np.float64)
@@ -171,7 +187,7 @@ def expert_outputs(x, idx, w_gate_up, w_down):
     for e in range(M):
         lo, hi = int(seg[e]), int(seg[e + 1])
         if hi > lo:
-            y_perm[lo:hi] = swiglu_expert(x[perm_src[lo:hi]], w_gate_up[e], w_down[e])
+            y_perm[lo:hi] = expert(x[perm_src[lo:hi]], w_gate_up[e], w_down[e])
     return y_perm, seg, perm_src, inv_perm
 
 
@@ -185,9 +201,9 @@ def combine(y_perm, inv_perm, w):
     return y
 
 
-def moe_forward(x, idx, w, w_gate_up, w_down):
+def moe_forward(x, idx, w, w_gate_up, w_down, activation="swiglu"):
     """The sparse MoE output y [T][d] for given routing (idx, w)."""
-    y_perm, _, _, inv_perm = expert_outputs(x, idx, w_gate_up, w_down)
+    y_perm, _, _, inv_perm = expert_outputs(x, idx, w_gate_up, w_down, activation)
     return combine(y_perm, inv_perm, w)
 
 
@@ -206,12 +222,17 @@ def lowrank_decode(z, u_hat, v_hat):
 # ----------------------------------------------------------------------------- the layer
 
 def layer(x, mask_words, w_global, b_global, w_local, b_local, w_gate_up, w_down,
-          u, v, u_hat, v_hat, n_groups, top_k, renormalize=True):
+          u, v, u_hat, v_hat, n_groups, top_k, renormalize=True, activation="swiglu",
+          codec_slices=1):
     """Routing is taken on the end side from X; the experts run in the cloud on the
-    reconstruction X_hat = decode(encode(X)). Returns a dict of every stage output."""
+    reconstruction X_hat = decode(encode(X)), slice by slice. Returns a dict of every
+    stage output (z is [r_h][r_w] for one slice, [c][r_h][r_w] for c > 1)."""
     idx, w, g = group_gate(x, w_global, b_global, w_local, b_local, mask_words,
                            n_groups, top_k, renormalize)
-    z = lowrank_encode(x, u, v)
-    x_hat = lowrank_decode(z, u_hat, v_hat)
-    y = moe_forward(x_hat, idx, w, w_gate_up, w_down)
+    x = np.asarray(x, np.float64)
+    h = x.shape[0] // codec_slices
+    zs = [lowrank_encode(x[s * h:(s + 1) * h], u, v) for s in range(codec_slices)]
+    x_hat = np.concatenate([lowrank_decode(z_s, u_hat, v_hat) for z_s in zs], axis=0)
+    z = zs[0] if codec_slices == 1 else np.stack(zs)
+    y = moe_forward(x_hat, idx, w, w_gate_up, w_down, activation)
     return {"idx": idx, "w": w, "g": g, "z": z, "x_hat": x_hat, "y": y}

@@ -13,9 +13,12 @@ Shapes follow the paper's problem statement:
   * the hardware-aware candidate set E_local as a bitmask over the M experts
     (Local Expert Selection, Eq. 4),
   * SwiGLU expert weights W_gate_up [M][2H][d] (rows 0..H-1 gate branch, rows
-    H..2H-1 up branch) and W_down [M][d][H],
-  * codec projections U [T][r_h], V [d][r_w] (Encoder-Decoder based on
-    Low-Rank Compression, Z = U^T X V).
+    H..2H-1 up branch) and W_down [M][d][H], or for two-layer ReLU experts (the
+    Switch Transformer FFN of the paper's experiments) W_in [M][H][d] in the same
+    array and W_down [M][d][H],
+  * codec projections U [h][r_h], V [d][r_w] (Encoder-Decoder based on
+    Low-Rank Compression, Z = U^T X V), applied to each of the c slices X[s] =
+    rows s*h .. (s+1)*h - 1 of X, h = T / c.
 
 Every tensor has its own PCG64 stream, keyed by (seed, tensor tag[, expert]), so
 one expert's weights can be regenerated without drawing the others and the
@@ -65,10 +68,21 @@ class LayerConfig:
     keep_range: tuple = ()  # "per_call": n_keep drawn uniformly from this closed range
     n_calls: int = 1      # "per_call": number of distinct (X, mask) draws timed
     first_call_seed: int = 0
+    activation: str = "swiglu"  # expert FFN: "swiglu" or "relu"
+    codec_slices: int = 1  # c: X is c slices of h = T / c rows, each coded with the same U, V
 
     @property
     def group_size(self) -> int:
         return self.n_experts // self.n_groups
+
+    @property
+    def w_in_rows(self) -> int:
+        """Rows of one expert's input-layer weight (gate and up branches, or W_in)."""
+        return self.ffn_hidden if self.activation == "relu" else 2 * self.ffn_hidden
+
+    @property
+    def codec_h(self) -> int:
+        return self.n_tokens // self.codec_slices
 
     @property
     def n_assign(self) -> int:
@@ -108,6 +122,26 @@ CONFIGS = {
                           gate_std=0.02, n_calls=1000, first_call_seed=4),
 }
 CONFIG_ORDER = ["tiny", "small", "mixtral", "finegrained", "decode"]
+
+
+def switch_config(n_experts: int) -> LayerConfig:
+    """The paper's experimental setting (Parameter Selection): a batch of 4 sequences of
+    256 tokens, top-1 routing, a candidate set capped at 40% of the experts (here exactly
+    floor(0.4 M), drawn at random), experts in K = default_groups(M) groups. Experts are
+    Switch-style two-layer ReLU FFNs; the paper does not state the model width, so
+    d = 768 and H = 3072 are a stated synthetic choice. The codec treats each sequence
+    as one slice X[s] of 256 x 768 (X in R^{h x w x c} with h = 256, w = 768, c = 4),
+    rank 64 on both sides."""
+    M = n_experts
+    return LayerConfig(f"switch{M}", BF16, 1024, 768, M, default_groups(M), 3072, 1, 64, 64,
+                       seed=100 + M, mask="random", n_keep=(2 * M) // 5, x_dist="rms",
+                       gate_std=0.02, activation="relu", codec_slices=4)
+
+
+for _m in (8, 16, 32, 64):
+    CONFIGS[f"switch{_m}"] = switch_config(_m)
+SWITCH_ORDER = ["switch8", "switch16", "switch32", "switch64"]
+ALL_ORDER = CONFIG_ORDER + SWITCH_ORDER
 
 
 # ----------------------------------------------------------------------------- bit formats
@@ -208,9 +242,9 @@ class LayerInputs:
     b_global: np.ndarray   # [K] float32
     w_local: np.ndarray    # [M][d]
     b_local: np.ndarray    # [M] float32
-    w_gate_up: np.ndarray  # [M][2H][d]
+    w_gate_up: np.ndarray  # [M][2H][d] (SwiGLU) or [M][H][d] (ReLU)
     w_down: np.ndarray     # [M][d][H]
-    u: np.ndarray          # [T][r_h]
+    u: np.ndarray          # [h][r_h], h = T / codec_slices
     v: np.ndarray          # [d][r_w]
 
     def f64(self, name: str) -> np.ndarray:
@@ -239,10 +273,10 @@ def _zipf_biases(cfg: LayerConfig, seed: int):
 
 
 def gen_expert(cfg: LayerConfig, e: int, seed: Optional[int] = None):
-    """(W_gate_up[e] [2H][d], W_down[e] [d][H]) in storage format."""
+    """(W_gate_up[e] [2H][d] or W_in[e] [H][d], W_down[e] [d][H]) in storage format."""
     s = cfg.seed if seed is None else seed
     H, d = cfg.ffn_hidden, cfg.d_model
-    gu = _normal(s, (_TAG_WGU, e), (2 * H, d), cfg.expert_std)
+    gu = _normal(s, (_TAG_WGU, e), (cfg.w_in_rows, d), cfg.expert_std)
     dn = _normal(s, (_TAG_WD, e), (d, H), cfg.expert_std)
     if cfg.dtype == BF16:
         return f32_to_bf16_bits(gu), f32_to_bf16_bits(dn)
@@ -252,7 +286,7 @@ def gen_expert(cfg: LayerConfig, e: int, seed: Optional[int] = None):
 def gen_experts(cfg: LayerConfig, threads: Optional[int] = None):
     M, H, d = cfg.n_experts, cfg.ffn_hidden, cfg.d_model
     st = np.uint16 if cfg.dtype == BF16 else np.float32
-    w_gu = np.empty((M, 2 * H, d), dtype=st)
+    w_gu = np.empty((M, cfg.w_in_rows, d), dtype=st)
     w_dn = np.empty((M, d, H), dtype=st)
 
     def one(e):
@@ -298,9 +332,9 @@ def gen_layer(cfg: LayerConfig, call_seed: Optional[int] = None, experts: bool =
         w_gu, w_dn = gen_experts(cfg, threads)
     else:
         st = np.uint16 if cfg.dtype == BF16 else np.float32
-        w_gu = np.zeros((0, 2 * cfg.ffn_hidden, d), st)
+        w_gu = np.zeros((0, cfg.w_in_rows, d), st)
         w_dn = np.zeros((0, d, cfg.ffn_hidden), st)
-    u = haar_orthonormal(s, (_TAG_U,), T, cfg.r_h)
+    u = haar_orthonormal(s, (_TAG_U,), cfg.codec_h, cfg.r_h)
     v = haar_orthonormal(s, (_TAG_V,), d, cfg.r_w)
     return LayerInputs(cfg, x, mask, _store(w_global, cfg.dtype), b_global,
                        _store(w_local, cfg.dtype), b_local, w_gu, w_dn,

@@ -305,6 +305,77 @@ def test_top1_combine_is_a_gather_and_zero_rows_stay_zero():
     assert np.all(y[3] == 0.0)
 
 
+# ----------------------------------------------------------------------------- ReLU experts
+
+def test_relu_expert_hand_example():
+    c = _load("relu_hand.json")
+    y = O.relu_expert(np.array(c["x"]), np.array(c["w_in"][0]), np.array(c["w_down"][0]))
+    np.testing.assert_array_equal(y[0], np.array(c["y"]))
+    # the same through the MoE path: one expert, top-1, weight 1
+    y2 = O.moe_forward(np.array(c["x"]), np.zeros((1, 1), np.int32), np.ones((1, 1)),
+                       np.array(c["w_in"]), np.array(c["w_down"]), activation="relu")
+    np.testing.assert_array_equal(y2[0], np.array(c["y"]))
+
+
+def test_one_expert_relu_moe_is_dense_relu_ffn():
+    """A 1-expert ReLU MoE (gate forced by a one-expert candidate set) equals a dense
+    ReLU FFN built from torch's linear and relu."""
+    rng = np.random.default_rng(16)
+    T, d, H = 19, 24, 56
+    x = rng.standard_normal((T, d))
+    w_in = rng.standard_normal((1, H, d)) * 0.3
+    wd = rng.standard_normal((1, d, H)) * 0.3
+    wg, bg, wl, bl = np.zeros((1, d)), np.zeros(1), rng.standard_normal((1, d)), np.zeros(1)
+    idx, w, _ = O.group_gate(x, wg, bg, wl, bl, [1], 1, 1)
+    y = O.moe_forward(x, idx, w, w_in, wd, activation="relu")
+    f = torch.nn.functional
+    xt, wi, wdn = (torch.tensor(a, dtype=torch.float64) for a in (x, w_in[0], wd[0]))
+    np.testing.assert_allclose(y, f.linear(f.relu(f.linear(xt, wi)), wdn).numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_relu_expert_identities():
+    """relu(z) - relu(-z) = z, so E(x) - E(-x) = W_down W_in x; and E(a x) = a E(x) for
+    a > 0 (positive homogeneity of a bias-free ReLU network)."""
+    rng = np.random.default_rng(17)
+    T, d, H = 13, 10, 30
+    x = rng.standard_normal((T, d))
+    w_in = rng.standard_normal((H, d))
+    wd = rng.standard_normal((d, H))
+    e_pos, e_neg = O.relu_expert(x, w_in, wd), O.relu_expert(-x, w_in, wd)
+    np.testing.assert_allclose(e_pos - e_neg, x @ (wd @ w_in).T, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(O.relu_expert(2.5 * x, w_in, wd), 2.5 * e_pos, rtol=1e-13, atol=1e-13)
+    # a row whose every hidden unit is negative gives a zero output
+    x1 = -np.abs(rng.standard_normal((1, d)))
+    np.testing.assert_array_equal(O.relu_expert(x1, np.abs(w_in), wd), np.zeros((1, d)))
+
+
+def test_relu_top1_moe_matches_per_token_definition():
+    """Top-1 routing over ReLU experts, token by token against Eq. (1) with one term."""
+    rng = np.random.default_rng(18)
+    T, d, H, M = 27, 8, 16, 5
+    x = rng.standard_normal((T, d))
+    w_in = rng.standard_normal((M, H, d)) * 0.5
+    wd = rng.standard_normal((M, d, H)) * 0.5
+    idx, w = W.gen_routing(T, M, 1, [0, 2, 3, 4], seed=4)
+    y = O.moe_forward(x, idx, w, w_in, wd, activation="relu")
+    for t in range(T):
+        e = int(idx[t, 0])
+        h = np.maximum(w_in[e] @ x[t], 0.0)
+        np.testing.assert_allclose(y[t], float(w[t, 0]) * (wd[e] @ h), rtol=1e-12, atol=1e-12)
+
+
+def test_switch_workloads_follow_the_parameter_selection():
+    """4 x 256 tokens, top-1, 8/16/32/64 experts, candidate set at most 40% of them."""
+    for n in W.SWITCH_ORDER:
+        cfg = W.CONFIGS[n]
+        assert cfg.n_tokens == 4 * 256 and cfg.top_k == 1 and cfg.codec_slices == 4
+        assert cfg.n_experts in (8, 16, 32, 64) and cfg.activation == "relu"
+        x, mask = W.gen_call(cfg)
+        kept = W.mask_members(mask, cfg.n_experts)
+        assert len(kept) == int(0.4 * cfg.n_experts) and len(kept) <= 0.4 * cfg.n_experts
+        assert cfg.w_in_rows == cfg.ffn_hidden
+
+
 # ----------------------------------------------------------------------------- codec
 
 def test_codec_full_rank_round_trip():
@@ -336,6 +407,30 @@ def test_codec_projection_identities():
     # U = I reduces to the one-sided product X V
     zi = O.lowrank_encode(x, np.eye(T), v)
     np.testing.assert_allclose(zi, x @ v, rtol=1e-13, atol=1e-13)
+
+
+def test_layer_codes_each_slice_separately():
+    """c slices: every slice s of X is projected on its own, X_hat[s] = U U^T X[s] V V^T,
+    and a full-rank codec round-trips every slice."""
+    rng = np.random.default_rng(15)
+    c, h, d, M, H = 3, 8, 6, 4, 8
+    x = rng.standard_normal((c * h, d))
+    u = W.haar_orthonormal(2, (1,), h, 5)
+    v = W.haar_orthonormal(2, (2,), d, 4)
+    w_in = rng.standard_normal((M, H, d))
+    wd = rng.standard_normal((M, d, H))
+    wl = rng.standard_normal((M, d))
+    out = O.layer(x, [0b1111], np.zeros((2, d)), np.zeros(2), wl, np.zeros(M), w_in, wd,
+                  u, v, u, v, 2, 1, activation="relu", codec_slices=c)
+    assert out["z"].shape == (c, 5, 4)
+    for s in range(c):
+        xs = x[s * h:(s + 1) * h]
+        np.testing.assert_allclose(out["z"][s], u.T @ xs @ v, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(out["x_hat"][s * h:(s + 1) * h], u @ u.T @ xs @ v @ v.T, atol=1e-12)
+    uf, vf = W.haar_orthonormal(3, (1,), h, h), W.haar_orthonormal(3, (2,), d, d)
+    full = O.layer(x, [0b1111], np.zeros((2, d)), np.zeros(2), wl, np.zeros(M), w_in, wd,
+                   uf, vf, uf, vf, 2, 1, activation="relu", codec_slices=c)
+    np.testing.assert_allclose(full["x_hat"], x, atol=1e-13)
 
 
 def test_codec_eckart_young():
