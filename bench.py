@@ -3,8 +3,9 @@
 
 One step is the whole path on one batch: route X with the hardware-aware group gate,
 compress it with the low-rank encoder, reconstruct it with the decoder, and run the
-sparse SwiGLU MoE layer on the reconstruction with the gate's routing (permute,
-grouped expert GEMMs, combine). Inputs are seeded synthetic tensors of the workload's
+sparse MoE layer (SwiGLU, or two-layer ReLU experts for the paper-shaped "switch"
+workloads) on the reconstruction with the gate's routing (permute, grouped expert
+GEMMs, combine). Inputs are seeded synthetic tensors of the workload's
 shape, resident in HBM before timing. Default workload: the Mixtral-shaped layer
 (T=4096 tokens, d=4096, 8 experts in 2 groups, SwiGLU hidden 14336, top-2, codec
 rank 256).
@@ -32,12 +33,12 @@ def log(msg):
 
 
 def parse():
-    from paper_2508_06024_amd.workload import CONFIG_ORDER
+    from paper_2508_06024_amd.workload import ALL_ORDER
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default 50; 1000 for 'decode')")
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="mixtral", choices=CONFIG_ORDER)
+    ap.add_argument("--workload", default="mixtral", choices=ALL_ORDER)
     ap.add_argument("--rotate", type=int, default=4, help="distinct copies of X cycled through the steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
@@ -57,7 +58,8 @@ def blas_threads():
 
 def cpu_baseline(inp, cfg, target_s):
     """The oracle's step (gate, encode, decode, experts, combine) on the first S tokens,
-    with U restricted to those rows; weights are upcast to float64 before timing."""
+    with U restricted to those rows (one codec slice) or on the first S / h whole slices
+    (several slices); weights are upcast to float64 before timing."""
     import oracle as O
     from paper_2508_06024_amd import workload as W
     f = inp.f64
@@ -66,21 +68,26 @@ def cpu_baseline(inp, cfg, target_s):
     gu = [W.to_f64(inp.w_gate_up[e], cfg.dtype) for e in range(cfg.n_experts)]
     dn = [W.to_f64(inp.w_down[e], cfg.dtype) for e in range(cfg.n_experts)]
 
+    c, h = cfg.codec_slices, cfg.codec_h
+
     def run(S):
         t = time.perf_counter()
-        O.layer(x[:S], inp.mask, wg, inp.b_global, wl, inp.b_local, gu, dn, u[:S], v, u[:S], v,
-                cfg.n_groups, cfg.top_k)
+        uu = u[:S] if c == 1 else u
+        O.layer(x[:S], inp.mask, wg, inp.b_global, wl, inp.b_local, gu, dn, uu, v, uu, v,
+                cfg.n_groups, cfg.top_k, activation=cfg.activation, codec_slices=max(1, S // h) if c > 1 else 1)
         return time.perf_counter() - t
 
     T = cfg.n_tokens
-    S0 = min(T, max(cfg.r_h, 64))
+    quantum = h if c > 1 else 64
+    S0 = min(T, max(cfg.r_h, quantum))
     t0 = run(S0)
     S = int(min(T, max(S0, S0 * target_s / max(t0, 1e-6))))
-    S = max(cfg.r_h, (S // 64) * 64) if S < T else T
+    S = max(S0, (S // quantum) * quantum) if S < T else T
     t = run(S) if S != S0 else t0
     return {"value": S / t, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
             "sample": f"oracle step (gate, encode, decode, experts, combine) on the first {S} of {T} tokens "
-                      f"of the same inputs, U restricted to those rows, float64, {t:.1f} s",
+                      f"of the same inputs" + (", U restricted to those rows" if c == 1 else
+                                                f", {S // h} of {c} codec slices") + f", float64, {t:.1f} s",
             "seconds": round(t, 2)}
 
 
@@ -122,7 +129,8 @@ def main():
         masks = [inp.mask]
     layer = Ec2moeLayer(xs[0], masks[0], up(inp.w_global), f32(inp.b_global), up(inp.w_local), f32(inp.b_local),
                         up(inp.w_gate_up), up(inp.w_down), up(inp.u), up(inp.v),
-                        n_groups=cfg.n_groups, top_k=cfg.top_k)
+                        n_groups=cfg.n_groups, top_k=cfg.top_k, activation=cfg.activation,
+                        codec_slices=cfg.codec_slices)
 
     def step(i):
         layer.set_input(xs[i % len(xs)], masks[i % len(masks)])
@@ -245,8 +253,10 @@ def main():
         "dtype": cfg.dtype,
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: T={cfg.n_tokens} d={cfg.d_model} experts={cfg.n_experts} "
-                               f"groups={cfg.n_groups} SwiGLU H={cfg.ffn_hidden} top-{cfg.top_k} "
-                               f"codec {cfg.r_h}x{cfg.r_w}, mask={cfg.mask}",
+                               f"groups={cfg.n_groups} {'ReLU' if cfg.activation == 'relu' else 'SwiGLU'} "
+                               f"H={cfg.ffn_hidden} top-{cfg.top_k} codec {cfg.r_h}x{cfg.r_w}"
+                               + (f" on {cfg.codec_slices} slices of {cfg.codec_h} tokens" if cfg.codec_slices > 1
+                                  else "") + f", mask={cfg.mask}" + (f" keeping {cfg.n_keep}" if cfg.n_keep else ""),
                    "tokens_per_step": cfg.n_tokens},
         "roofline": roof,
         "layer_roofline_frac": round(step_roof_ms / ms_step, 4),

@@ -49,9 +49,13 @@ typedef enum {
 /* flags of ec2moe_moe_desc */
 #define EC2MOE_GATE_RENORMALIZE 1u /* selected gate weights are divided by their sum (Eq. 1:
                                       the gate weights of a token sum to 1); else raw g */
+#define EC2MOE_EXPERT_RELU 2u      /* expert networks are two-layer ReLU feed-forward layers,
+                                      E(x) = W_out relu(W_in x), as in the Switch Transformer
+                                      base model of the paper's experiments (Experimental
+                                      Setup); else SwiGLU. Changes the layout of w_gate_up. */
 
 /* Shape of one MoE layer call: T tokens of width d, M experts in K contiguous equal
- * groups (group k = experts [k*M/K, (k+1)*M/K)), SwiGLU hidden width H, top-k routing. */
+ * groups (group k = experts [k*M/K, (k+1)*M/K)), expert hidden width H, top-k routing. */
 typedef struct {
     int32_t n_tokens;   /* T */
     int32_t n_experts;  /* M */
@@ -60,7 +64,7 @@ typedef struct {
     int32_t ffn_hidden; /* H */
     int32_t top_k;      /* k */
     int32_t dtype;      /* ec2moe_dtype of x, gate weights, expert weights and y */
-    uint32_t flags;     /* EC2MOE_GATE_RENORMALIZE or 0 */
+    uint32_t flags;     /* OR of EC2MOE_GATE_RENORMALIZE, EC2MOE_EXPERT_RELU, or 0 */
 } ec2moe_moe_desc;
 
 /* Shape of the codec: n_slices blocks X[c] of h x w (h = tokens, w = model width),
@@ -118,13 +122,15 @@ ec2moe_status ec2moe_permute(const ec2moe_moe_desc* desc, const int32_t* topk_id
                              hipStream_t stream);
 
 /*
- * The expert networks E_i of Eq. 1 as SwiGLU feed-forward layers,
- * E(x) = W_down (silu(W_gate x) * (W_up x)), on permuted rows:
+ * The expert networks E_i of Eq. 1 on permuted rows:
  *   y_perm[p] = E_e(x[perm_src[p]]) for every position p of segment e.
- *   x [T][d]; seg_offsets [M+1], perm_src [T*k] as from ec2moe_permute;
- *   w_gate_up [M][2H][d] (rows 0..H-1 gate branch, H..2H-1 up branch); w_down [M][d][H];
- *   act [T*k][H] out or NULL: silu(gate) * up in the layer dtype;
- *   y_perm [T*k][d] out.
+ * Default: SwiGLU feed-forward layers, E(x) = W_down (silu(W_gate x) * (W_up x)),
+ *   w_gate_up [M][2H][d] (rows 0..H-1 gate branch, H..2H-1 up branch);
+ *   act [T*k][H] out or NULL: silu(gate) * up in the layer dtype.
+ * With EC2MOE_EXPERT_RELU: two-layer ReLU feed-forward layers, E(x) = W_down relu(W_in x),
+ *   w_gate_up [M][H][d] holding W_in; act [T*k][H] out or NULL: relu(W_in x).
+ * Both: x [T][d]; seg_offsets [M+1], perm_src [T*k] as from ec2moe_permute;
+ *   w_down [M][d][H]; y_perm [T*k][d] out.
  * Intermediates are accumulated in float32 and rounded once to the layer dtype.
  */
 ec2moe_status ec2moe_expert_ffn(const ec2moe_moe_desc* desc, const void* x,
@@ -145,8 +151,8 @@ ec2moe_status ec2moe_combine(const ec2moe_moe_desc* desc, const void* y_perm,
  * Sparse MoE layer output, Eq. 1, for given routing: permute, expert networks,
  * combine. y[t] = sum_j topk_w[t][j] * E_{topk_idx[t][j]}(x[t]).
  *   x [T][d]; topk_idx [T][k] int32 in [0, M); topk_w [T][k] float32;
- *   w_gate_up [M][2H][d]; w_down [M][d][H]; y [T][d] out; ws of
- *   ec2moe_moe_workspace_size bytes.
+ *   w_gate_up [M][2H][d] (SwiGLU) or [M][H][d] (EC2MOE_EXPERT_RELU); w_down [M][d][H];
+ *   y [T][d] out; ws of ec2moe_moe_workspace_size bytes.
  * Routing may come from ec2moe_group_gate on other hidden states (the end-cloud split:
  * route on X, run the experts on the reconstruction X_hat).
  */

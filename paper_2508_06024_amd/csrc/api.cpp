@@ -67,8 +67,8 @@ ec2moe_status check_moe_desc(const ec2moe_moe_desc* d) {
             "n_groups %d does not divide n_experts %d", d->n_groups, d->n_experts);
     REQUIRE(d->top_k <= d->n_experts, EC2MOE_ERR_INVALID_ARGUMENT, "top_k %d > n_experts %d", d->top_k,
             d->n_experts);
-    REQUIRE((d->flags & ~EC2MOE_GATE_RENORMALIZE) == 0, EC2MOE_ERR_INVALID_ARGUMENT, "unknown flags 0x%x",
-            d->flags);
+    REQUIRE((d->flags & ~(EC2MOE_GATE_RENORMALIZE | EC2MOE_EXPERT_RELU)) == 0, EC2MOE_ERR_INVALID_ARGUMENT,
+            "unknown flags 0x%x", d->flags);
     REQUIRE(d->n_experts <= kMaxExperts, EC2MOE_ERR_UNSUPPORTED, "n_experts %d > %d", d->n_experts, kMaxExperts);
     REQUIRE(d->n_experts + d->n_groups <= kMaxGateRows, EC2MOE_ERR_UNSUPPORTED, "n_experts + n_groups > %d",
             kMaxGateRows);
@@ -322,12 +322,15 @@ hipError_t run_experts(const ec2moe_moe_desc* desc, const void* x, const int32_t
     const DType dt = static_cast<DType>(desc->dtype);
     const int64_t A = static_cast<int64_t>(desc->n_tokens) * desc->top_k;
     const int d = desc->d_model, H = desc->ffn_hidden;
+    // SwiGLU: [2H][d] gate and up rows per expert; ReLU: [H][d] input-layer rows
+    const bool relu = (desc->flags & EC2MOE_EXPERT_RELU) != 0;
+    const int64_t w_in_rows = relu ? H : int64_t(2) * H;
     GemmArgs g1{};
     g1.tok = x; g1.row_index = perm_src; g1.w = w_gate_up;
-    g1.w_group_stride = int64_t(2) * H * d; g1.seg = seg; g1.n_groups = desc->n_experts;
-    g1.rows = A; g1.K = d; g1.N = H; g1.out = act; g1.ldo = H; g1.name = "expert_gate_up";
-    g1.src_rows = desc->n_tokens; g1.w_rows = int64_t(2) * H; g1.part = part; g1.max_split = kMaxSplit;
-    hipError_t e = launch_gemm(dt, Epilogue::SwiGLU, OutType::Same, g1, stream);
+    g1.w_group_stride = w_in_rows * d; g1.seg = seg; g1.n_groups = desc->n_experts;
+    g1.rows = A; g1.K = d; g1.N = H; g1.out = act; g1.ldo = H; g1.name = relu ? "expert_in_relu" : "expert_gate_up";
+    g1.src_rows = desc->n_tokens; g1.w_rows = w_in_rows; g1.part = part; g1.max_split = kMaxSplit;
+    hipError_t e = launch_gemm(dt, relu ? Epilogue::ReLU : Epilogue::SwiGLU, OutType::Same, g1, stream);
     if (e != hipSuccess) return e;
     GemmArgs g2{};
     g2.tok = act; g2.row_index = nullptr; g2.w = w_down;

@@ -34,6 +34,9 @@
 //
 // SwiGLU epilogue: the weight tile holds TN/2 gate rows followed by the matching TN/2 up
 // rows; each wave owns equal gate and up slices, so silu(gate) * up is formed in registers.
+// ReLU epilogue (hidden layer of a two-layer ReLU expert): the plain store with max(v, 0)
+// applied to the float32 sums before rounding, in every store path including the split-K
+// reduction.
 #include "device_common.h"
 #include "internal.h"
 
@@ -191,6 +194,17 @@ __device__ __forceinline__ float silu(float g) {
     return g * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
+// Plain-store epilogue: max(v, 0) when the GEMM carries the ReLU flag (the hidden layer of
+// a two-layer ReLU expert), else v. The flag is uniform over the launch.
+__device__ __forceinline__ float store_act(const GemmArgs& a, float v) { return a.relu ? fmaxf(v, 0.f) : v; }
+__device__ __forceinline__ f32x4 store_act(const GemmArgs& a, f32x4 v) {
+    if (a.relu) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.f);
+    }
+    return v;
+}
+
 template <typename TO>
 __device__ __forceinline__ void store4(TO* dst, f32x4 v);
 
@@ -245,7 +259,7 @@ __device__ __forceinline__ void write_tile(const GemmArgs& a, const TileInfo& ti
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) {
                 const int col = ti.nt * TN + wn * (TN / WN) + ni * 16 + 4 * lg;
-                if (col < a.N) store4<TO>(orow + col, acc[ni][mi]);
+                if (col < a.N) store4<TO>(orow + col, store_act(a, acc[ni][mi]));
             }
         }
     }
@@ -430,7 +444,7 @@ __device__ __forceinline__ void write_tile32(const GemmArgs& a, const TileInfo& 
                     const int col = ti.nt * TN + wn * (TN / WN) + ni * 32 + 8 * q + 4 * lh;
                     f32x4 v;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) v[i] = acc[ni][mi][4 * q + i];
+                    for (int i = 0; i < 4; ++i) v[i] = store_act(a, acc[ni][mi][4 * q + i]);
                     if (col < a.N) store4<TO>(orow + col, v);
                 }
             }
@@ -915,7 +929,8 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
                     float v[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        v[e] = SWIGLU ? silu(acc[ni][mi][4 * q + e]) * acc[ni + NB][mi][4 * q + e] : acc[ni][mi][4 * q + e];
+                        v[e] = SWIGLU ? silu(acc[ni][mi][4 * q + e]) * acc[ni + NB][mi][4 * q + e]
+                                       : store_act(a, acc[ni][mi][4 * q + e]);
                     bf16x4 o;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(v[e]);
@@ -947,7 +962,7 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
 }
 
 // Sums the float32 partial tiles of the split tail in chunk order and applies the
-// epilogue (store, or silu(gate) * up) of the large-tile kernel. One workgroup per
+// epilogue (store, ReLU store, or silu(gate) * up) of the large-tile kernel. One workgroup per
 // (tail tile, 16 rows); every thread owns a run of 4 output columns per pass and issues
 // the loads of all chunks before adding them in order.
 template <int TM, int TN, bool SWIGLU, typename TO>
@@ -996,7 +1011,7 @@ __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs a) {
             if (ti.nt * NOUT + c < a.N) store4<TO>(orow + ti.nt * NOUT + c, v);
         } else {
             const int col = ti.nt * TN + c;
-            if (col < a.N) store4<TO>(orow + col, sg);
+            if (col < a.N) store4<TO>(orow + col, store_act(a, sg));
         }
     }
 }
@@ -1106,8 +1121,10 @@ size_t gemm_split_scratch_bytes() {
                     static_cast<size_t>(gemm_slots<128, 128>()) * 128 * 128) * sizeof(float);
 }
 
-hipError_t launch_gemm(DType dt, Epilogue epi, OutType ot, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_gemm(DType dt, Epilogue epi, OutType ot, const GemmArgs& args, hipStream_t s) {
     const bool sw = epi == Epilogue::SwiGLU;
+    GemmArgs a = args;
+    a.relu = epi == Epilogue::ReLU ? 1 : 0;
     if (dt == DType::BF16) {
         if (sw) return dispatch<bf16_t, bf16_t, true>(a, s);
         if (ot == OutType::F32) return dispatch<bf16_t, float, false>(a, s);

@@ -54,8 +54,8 @@ hipError_t launch_gather_rows(DType dt, const void* x, int64_t n_src, const int3
 // out[p][n] = sum_k tok[row(p)][k] * w_e[n][k] for every row p of group e, where
 // row(p) = row_index ? row_index[p] : p and w_e = w + e * w_group_stride.
 // SwiGLU mode: weight rows 0..N-1 are the gate branch and N..2N-1 the up branch; the
-// output is silu(gate) * up with N columns.
-enum class Epilogue : int { Store = 0, SwiGLU = 1 };
+// output is silu(gate) * up with N columns. ReLU mode: out = max(sum, 0).
+enum class Epilogue : int { Store = 0, SwiGLU = 1, ReLU = 2 };
 enum class OutType : int { Same = 0, F32 = 1 };
 
 struct GemmArgs {
@@ -79,6 +79,7 @@ struct GemmArgs {
     // part == nullptr or max_split <= 1 disables the split.
     float* part;              // [slots][TM][TN] float32 scratch
     int max_split;
+    int relu;                 // set by launch_gemm from the epilogue: plain stores take max(v, 0)
 };
 // Bytes of `part` scratch the large-tile GEMM may use (0 if it cannot split).
 size_t gemm_split_scratch_bytes();

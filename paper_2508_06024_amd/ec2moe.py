@@ -19,6 +19,8 @@ LIB_PATH = os.path.join(_HERE, "libec2moe.so")
 
 F32, BF16 = 0, 1
 GATE_RENORMALIZE = 1
+EXPERT_RELU = 2
+ACTIVATIONS = ("swiglu", "relu")
 
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "too few candidates",
           4: "workspace too small", 5: "HIP error"}
@@ -113,10 +115,18 @@ def _dev(t: torch.Tensor, name: str, dtype=None, shape=None):
     return t
 
 
-def moe_desc(n_tokens, n_experts, n_groups, d_model, ffn_hidden, top_k, dtype, renormalize=True) -> MoeDesc:
+def moe_desc(n_tokens, n_experts, n_groups, d_model, ffn_hidden, top_k, dtype, renormalize=True,
+             activation="swiglu") -> MoeDesc:
+    if activation not in ACTIVATIONS:
+        raise ValueError(f"activation must be one of {ACTIVATIONS}, got {activation!r}")
+    flags = (GATE_RENORMALIZE if renormalize else 0) | (EXPERT_RELU if activation == "relu" else 0)
     return MoeDesc(n_tokens, n_experts, n_groups, d_model, ffn_hidden, top_k,
-                   dtype if isinstance(dtype, int) else dtype_code(dtype),
-                   GATE_RENORMALIZE if renormalize else 0)
+                   dtype if isinstance(dtype, int) else dtype_code(dtype), flags)
+
+
+def w_in_rows(ffn_hidden: int, activation: str) -> int:
+    """Rows of one expert's input-layer weight: gate and up branches (SwiGLU) or W_in (ReLU)."""
+    return ffn_hidden if activation == "relu" else 2 * ffn_hidden
 
 
 def mask_array(words: Sequence[int]):
@@ -189,17 +199,17 @@ def permute(topk_idx, n_experts, x=None, d_model=None, dtype=None, ws=None):
     return seg, perm_src, inv_perm, x_perm
 
 
-def expert_ffn(x, seg_offsets, perm_src, w_gate_up, w_down, top_k, with_act=False, ws=None):
+def expert_ffn(x, seg_offsets, perm_src, w_gate_up, w_down, top_k, with_act=False, ws=None,
+               activation="swiglu"):
     T, d = x.shape
-    M, H2, _ = w_gate_up.shape
-    H = H2 // 2
+    M, _, H = w_down.shape
     dt = x.dtype
     _dev(x, "x", dt)
-    _dev(w_gate_up, "w_gate_up", dt, (M, 2 * H, d))
+    _dev(w_gate_up, "w_gate_up", dt, (M, w_in_rows(H, activation), d))
     _dev(w_down, "w_down", dt, (M, d, H))
     _dev(seg_offsets, "seg_offsets", torch.int32, (M + 1,))
     _dev(perm_src, "perm_src", torch.int32, (T * top_k,))
-    desc = moe_desc(T, M, 1, d, H, top_k, dt)
+    desc = moe_desc(T, M, 1, d, H, top_k, dt, activation=activation)
     ws = ws if ws is not None else workspace(moe_workspace_size(desc), x.device)
     act = torch.empty((T * top_k, H), dtype=dt, device=x.device) if with_act else None
     y_perm = torch.empty((T * top_k, d), dtype=dt, device=x.device)
@@ -228,18 +238,17 @@ def moe_forward_into(desc: MoeDesc, x, topk_idx, topk_w, w_gate_up, w_down, y, w
                                    _ptr(w_gate_up), _ptr(w_down), _ptr(y), _ptr(ws), ws.numel(), _stream()))
 
 
-def moe_forward(x, topk_idx, topk_w, w_gate_up, w_down, ws=None):
+def moe_forward(x, topk_idx, topk_w, w_gate_up, w_down, ws=None, activation="swiglu"):
     T, d = x.shape
-    M, H2, _ = w_gate_up.shape
-    H = H2 // 2
+    M, _, H = w_down.shape
     k = topk_idx.shape[1]
     dt = x.dtype
     _dev(x, "x", dt)
     _dev(topk_idx, "topk_idx", torch.int32, (T, k))
     _dev(topk_w, "topk_w", torch.float32, (T, k))
-    _dev(w_gate_up, "w_gate_up", dt, (M, 2 * H, d))
+    _dev(w_gate_up, "w_gate_up", dt, (M, w_in_rows(H, activation), d))
     _dev(w_down, "w_down", dt, (M, d, H))
-    desc = moe_desc(T, M, 1, d, H, k, dt)
+    desc = moe_desc(T, M, 1, d, H, k, dt, activation=activation)
     ws = ws if ws is not None else workspace(moe_workspace_size(desc), x.device)
     y = torch.empty((T, d), dtype=dt, device=x.device)
     moe_forward_into(desc, x, topk_idx, topk_w, w_gate_up, w_down, y, ws)

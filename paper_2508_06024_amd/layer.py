@@ -2,7 +2,8 @@
 
 The step follows the paper's pipeline (EC2MoE Overall Design; HL-GGN then PO-ECC):
 the end side routes the hidden states X with the hardware-aware group gate and
-compresses them, Z = U^T X V; the cloud side reconstructs X_hat = U_hat Z V_hat^T and
+compresses them, Z = U^T X V (per slice of h = T / c rows); the cloud side
+reconstructs X_hat = U_hat Z V_hat^T and
 runs the sparse MoE layer of Eq. 1 on X_hat with the end side's routing:
 
     route = group_gate(X, mask);  Z = encode(X);  X_hat = decode(Z);  y = moe(X_hat, route)
@@ -19,9 +20,10 @@ from . import ec2moe as E
 
 class Ec2moeLayer:
     def __init__(self, x, mask_words, w_global, b_global, w_local, b_local, w_gate_up, w_down, u, v,
-                 u_hat=None, v_hat=None, n_groups=1, top_k=1, renormalize=True):
+                 u_hat=None, v_hat=None, n_groups=1, top_k=1, renormalize=True, activation="swiglu",
+                 codec_slices=1):
         T, d = x.shape
-        M, H2, _ = w_gate_up.shape
+        M, _, H = w_down.shape
         dt = x.dtype
         dev = x.device
         self.x, self.mask = x, list(mask_words)
@@ -30,11 +32,15 @@ class Ec2moeLayer:
         self.u, self.v = u, v
         self.u_hat = u if u_hat is None else u_hat
         self.v_hat = v if v_hat is None else v_hat
-        self.moe_desc = E.moe_desc(T, M, n_groups, d, H2 // 2, top_k, dt, renormalize)
-        self.codec_desc = E.codec_desc(T, d, u.shape[1], v.shape[1], dt)
+        if tuple(w_gate_up.shape) != (M, E.w_in_rows(H, activation), d):
+            raise ValueError(f"w_gate_up has shape {tuple(w_gate_up.shape)} for {activation} experts of width {H}")
+        self.moe_desc = E.moe_desc(T, M, n_groups, d, H, top_k, dt, renormalize, activation)
+        if T % codec_slices or u.shape[0] != T // codec_slices:
+            raise ValueError(f"u has {u.shape[0]} rows for {codec_slices} slices of {T} tokens")
+        self.codec_desc = E.codec_desc(T // codec_slices, d, u.shape[1], v.shape[1], dt, codec_slices)
         self.topk_idx = torch.empty((T, top_k), dtype=torch.int32, device=dev)
         self.topk_w = torch.empty((T, top_k), dtype=torch.float32, device=dev)
-        self.z = torch.empty((u.shape[1], v.shape[1]), dtype=torch.float32, device=dev)
+        self.z = torch.empty((codec_slices, u.shape[1], v.shape[1]), dtype=torch.float32, device=dev)
         self.x_hat = torch.empty((T, d), dtype=dt, device=dev)
         self.y = torch.empty((T, d), dtype=dt, device=dev)
         self.moe_ws = E.workspace(E.moe_workspace_size(self.moe_desc), dev)

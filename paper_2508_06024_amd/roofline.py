@@ -31,15 +31,23 @@ def kernel_work(cfg, rows_per_expert: np.ndarray) -> dict:
     A = T * k
     act = int(np.count_nonzero(rows_per_expert))
     rh, rw = cfg.r_h, cfg.r_w
-    return {
+    c = getattr(cfg, "codec_slices", 1)
+    h = T // c
+    work = {
         "gate": (2.0 * T * d * (M + K), T * d * s + (M + K) * d * s + 8.0 * T * k),
-        "expert_gate_up": (4.0 * A * d * H, act * 2.0 * H * d * s + A * d * s + A * H * s),
         "expert_down": (2.0 * A * H * d, act * 1.0 * d * H * s + A * H * s + A * d * s),
         "combine": (2.0 * A * d, A * d * s + 8.0 * T * k + T * d * s),
         "permute": (0.0, 4.0 * A + 12.0 * A),
-        "encode": (2.0 * T * d * rw + 2.0 * rh * rw * T, T * d * s + (T * rh + d * rw) * s + 4.0 * rh * rw),
-        "decode": (2.0 * d * rw * rh + 2.0 * T * rh * d, T * d * s + (T * rh + d * rw) * s + 4.0 * rh * rw),
+        # per slice: X V then U^T (X V); U and V read once for all slices
+        "encode": (2.0 * T * d * rw + 2.0 * rh * rw * T, T * d * s + (h * rh + d * rw) * s + 4.0 * c * rh * rw),
+        # per slice: V Z^T then U (V Z^T)^T
+        "decode": (c * 2.0 * d * rw * rh + 2.0 * T * rh * d, T * d * s + (h * rh + d * rw) * s + 4.0 * c * rh * rw),
     }
+    if getattr(cfg, "activation", "swiglu") == "relu":
+        work["expert_in_relu"] = (2.0 * A * d * H, act * 1.0 * H * d * s + A * d * s + A * H * s)
+    else:
+        work["expert_gate_up"] = (4.0 * A * d * H, act * 2.0 * H * d * s + A * d * s + A * H * s)
+    return work
 
 
 def source_digest(*names: str) -> str:

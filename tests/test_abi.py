@@ -74,6 +74,16 @@ def test_descriptor_validation(kw, status):
         assert E.last_error()
 
 
+def test_descriptor_flags():
+    d = _desc(activation="relu")
+    assert d.flags == E.GATE_RENORMALIZE | E.EXPERT_RELU
+    assert _ws_size(d)[0] == OK
+    d.flags = 4  # no such flag
+    assert _ws_size(d)[0] == INVALID and "flags" in E.last_error()
+    with pytest.raises(ValueError):
+        _desc(activation="gelu")
+
+
 def test_workspace_size_grows_with_tokens():
     _, a = _ws_size(_desc(n_tokens=64))
     _, b = _ws_size(_desc(n_tokens=4096))

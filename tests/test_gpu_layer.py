@@ -16,30 +16,35 @@ def build(inp):
     dt = cfg.dtype
     return Ec2moeLayer(up(inp.x, dt), inp.mask, up(inp.w_global, dt), up_f32(inp.b_global), up(inp.w_local, dt),
                        up_f32(inp.b_local), up(inp.w_gate_up, dt), up(inp.w_down, dt), up(inp.u, dt),
-                       up(inp.v, dt), n_groups=cfg.n_groups, top_k=cfg.top_k)
+                       up(inp.v, dt), n_groups=cfg.n_groups, top_k=cfg.top_k, activation=cfg.activation,
+                       codec_slices=cfg.codec_slices)
 
 
 def oracle_sampled(inp, toks):
     """Oracle layer outputs of the sampled tokens: the gate and the experts act per token;
-    the codec's Z couples all tokens and is computed in full."""
+    the codec's Z couples all tokens of a slice and is computed in full, slice by slice."""
     cfg = inp.cfg
     f = inp.f64
     x, u, v = f("x"), f("u"), f("v")
     idx, w, g = O.group_gate(x[toks], f("w_global"), inp.b_global, f("w_local"), inp.b_local, inp.mask,
                              cfg.n_groups, cfg.top_k)
-    z = O.lowrank_encode(x, u, v)
-    xh = O.lowrank_decode(z, u[toks], v)
+    h = cfg.codec_h
+    z = np.stack([O.lowrank_encode(x[s * h:(s + 1) * h], u, v) for s in range(cfg.codec_slices)])
+    xh = np.stack([O.lowrank_decode(z[t // h], u[[t % h]], v)[0] for t in toks])
     y = np.zeros((len(toks), cfg.d_model))
+    expert = O.EXPERTS[cfg.activation]
     for e in np.unique(idx):
         gu = W.to_f64(inp.w_gate_up[e], cfg.dtype)
         dn = W.to_f64(inp.w_down[e], cfg.dtype)
         rows, slots = np.nonzero(idx == e)
-        y[rows] += w[rows, slots, None] * O.swiglu_expert(xh[rows], gu, dn)
+        y[rows] += w[rows, slots, None] * expert(xh[rows], gu, dn)
     return idx, w, g, z, xh, y
 
 
 @pytest.mark.parametrize("name,call,sample", [("tiny", None, 0), ("small", None, 0), ("mixtral", None, 40),
-                                              ("finegrained", None, 40), ("decode", 4, 0), ("decode", 777, 0)])
+                                              ("finegrained", None, 40), ("decode", 4, 0), ("decode", 777, 0),
+                                              ("switch8", None, 0), ("switch16", None, 64),
+                                              ("switch32", None, 64), ("switch64", None, 0)])
 def test_layer_step_matches_oracle(name, call, sample):
     cfg = W.CONFIGS[name]
     say(f"layer {name} call {call}")
@@ -57,7 +62,7 @@ def test_layer_step_matches_oracle(name, call, sample):
     idx, w, g, z, xh, y = oracle_sampled(inp, toks)
     gidx, gw = down(lay.topk_idx)[toks], down(lay.topk_w)[toks]
     n_cert = check_routing(gidx, gw, idx, w, g, W.mask_members(inp.mask, cfg.n_experts), cfg.top_k)
-    assert_close(down(lay.z), z, 1e-5, "Z")
+    assert_close(down(lay.z).reshape(z.shape), z, 1e-5, "Z")
     assert_close(down(lay.x_hat)[toks], xh, tol(cfg.dtype), "X_hat")
     same = ~(gidx != idx).any(axis=1)
     e = assert_close(down(lay.y)[toks][same], y[same], tol(cfg.dtype), "y")

@@ -1,5 +1,6 @@
 """Parity of the dispatch, expert-network, combine and MoE-forward kernels with the
-oracle (Mixture-of-Experts, Eq. 1, with SwiGLU expert networks), on seeded routing."""
+oracle (Mixture-of-Experts, Eq. 1, with SwiGLU or two-layer ReLU expert networks), on
+seeded routing."""
 import numpy as np
 import pytest
 import torch
@@ -59,7 +60,8 @@ class Layer:
     """Seeded inputs of one workload on host and device, with seeded routing."""
 
     def __init__(self, name, call_seed=None, **scale):
-        cfg = W.CONFIGS[name].scaled(**scale) if scale else W.CONFIGS[name]
+        cfg = name if isinstance(name, W.LayerConfig) else W.CONFIGS[name]
+        cfg = cfg.scaled(**scale) if scale else cfg
         say(f"generating {cfg.name} T={cfg.n_tokens} d={cfg.d_model} M={cfg.n_experts} H={cfg.ffn_hidden}")
         self.cfg = cfg
         self.inp = W.gen_layer(cfg, call_seed=call_seed)
@@ -86,7 +88,7 @@ class Layer:
                 need.setdefault(int(self.idx[t, j]), []).append((r, j, t))
         for e, items in need.items():
             gu, dn = self.expert_f64(e)
-            rows = O.swiglu_expert(x[[t for _, _, t in items]], gu, dn)
+            rows = O.EXPERTS[self.cfg.activation](x[[t for _, _, t in items]], gu, dn)
             for (r, j, _), row in zip(items, rows):
                 out[r, j] = row
         return out
@@ -96,7 +98,7 @@ _CACHE = {}
 
 
 def layer(name, **scale):
-    key = (name, tuple(sorted(scale.items())))
+    key = (name.name if isinstance(name, W.LayerConfig) else name, tuple(sorted(scale.items())))
     if key not in _CACHE:
         _CACHE.clear()
         torch.cuda.empty_cache()
@@ -207,3 +209,70 @@ def test_moe_forward_empty():
     x = L.x[:0]
     y = E.moe_forward(x, L.d_idx[:0], L.d_w[:0], L.wgu, L.wdn)
     assert y.shape == (0, L.cfg.d_model)
+
+
+# ----------------------------------------------------------------------------- ReLU experts
+
+def _relu_cfg(name, dtype, T, d, M, K, H, k, seed, n_keep=0):
+    return W.LayerConfig(name, dtype, T, d, M, K, H, k, 16, 16, seed=seed,
+                         mask="random" if n_keep else "all", n_keep=n_keep, x_dist="rms",
+                         activation="relu")
+
+
+RELU_FULL = [
+    # every assignment against the oracle, activation included
+    _relu_cfg("relu_f32", W.F32, 64, 128, 8, 2, 256, 2, seed=30, n_keep=6),   # fp32 register-staged GEMM
+    _relu_cfg("relu_split", W.BF16, 64, 4096, 1, 1, 256, 1, seed=31),          # 2 tiles, K=4096: split-K reduce
+    W.CONFIGS["switch8"],                                                     # paper shape, 3 candidates
+    W.CONFIGS["switch64"],                                                    # paper shape, 25 candidates
+]
+
+
+@pytest.mark.parametrize("cfg", RELU_FULL, ids=lambda c: c.name)
+def test_relu_expert_ffn_full(cfg):
+    say(f"relu experts {cfg.name} T={cfg.n_tokens} d={cfg.d_model} M={cfg.n_experts} H={cfg.ffn_hidden}")
+    L = layer(cfg)
+    seg, src, inv, _ = E.permute(L.d_idx, cfg.n_experts)
+    y_perm, act = E.expert_ffn(L.x, seg, src, L.wgu, L.wdn, cfg.top_k, with_act=True, activation="relu")
+    y = E.moe_forward(L.x, L.d_idx, L.d_w, L.wgu, L.wdn, activation="relu")
+    torch.cuda.synchronize()
+    x = L.inp.f64("x")
+    used = np.unique(L.idx)
+    w_in = {int(e): W.to_f64(L.inp.w_gate_up[e], cfg.dtype) for e in used}
+    dn = {int(e): W.to_f64(L.inp.w_down[e], cfg.dtype) for e in used}
+    w_in_all = [w_in.get(e) for e in range(cfg.n_experts)]
+    dn_all = [dn.get(e) for e in range(cfg.n_experts)]
+    ry_perm, rseg, rsrc, rinv = O.expert_outputs(x, L.idx, w_in_all, dn_all, "relu")
+    e1 = assert_close(down(y_perm)[down(inv)], ry_perm[rinv], tol(cfg.dtype), "y_perm")
+    # relu(W_in x) of every position, from the definition
+    ract = np.zeros((rsrc.size, cfg.ffn_hidden))
+    for e in used:
+        lo, hi = rseg[e], rseg[e + 1]
+        ract[lo:hi] = np.maximum(x[rsrc[lo:hi]] @ w_in[int(e)].T, 0.0)
+    got_act = down(act)
+    assert np.all(got_act >= 0.0), "ReLU activation has negative entries"
+    e2 = assert_close(got_act[down(inv)], ract[rinv], tol(cfg.dtype), "act")
+    ry = O.combine(ry_perm, rinv, L.w)
+    e3 = assert_close(down(y), ry, tol(cfg.dtype), "y")
+    say(f"  {cfg.name}: y_perm {e1:.2e} act {e2:.2e} y {e3:.2e}")
+
+
+def test_relu_moe_forward_large_tiles_sampled():
+    """Enough rows per expert for the 256x256 ping-pong GEMM and its split-K tail, with
+    the ReLU applied in the staged epilogue; the oracle computes a sample of tokens."""
+    cfg = _relu_cfg("relu_big", W.BF16, 8192, 1024, 8, 2, 2048, 1, seed=32)
+    L = layer(cfg)
+    y = E.moe_forward(L.x, L.d_idx, L.d_w, L.wgu, L.wdn, activation="relu")
+    torch.cuda.synchronize()
+    toks = sample_tokens(cfg.n_tokens)
+    per = L.oracle_assignments(toks)
+    ry = np.einsum("tk,tkd->td", L.w[toks].astype(np.float64), per)
+    e = assert_close(down(y)[toks], ry, tol(cfg.dtype), "y (sampled)")
+    say(f"  relu_big: y sampled rel err {e:.2e} over {len(toks)} tokens")
+
+
+def test_relu_and_swiglu_weights_are_not_interchangeable():
+    """The binding checks the input-layer weight shape against the activation."""
+    L = layer(W.CONFIGS["switch8"])
+    with pytest.raises(ValueError):
+        E.moe_forward(L.x, L.d_idx, L.d_w, L.wgu, L.wdn, activation="swiglu")
