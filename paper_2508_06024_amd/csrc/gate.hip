@@ -1,28 +1,32 @@
 // Hardware-aware lightweight group gate (Local Expert Selection, Eq. 4; Lightweight
 // Group Gate Network, Eq. 5-7) and top-k selection, for gfx950.
 //
-// One workgroup (4 or 8 waves) takes 16 tokens. Phase 1 computes the M local and K group
-// logits of those tokens with the matrix cores: gate-weight rows are the A operand,
-// token rows the B operand, and each wave contracts a quarter of d. Phase 2 adds the
-// partial sums in a fixed order (deterministic). Phase 3 gives each wave its tokens:
-// masked group softmax (stage 1), masked in-group softmax (stage 2), the product
-// g_i = p_group^(k) * p_local,i^(k), top-k by rank (ties to the lower expert index), and
-// renormalisation of the selected weights.
+// One workgroup takes a tile of TT = 16 * NB tokens. Phase 1 computes the M local and K
+// group logits of the tile with the matrix cores: gate-weight rows are the A operand,
+// token rows the B operand, and each of the WAVES waves contracts its share of d (all
+// its loads of a batch issued before the first MFMA). Phase 2 adds the partial sums in a
+// fixed order (deterministic) and the biases, and sets the local logits of non-candidates
+// to -inf. Phase 3 gives every token one lane of the first wave: the lane reads a group's
+// logits from LDS in one batch (its own column, no cross-lane traffic) and computes the
+// masked in-group softmax statistics (stage 2), the masked group softmax (stage 1), the
+// product g_i = p_group^(k) * p_local,i^(k) and a running top-k in registers (ties to the
+// lower expert index), then renormalises the selected weights. The other waves leave
+// after phase 2.
+//
+// Tiles of two 16-token blocks (NB = 2) halve the gate-weight reads per
+// token; they pay off when the gate has many rows and there are enough tokens to give
+// every CU a tile.
 #include "device_common.h"
 #include "internal.h"
 
 namespace ec2moe {
 namespace {
 
-constexpr int kTok = 16;           // tokens per workgroup
-constexpr int kMaxRowBlocks = 20;  // M + K <= 320 gate rows
+constexpr int kBlock = 16;          // tokens per MFMA block
+constexpr int kMaxRowBlocks = 20;   // M + K <= 320 gate rows
 constexpr int kMaxGroups = 160;
 constexpr int kMaxExperts = 256;
-constexpr int kMaxTopK = 16;
-
-__device__ __forceinline__ bool is_cand(const uint64_t* mask, int e) {
-    return (mask[e >> 6] >> (e & 63)) & 1ull;
-}
+constexpr int kChunk = 8;           // logits of one group read together in phase 3
 
 // Keeps a kernel-argument value in a scalar register: left alone, the compiler may reload
 // it from the argument segment at every use, and each reload waits on that memory.
@@ -35,53 +39,214 @@ __device__ __forceinline__ V pin(V v) {
 // e^x with the hardware 2^x (within about 1 ulp); the gate's probabilities are float32
 __device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
 
-// NRB: blocks of 16 gate rows (M + K <= 16 * NRB); WAVES: waves splitting d.
-template <typename T, int NRB, int WAVES>
+// Inserts (g, i) into the descending list (sv, si) of KP entries. Candidates arrive in
+// ascending index order and only a strictly larger g moves an entry down, so equal
+// values keep the lower index first.
+template <int KP>
+__device__ __forceinline__ void topk_insert(float (&sv)[KP], int (&si)[KP], float g, int i) {
+#pragma unroll
+    for (int j = KP - 1; j > 0; --j) {
+        const bool above = g > sv[j - 1];
+        const bool here = g > sv[j];
+        sv[j] = above ? sv[j - 1] : (here ? g : sv[j]);
+        si[j] = above ? si[j - 1] : (here ? i : si[j]);
+    }
+    const bool top = g > sv[0];
+    sv[0] = top ? g : sv[0];
+    si[0] = top ? i : si[0];
+}
+
+// Butterfly over the lanes of an aligned segment of `width` lanes (a power of two <= 8).
+__device__ __forceinline__ float seg_max(float v, int width) {
+    for (int off = 1; off < width; off <<= 1) v = fmaxf(v, __shfl_xor(v, off, 8));
+    return v;
+}
+__device__ __forceinline__ float seg_sum(float v, int width) {
+    for (int off = 1; off < width; off <<= 1) v += __shfl_xor(v, off, 8);
+    return v;
+}
+
+// Routing of token tl of the tile by its 8 lanes (sub-lane s holds experts s*EPL ..
+// s*EPL + EPL - 1, EPL = M / 8, all in group (s*EPL) / Mk, whose LG = Mk / EPL lanes are
+// aligned). Logits come from the summed, biased, masked rows in LDS; the token's fused
+// probabilities are kept in LDS (wave 1's partials, free after phase 2) for the outputs.
+//   stage 2: group max and sum of e^(l - max), lane-local then across the group's lanes;
+//   stage 1: softmax over the groups that hold a candidate, across the 8 lanes;
+//   fusion (Eq. 7) and top-k: every lane keeps its experts' keys (g truncated to its
+//   top 24 bits, then 255 - i) sorted, then three bitonic merges across the lanes leave
+//   the token's first KP keys in every lane. Distinct truncated values order as the
+//   exact ones; if two of the first k + 1 keys share their truncated g, lane 0 redoes the
+//   selection exactly from the stored probabilities (ties to the lower index).
+template <int KP>
+__device__ __forceinline__ void route_octet(float* part, int n_el, int TT, int tl, int s, int t0, int n_tokens,
+                                            int M, int Mk, int KT, bool renormalize, float* probs,
+                                            int32_t* topk_idx, float* topk_w) {
+    const int EPL = M >> 3;
+    const int LG = Mk / EPL;
+    const int t = t0 + tl;
+    const bool live = t < n_tokens;
+    const float* lg = part;
+    float* gb = part + n_el + static_cast<size_t>(tl) * M;  // this token's g, -1 off the candidate set
+    const int i0 = s * EPL;
+    const int grp = i0 / Mk;
+
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = j < EPL ? lg[(i0 + j) * TT + tl] : -INFINITY;
+    const float G = lg[(M + grp) * TT + tl];
+
+    float m = v[0];
+#pragma unroll
+    for (int j = 1; j < 8; ++j) m = fmaxf(m, v[j]);
+    m = seg_max(m, LG);
+    const bool active = m != -INFINITY;
+    float sum = 0.f;
+    if (active) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (v[j] != -INFINITY) sum += fast_exp(v[j] - m);
+    }
+    sum = seg_sum(sum, LG);
+
+    const float gmax = seg_max(active ? G : -INFINITY, 8);
+    const bool leader = (s & (LG - 1)) == 0;
+    const float gsum = seg_sum(leader && active ? fast_exp(G - gmax) : 0.f, 8);
+    const float pg = fast_exp(G - gmax) * __builtin_amdgcn_rcpf(gsum);
+    const float rs = __builtin_amdgcn_rcpf(sum);
+
+    uint32_t sk[KP];
+#pragma unroll
+    for (int j = 0; j < KP; ++j) sk[j] = 0;
+    float* prow = probs && live ? probs + static_cast<size_t>(t) * M : nullptr;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (j < EPL) {
+            const int i = i0 + j;
+            float g = -1.f;
+            if (v[j] != -INFINITY) {
+                g = pg * (fast_exp(v[j] - m) * rs);
+                const uint32_t key = ((__float_as_uint(g) << 2) & 0xffffff00u) | static_cast<uint32_t>(255 - i);
+#pragma unroll
+                for (int q = KP - 1; q > 0; --q) sk[q] = max(sk[q], min(sk[q - 1], key));
+                sk[0] = max(sk[0], key);
+            }
+            gb[i] = g;
+            if (prow) prow[i] = g < 0.f ? 0.f : g;
+        }
+    }
+    // merge with the lists of the lanes 1, 2, 4 apart: the elementwise max of one list and
+    // the other reversed is bitonic and holds the first KP of both; sort it descending
+#pragma unroll
+    for (int off = 1; off < 8; off <<= 1) {
+        uint32_t o[KP];
+#pragma unroll
+        for (int j = 0; j < KP; ++j) o[j] = __shfl_xor(sk[j], off, 8);
+#pragma unroll
+        for (int j = 0; j < KP; ++j) sk[j] = max(sk[j], o[KP - 1 - j]);
+#pragma unroll
+        for (int len = KP / 2; len >= 1; len >>= 1)
+#pragma unroll
+            for (int j = 0; j < KP; ++j)
+                if ((j & len) == 0) {
+                    const uint32_t a = sk[j], b = sk[j + len];
+                    sk[j] = max(a, b);
+                    sk[j + len] = min(a, b);
+                }
+    }
+    bool amb = false;
+#pragma unroll
+    for (int j = 0; j + 1 < KP; ++j)
+        if (j < KT && (sk[j] >> 8) == (sk[j + 1] >> 8)) amb = true;
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's probabilities are in LDS
+    __builtin_amdgcn_wave_barrier();
+    if (!live) return;
+    int32_t* oi = topk_idx + static_cast<size_t>(t) * KT;
+    float* ow = topk_w + static_cast<size_t>(t) * KT;
+    if (!amb) {
+        float gs[KP];
+        float denom = 0.f;
+#pragma unroll
+        for (int j = 0; j < KP; ++j) {
+            gs[j] = j < KT ? gb[255 - static_cast<int>(sk[j] & 0xffu)] : 0.f;
+            if (j < KT) denom += gs[j];
+        }
+#pragma unroll
+        for (int j = 0; j < KP; ++j)
+            if (j < KT && (j & 7) == s) {
+                oi[j] = 255 - static_cast<int>(sk[j] & 0xffu);
+                ow[j] = renormalize ? gs[j] / denom : gs[j];
+            }
+        return;
+    }
+    if (s != 0) return;
+    float sv[KP];
+    int si[KP];
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+        sv[j] = -1.f;
+        si[j] = 0;
+    }
+    for (int c = 0; c < M; c += 8) {
+        float g[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) g[u] = gb[c + u];  // M is a multiple of 8
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (g[u] >= 0.f) topk_insert<KP>(sv, si, g[u], c + u);
+    }
+    float denom = 0.f;
+#pragma unroll
+    for (int j = 0; j < KP; ++j)
+        if (j < KT) denom += sv[j];
+#pragma unroll
+    for (int j = 0; j < KP; ++j)
+        if (j < KT) {
+            oi[j] = si[j];
+            ow[j] = renormalize ? sv[j] / denom : sv[j];
+        }
+}
+
+// NRB: blocks of 16 gate rows (M + K <= 16 * NRB); NB: 16-token blocks per tile;
+// WAVES: waves splitting d; KP: top-k list length (>= k).
+template <typename T, int NRB, int NB, int WAVES, int KP>
 __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
-    extern __shared__ float part[];  // [WAVES][NRB*16 rows][16 tokens], then the sums in wave 0's slot
-    __shared__ float grp_max[WAVES][kMaxGroups];
-    __shared__ float grp_sum[WAVES][kMaxGroups];
-    __shared__ float grp_lg[WAVES][kMaxGroups];  // a wave's biased group logits
-    __shared__ float loc[WAVES][kMaxExperts];  // a wave's biased local logits (-inf off the candidate set), then g
-    __shared__ float sel_g[WAVES][kMaxTopK];
-    __shared__ int sel_i[WAVES][kMaxTopK];
-    __shared__ float s_bl[kMaxExperts];        // b_local (0 if absent)
-    __shared__ float s_bg[kMaxGroups];         // b_global (0 if absent)
+    constexpr int TT = kBlock * NB;
+    static_assert(TT <= 64, "phase 3 gives each token one lane of wave 0");
+    extern __shared__ float part[];  // [WAVES][NRB*16 rows][TT tokens]; sums land in wave 0's slot
+    __shared__ float s_bl[kMaxExperts];            // b_local (0 if absent)
+    __shared__ float s_bg[kMaxGroups];             // b_global (0 if absent)
     __shared__ unsigned char s_cand[kMaxExperts];  // candidate flags of the mask
 
     constexpr int EPC = Elem<T>::kPerChunk;
     constexpr int SLICE = 4 * EPC;  // k covered by one matrix-core step
-    // k-slices whose loads are issued together: deep for few gate rows, shallow for many
-    // (U (NRB + 1) uint4 registers; the budget shrinks with more waves per SIMD)
-    // (one batch covers a wave's whole share of d = 4096 with 8 waves and one row block)
+    // k-slices whose loads are issued together: U * (NB + NRB) 16-byte registers per lane
     constexpr int UB = WAVES <= 8 ? 40 : 16;
-    constexpr int U = UB / (NRB + 1) < 1 ? 1 : (UB / (NRB + 1) > 16 ? 16 : UB / (NRB + 1));
+    constexpr int U = UB / (NB + NRB) < 1 ? 1 : (UB / (NB + NRB) > 16 ? 16 : UB / (NB + NRB));
     constexpr int THREADS = 64 * WAVES;
-    constexpr int TPW = kTok / WAVES;  // tokens per wave in the softmax phase
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int g4 = lane >> 4;
     const int M = pin(p.n_experts), K = pin(p.n_groups), d = pin(p.d);
-    const int KT = pin(p.top_k);
     const int n_tokens = pin(p.n_tokens);
-    const bool renormalize = pin(static_cast<int>(p.renormalize)) != 0;
-    float* const probs = pin(p.probs);
-    int32_t* const topk_idx = pin(p.topk_idx);
-    float* const topk_w = pin(p.topk_w);
     const int R = M + K;
-    const int t0 = blockIdx.x * kTok;
+    const int Mk = M / K;
+    const int t0 = blockIdx.x * TT;
 
-    // biases staged once (read by the softmax phase; the barrier after phase 1 orders them)
-    for (int i = threadIdx.x; i < M; i += 64 * WAVES) {
+    // mask and biases staged once (read by phase 2 after the first barrier)
+    for (int i = threadIdx.x; i < M; i += THREADS) {
         s_bl[i] = p.b_local ? p.b_local[i] : 0.f;
-        s_cand[i] = is_cand(p.mask, i) ? 1 : 0;
+        s_cand[i] = (p.mask[i >> 6] >> (i & 63)) & 1ull ? 1 : 0;
     }
-    for (int i = threadIdx.x; i < K; i += 64 * WAVES) s_bg[i] = p.b_global ? p.b_global[i] : 0.f;
+    for (int kk = threadIdx.x; kk < K; kk += THREADS) s_bg[kk] = p.b_global ? p.b_global[kk] : 0.f;
 
     // ---------------- phase 1: partial logits over this wave's share of d
-    int tok = t0 + (lane & 15);
-    if (tok >= n_tokens) tok = n_tokens - 1;
-    const T* xrow = static_cast<const T*>(p.x) + static_cast<size_t>(tok) * d + g4 * EPC;
+    const T* xrow[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        int tok = t0 + nb * kBlock + (lane & 15);
+        if (tok >= n_tokens) tok = n_tokens - 1;
+        xrow[nb] = static_cast<const T*>(p.x) + static_cast<size_t>(tok) * d + g4 * EPC;
+    }
     const T* wrow[NRB];
     bool wvalid[NRB];
 #pragma unroll
@@ -95,188 +260,276 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     const int kq = d / WAVES;
     const int kbeg = wave * kq;
 
-    f32x4 acc[NRB];
+    f32x4 acc[NRB][NB];
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    int k = kbeg;
-    for (; k + U * SLICE <= kbeg + kq; k += U * SLICE) {
-        uint4 bx[U], aw[U][NRB];
+    // batches of U slices; the last batch of a wave may be partial (its missing slices
+    // contribute zero products)
+    const int kend = kbeg + kq;
+    for (int k = kbeg; k < kend; k += U * SLICE) {
+        uint4 bx[U][NB], aw[U][NRB];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            bx[u] = ldg16(xrow + k + u * SLICE);
+            const bool in = k + u * SLICE < kend;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) bx[u][nb] = in ? ldg16(xrow[nb] + k + u * SLICE) : make_uint4(0, 0, 0, 0);
 #pragma unroll
             for (int rb = 0; rb < NRB; ++rb)
-                aw[u][rb] = wvalid[rb] ? ldg16(wrow[rb] + k + u * SLICE) : make_uint4(0, 0, 0, 0);
+                aw[u][rb] = in && wvalid[rb] ? ldg16(wrow[rb] + k + u * SLICE) : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int rb = 0; rb < NRB; ++rb) acc[rb] = Mfma<T>::step(aw[u][rb], bx[u], acc[rb]);
-    }
-    for (; k < kbeg + kq; k += SLICE) {
-        const uint4 bx = ldg16(xrow + k);
+            for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-        for (int rb = 0; rb < NRB; ++rb) {
-            const uint4 aw = wvalid[rb] ? ldg16(wrow[rb] + k) : make_uint4(0, 0, 0, 0);
-            acc[rb] = Mfma<T>::step(aw, bx, acc[rb]);
-        }
+                for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = Mfma<T>::step(aw[u][rb], bx[u][nb], acc[rb][nb]);
     }
 
-    constexpr int ROWS_PAD = NRB * 16;
-    constexpr int N_EL = ROWS_PAD * kTok;
+    constexpr int N_EL = NRB * 16 * TT;
     float* mine = part + static_cast<size_t>(wave) * N_EL;
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) mine[(rb * 16 + g4 * 4 + i) * kTok + (lane & 15)] = acc[rb][i];
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mine[(rb * 16 + g4 * 4 + i) * TT + nb * kBlock + (lane & 15)] = acc[rb][nb][i];
     __syncthreads();
 
-    // ---------------- phase 2: fixed-order sum of the partials
+    // ---------------- phase 2: fixed-order sum of the partials, then the biases; local
+    // logits off the candidate set become -inf (Eq. 4 applied before both softmaxes)
     for (int i = threadIdx.x; i < N_EL; i += THREADS) {
         float sum = part[i];
 #pragma unroll
         for (int w = 1; w < WAVES; ++w) sum += part[w * N_EL + i];
+        const int r = i / TT;
+        if (r < M) sum = s_cand[r] ? sum + s_bl[r] : -INFINITY;
+        else if (r < R) sum += s_bg[r - M];
         part[i] = sum;
     }
     __syncthreads();
 
-    // ---------------- phase 3: two-stage softmax, fusion, top-k; TPW tokens per wave.
-    // Each wave works on its own LDS rows with wave-level ordering only. Values every lane
-    // needs (group softmax, the rank order) are read back from LDS by all lanes in the
-    // same order instead of cross-lane shuffles, whose latency chains dominated.
-    const float* logit = part;  // [row][token]
-    const int Mk = M / K;
-    const int Mpad = (M + 3) & ~3;
-    auto wave_sync = [] {
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS traffic is done
-        __builtin_amdgcn_wave_barrier();
-    };
-    for (int it = 0; it < TPW; ++it) {
-        const int tl = wave * TPW + it;
-        const int t = t0 + tl;
-        float* gl = loc[wave];
+    // ---------------- phase 3
+    const int KT = pin(p.top_k);
+    const bool renormalize = pin(static_cast<int>(p.renormalize)) != 0;
+    float* const probs = pin(p.probs);
+    // Regular shapes (M a multiple of 8 up to 64, the experts of each of 8 lanes inside one
+    // group, whose lanes are a power of two): 8 lanes per token.
+    const int EPL = M >> 3;
+    const int LG = EPL > 0 ? Mk / EPL : 0;
+    if ((M & 7) == 0 && M <= 64 && Mk % EPL == 0 && (LG & (LG - 1)) == 0 && KT < KP) {
+        if (wave * 8 >= TT) return;
+        route_octet<KP>(part, N_EL, TT, wave * 8 + (lane >> 3), lane & 7, t0, n_tokens, M, Mk, KT, renormalize,
+                        probs, p.topk_idx, p.topk_w);
+        return;
+    }
 
-        // biased logits: local ones of the candidates (lane owns experts lane + 64 q), group ones
-        float lv[4];
+    // General shapes: one lane per token of the tile.
+    if (wave != 0) return;
+    const int tl = lane;
+    const int t = t0 + tl;
+    if (tl >= TT || t >= n_tokens) return;
+    const float* lg = part;    // biased logits [row][TT], -inf off the candidate set
+    float* gst = part + N_EL;  // this lane's stage-2 statistics: max at [kk][TT], sum at [K + kk][TT]
+                               // (wave 1's partials, free after phase 2; N_EL >= 2 K TT since M >= K)
+
+    // stage 2 statistics per group: max over its candidates and the sum of e^(l - max) in
+    // expert order; stage 1 maximum over the groups that hold a candidate
+    float gmax = -INFINITY;
+    for (int kk = 0; kk < K; ++kk) {
+        const int i0 = kk * Mk;
+        const float G = lg[(M + kk) * TT + tl];
+        float m = -INFINITY, s = 0.f;
+        if (Mk <= kChunk) {
+            float v[kChunk];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = lane + 64 * q;
-            lv[q] = -INFINITY;
-            if (i < M && s_cand[i]) lv[q] = logit[i * kTok + tl] + s_bl[i];
-            if (i < M) gl[i] = lv[q];
-        }
-        for (int kk = lane; kk < K; kk += 64) grp_lg[wave][kk] = logit[(M + kk) * kTok + tl] + s_bg[kk];
-        wave_sync();
-
-        // stage 2 statistics per group over its candidates: max and sum of exp
-        for (int kk = lane; kk < K; kk += 64) {
-            float m = -INFINITY;
-            for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) m = fmaxf(m, gl[i]);
-            float sum = 0.f;
+            for (int u = 0; u < kChunk; ++u) v[u] = u < Mk ? lg[(i0 + u) * TT + tl] : -INFINITY;
+#pragma unroll
+            for (int u = 0; u < kChunk; ++u) m = fmaxf(m, v[u]);
+            if (m != -INFINITY) {
+#pragma unroll
+                for (int u = 0; u < kChunk; ++u)
+                    if (v[u] != -INFINITY) s += fast_exp(v[u] - m);
+            }
+        } else {
+            for (int c = 0; c < Mk; c += kChunk) {
+                float v[kChunk];
+#pragma unroll
+                for (int u = 0; u < kChunk; ++u) v[u] = c + u < Mk ? lg[(i0 + c + u) * TT + tl] : -INFINITY;
+#pragma unroll
+                for (int u = 0; u < kChunk; ++u) m = fmaxf(m, v[u]);
+            }
             if (m != -INFINITY)
-                for (int i = kk * Mk; i < (kk + 1) * Mk; ++i) {
-                    const float l = gl[i];
-                    if (l != -INFINITY) sum += fast_exp(l - m);
-                }
-            grp_max[wave][kk] = m;
-            grp_sum[wave][kk] = sum;
-        }
-        wave_sync();
-
-        // stage 1: softmax over the groups that hold a candidate (every lane, group order)
-        float gmax = -INFINITY;
-        for (int kk = 0; kk < K; ++kk)
-            if (grp_max[wave][kk] != -INFINITY) gmax = fmaxf(gmax, grp_lg[wave][kk]);
-        float gsum = 0.f;
-        for (int kk = 0; kk < K; ++kk)
-            if (grp_max[wave][kk] != -INFINITY) gsum += fast_exp(grp_lg[wave][kk] - gmax);
-        const float rgsum = __builtin_amdgcn_rcpf(gsum);
-
-        // fusion, Eq. 7: g_i = p_group^(k) * p_local,i^(k); -1 marks a non-candidate
-        float gv[4];
+                for (int c = 0; c < Mk; c += kChunk) {
+                    float v[kChunk];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = lane + 64 * q;
-            gv[q] = -1.f;
-            if (lv[q] != -INFINITY) {
-                const int kk = i / Mk;
-                const float pg = fast_exp(grp_lg[wave][kk] - gmax) * rgsum;
-                const float pl = fast_exp(lv[q] - grp_max[wave][kk]) * __builtin_amdgcn_rcpf(grp_sum[wave][kk]);
-                gv[q] = pg * pl;
+                    for (int u = 0; u < kChunk; ++u) v[u] = c + u < Mk ? lg[(i0 + c + u) * TT + tl] : -INFINITY;
+#pragma unroll
+                    for (int u = 0; u < kChunk; ++u)
+                        if (v[u] != -INFINITY) s += fast_exp(v[u] - m);
+                }
+        }
+        gst[kk * TT + tl] = m;
+        gst[(K + kk) * TT + tl] = s;
+        if (m != -INFINITY) gmax = fmaxf(gmax, G);
+    }
+    // stage 1: softmax over the groups that hold a candidate
+    float gsum = 0.f;
+    for (int kk = 0; kk < K; ++kk)
+        if (gst[kk * TT + tl] != -INFINITY) gsum += fast_exp(lg[(M + kk) * TT + tl] - gmax);
+    const float rgsum = __builtin_amdgcn_rcpf(gsum);
+
+    // Fusion (Eq. 7) of expert i of group kk: g_i = p_group^(kk) * p_local,i^(kk). The same
+    // expression everywhere below, so a recomputed g has the same bits.
+    auto fused = [&](int kk, float v) {
+        const float pg = fast_exp(lg[(M + kk) * TT + tl] - gmax) * rgsum;
+        return pg * (fast_exp(v - gst[kk * TT + tl]) * __builtin_amdgcn_rcpf(gst[(K + kk) * TT + tl]));
+    };
+    float* prow = probs ? probs + static_cast<size_t>(t) * M : nullptr;
+    int32_t* oi = p.topk_idx + static_cast<size_t>(t) * KT;
+    float* ow = p.topk_w + static_cast<size_t>(t) * KT;
+
+    // Fast top-k: keys (g truncated to its top 24 bits, then 255 - i) kept sorted by a
+    // min/max network, two instructions per slot. Distinct truncated values order as the
+    // exact ones, so the result is exact unless two of the first k + 1 keys share their
+    // truncated g; such tokens take the exact pass below.
+    bool exact_pass = KT >= KP;
+    if (!exact_pass) {
+        uint32_t sk[KP];
+#pragma unroll
+        for (int j = 0; j < KP; ++j) sk[j] = 0;
+        for (int kk = 0; kk < K; ++kk) {
+            const int i0 = kk * Mk;
+            for (int c = 0; c < Mk; c += kChunk) {
+                float v[kChunk];
+#pragma unroll
+                for (int u = 0; u < kChunk; ++u) v[u] = c + u < Mk ? lg[(i0 + c + u) * TT + tl] : -INFINITY;
+                if (gst[kk * TT + tl] == -INFINITY) {  // no candidate in this group
+                    if (prow)
+                        for (int u = 0; u < kChunk && c + u < Mk; ++u) prow[i0 + c + u] = 0.f;
+                    continue;
+                }
+                const float pg = fast_exp(lg[(M + kk) * TT + tl] - gmax) * rgsum;
+                const float m = gst[kk * TT + tl];
+                const float rs = __builtin_amdgcn_rcpf(gst[(K + kk) * TT + tl]);
+#pragma unroll
+                for (int u = 0; u < kChunk; ++u) {
+                    if (c + u >= Mk) break;
+                    const int i = i0 + c + u;
+                    float g = 0.f;
+                    if (v[u] != -INFINITY) {
+                        g = pg * (fast_exp(v[u] - m) * rs);
+                        const uint32_t key = ((__float_as_uint(g) << 2) & 0xffffff00u) | static_cast<uint32_t>(255 - i);
+#pragma unroll
+                        for (int j = KP - 1; j > 0; --j) sk[j] = max(sk[j], min(sk[j - 1], key));
+                        sk[0] = max(sk[0], key);
+                    }
+                    if (prow) prow[i] = g;
+                }
             }
-            if (probs && t < n_tokens && i < M) probs[static_cast<size_t>(t) * M + i] = gv[q] < 0.f ? 0.f : gv[q];
         }
-        wave_sync();  // every lane is done with the local logits
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = lane + 64 * q;
-            if (i < Mpad) gl[i] = i < M ? gv[q] : -1.f;
-        }
-        wave_sync();
-
-        // top-k by rank: a larger g, or an equal g at a lower index, ranks first
+        for (int j = 0; j + 1 < KP; ++j)
+            if (j < KT && (sk[j] >> 8) == (sk[j + 1] >> 8)) exact_pass = true;
+        if (!exact_pass) {
+            float gs[KP];
+            float denom = 0.f;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = lane + 64 * q;
-            if (gv[q] >= 0.f) {
-                const float g = gv[q];
-                int r = 0;
-                for (int j = 0; j < Mpad; j += 4) {
-                    const f32x4 o = *reinterpret_cast<const f32x4*>(gl + j);
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) r += (o[u] > g || (o[u] == g && j + u < i)) ? 1 : 0;
-                }
-                if (r < KT) {
-                    sel_g[wave][r] = g;
-                    sel_i[wave][r] = i;
+            for (int j = 0; j < KP; ++j) {
+                if (j < KT) {
+                    const int i = 255 - static_cast<int>(sk[j] & 0xffu);
+                    gs[j] = fused(i / Mk, lg[i * TT + tl]);
+                    denom += gs[j];
+                    oi[j] = i;
                 }
             }
+#pragma unroll
+            for (int j = 0; j < KP; ++j)
+                if (j < KT) ow[j] = renormalize ? gs[j] / denom : gs[j];
+            return;
         }
-        wave_sync();
+    }
 
-        // slot j of the output (lane j); renormalised by the sum in slot order
-        float denom = 1.f;
-        if (renormalize) {
-            float sum = 0.f;
-            for (int j = 0; j < KT; ++j) sum += sel_g[wave][j];
-            denom = sum;
+    // Exact top-k: (g, i) pairs kept sorted in expert order (ties to the lower index).
+    float sv[KP];
+    int si[KP];
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+        sv[j] = -1.f;  // below every probability
+        si[j] = 0;
+    }
+    const bool write_probs = prow && KT >= KP;  // the fast pass has written them otherwise
+    for (int kk = 0; kk < K; ++kk) {
+        const int i0 = kk * Mk;
+        const bool active = gst[kk * TT + tl] != -INFINITY;
+        for (int i = i0; i < i0 + Mk; ++i) {
+            const float v = lg[i * TT + tl];
+            float g = 0.f;
+            if (active && v != -INFINITY) {
+                g = fused(kk, v);
+                topk_insert<KP>(sv, si, g, i);
+            }
+            if (write_probs) prow[i] = g;
         }
-        if (t < n_tokens && lane < KT) {
-            topk_idx[static_cast<size_t>(t) * KT + lane] = sel_i[wave][lane];
-            topk_w[static_cast<size_t>(t) * KT + lane] = renormalize ? sel_g[wave][lane] / denom : sel_g[wave][lane];
+    }
+    float denom = 0.f;
+#pragma unroll
+    for (int j = 0; j < KP; ++j)
+        if (j < KT) denom += sv[j];
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+        if (j < KT) {
+            oi[j] = si[j];
+            ow[j] = renormalize ? sv[j] / denom : sv[j];
         }
-        wave_sync();  // the next token rewrites this wave's rows
     }
 }
 
-template <typename T, int NRB, int WAVES>
-hipError_t launch_waves(const GateArgs& a, hipStream_t s) {
-    const size_t lds = static_cast<size_t>(WAVES) * NRB * 16 * kTok * sizeof(float);
+template <typename T, int NRB, int NB, int WAVES, int KP>
+hipError_t launch_cfg(const GateArgs& a, hipStream_t s) {
+    constexpr int TT = kBlock * NB;
+    const size_t lds = static_cast<size_t>(WAVES) * NRB * 16 * TT * sizeof(float);
     static bool attr_set = false;  // once per instantiation: allow the partials beside the static arrays
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gate_kernel<T, NRB, WAVES>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gate_kernel<T, NRB, NB, WAVES, KP>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    const int grid = (a.n_tokens + kTok - 1) / kTok;
+    const int grid = (a.n_tokens + TT - 1) / TT;
     ProfileScope prof("gate", s);
-    hipLaunchKernelGGL((gate_kernel<T, NRB, WAVES>), dim3(grid), dim3(64 * WAVES), lds, s, a);
+    hipLaunchKernelGGL((gate_kernel<T, NRB, NB, WAVES, KP>), dim3(grid), dim3(64 * WAVES), lds, s, a);
     return hipGetLastError();
 }
 
-// 8 waves split d when their partial logits fit in 64 KB of LDS and d splits evenly, else
-// 4; with fewer token blocks than CUs (small batches) 16 waves shorten each wave's walk
-// over d.
+// KP > k lets the fast top-k see the (k+1)-th key; k = 16 runs the exact pass only
+template <typename T, int NRB, int NB, int WAVES>
+hipError_t launch_kp(const GateArgs& a, hipStream_t s) {
+    if (a.top_k <= 1) return launch_cfg<T, NRB, NB, WAVES, 2>(a, s);
+    if (a.top_k <= 3) return launch_cfg<T, NRB, NB, WAVES, 4>(a, s);
+    if (a.top_k <= 7) return launch_cfg<T, NRB, NB, WAVES, 8>(a, s);
+    return launch_cfg<T, NRB, NB, WAVES, 16>(a, s);
+}
+
+// Tile and wave split:
+//   * fewer 16-token tiles than CUs (small batches): 16 waves shorten each wave's walk
+//     over d (gates of at most 96 rows, whose partials fit the LDS);
+//   * gates of 48..128 rows with at least two tiles per CU: 32-token tiles, 8 waves
+//     (the gate weights are then read once per 32 tokens instead of per 16);
+//   * otherwise 16-token tiles with 8 waves when d splits evenly, else 4.
 template <typename T, int NRB>
 hipError_t launch_nrb(const GateArgs& a, hipStream_t s) {
     constexpr int SLICE = 4 * Elem<T>::kPerChunk;
-    const int blocks = (a.n_tokens + kTok - 1) / kTok;
+    const int tiles16 = (a.n_tokens + kBlock - 1) / kBlock;
     if constexpr (NRB <= 6)
-        if (blocks < 256 && a.d % (16 * SLICE) == 0) return launch_waves<T, NRB, 16>(a, s);
-    if (NRB <= 8 && a.d % (8 * SLICE) == 0) return launch_waves<T, NRB, 8>(a, s);
-    return launch_waves<T, NRB, 4>(a, s);
+        if (tiles16 < 256 && a.d % (16 * SLICE) == 0) return launch_kp<T, NRB, 1, 16>(a, s);
+    if constexpr (NRB >= 3 && NRB <= 8)
+        if (tiles16 >= 512 && a.d % (8 * SLICE) == 0) return launch_kp<T, NRB, 2, 8>(a, s);
+    if constexpr (NRB <= 8)
+        if (a.d % (8 * SLICE) == 0) return launch_kp<T, NRB, 1, 8>(a, s);
+    return launch_kp<T, NRB, 1, 4>(a, s);
 }
 
 template <typename T>
