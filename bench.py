@@ -185,7 +185,7 @@ def main():
     # per-kernel algorithmic work at the realised routing
     base = {"perm_small": "permute", "perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
             "transpose": "encode", "codec_xv": "encode", "codec_utp": "encode",
-            "codec_z_bf16": "decode", "codec_vzt": "decode", "codec_uw": "decode"}
+            "codec_z_bf16": "decode", "codec_prep": "decode", "codec_vzt": "decode", "codec_uw": "decode"}
 
     def stage_of(name):
         # a split-K "<kernel>_tail" / "<kernel>_reduce" launch belongs to its kernel's stage

@@ -143,18 +143,29 @@ ec2moe_status check_codec_desc(const ec2moe_codec_desc* d) {
 
 struct CodecWs {
     size_t gpart;  // split-K tail scratch of the matrix-core GEMMs (shared by encode and decode)
+    int batch;     // slices handled by one set of launches
     // encode: V^T, P = X V (float32), per-chunk partial sums of U^T P
     size_t vt, p, epart, enc_total;
     int tc;  // tokens per chunk of the U^T P contraction
-    // decode: Z rounded to the layer dtype (bf16 only), W = V_hat Z^T
-    size_t zb, wt, dec_total;
+    // decode: Z rounded to the layer dtype (bf16 only), W = V_hat Z^T per slice, and the segment
+    // offsets and row maps of the grouped products over a batch of slices
+    size_t zb, wt, seg_w, rows_w, seg_h, rows_h, dec_total;
 };
 
-// Token chunk of the U^T P contraction: about one workgroup per CU over (chunk, 64-column
-// block) pairs, in multiples of 4 tokens.
-int utp_chunk(int h, int r_w) {
+// Slices coded by one set of launches: at most 16, and few enough that a batch of X stays
+// below 4 GiB (32-bit byte offsets in the GEMM's buffer descriptors).
+constexpr int kMaxCodecBatch = 16;
+int codec_batch(const ec2moe_codec_desc* d) {
+    const int64_t slice = std::max<int64_t>(1, static_cast<int64_t>(d->h) * d->w * elem_bytes(static_cast<DType>(d->dtype)));
+    const int64_t fit = ((int64_t(1) << 32) - 1) / slice;
+    return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({fit, kMaxCodecBatch, std::max(1, d->n_slices)})));
+}
+
+// Token chunk of the U^T P contraction: about one workgroup per CU over (slice, chunk,
+// 64-column block) triples, in multiples of 4 tokens.
+int utp_chunk(int h, int r_w, int slices) {
     const int col_blocks = (r_w + 63) / 64;
-    const int target = std::max(1, 256 / col_blocks);
+    const int target = std::max(1, 256 / (col_blocks * slices));
     const int tc = (std::max(1, h) + target - 1) / target;
     return (tc + 3) & ~3;
 }
@@ -162,18 +173,24 @@ int utp_chunk(int h, int r_w) {
 CodecWs codec_ws(const ec2moe_codec_desc* d) {
     const size_t eb = elem_bytes(static_cast<DType>(d->dtype));
     CodecWs w{};
-    w.tc = utp_chunk(d->h, d->r_w);
+    w.batch = codec_batch(d);
+    const size_t nb = static_cast<size_t>(w.batch);
+    w.tc = utp_chunk(d->h, d->r_w, w.batch);
     const size_t chunks = (static_cast<size_t>(std::max(1, d->h)) + w.tc - 1) / w.tc;
     size_t o = 0;
     w.gpart = o; o += up(gemm_split_scratch_bytes());
     const size_t shared = o;
     w.vt = o; o += up(static_cast<size_t>(d->r_w) * d->w * eb);
-    w.p = o; o += up(static_cast<size_t>(d->h) * d->r_w * 4);
-    w.epart = o; o += up(chunks * d->r_h * d->r_w * 4);
+    w.p = o; o += up(nb * d->h * d->r_w * 4);
+    w.epart = o; o += up(nb * chunks * d->r_h * d->r_w * 4);
     w.enc_total = o;
     o = shared;
-    w.zb = o; o += up(static_cast<size_t>(d->r_h) * d->r_w * eb);
-    w.wt = o; o += up(static_cast<size_t>(d->w) * d->r_h * eb);
+    w.zb = o; o += up(nb * d->r_h * d->r_w * eb);
+    w.wt = o; o += up(nb * d->w * d->r_h * eb);
+    w.seg_w = o; o += up((nb + 1) * 4);
+    w.rows_w = o; o += up(nb * d->w * 4);
+    w.seg_h = o; o += up((nb + 1) * 4);
+    w.rows_h = o; o += up(nb * std::max(1, d->h) * 4);
     w.dec_total = o;
     return w;
 }
@@ -418,20 +435,23 @@ ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x
     void* vt = at<void>(ws, w.vt);
     float* p = at<float>(ws, w.p);
     hipError_t e = launch_transpose(dt, v, desc->w, desc->r_w, vt, stream);
-    for (int c = 0; c < desc->n_slices && e == hipSuccess; ++c) {
-        const char* xc = static_cast<const char*>(x) + static_cast<size_t>(c) * desc->h * desc->w * eb;
-        // P = X V  [h][r_w], float32
+    const size_t slice_bytes = static_cast<size_t>(desc->h) * desc->w * eb;
+    for (int c0 = 0; c0 < desc->n_slices && e == hipSuccess; c0 += w.batch) {
+        const int nc = std::min(w.batch, desc->n_slices - c0);
+        // P = X V  [nc * h][r_w], float32: V is shared, so the slices stack into one product
         GemmArgs g{};
-        g.tok = xc; g.row_index = nullptr; g.w = vt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
-        g.rows = desc->h; g.K = desc->w; g.N = desc->r_w; g.out = p; g.ldo = desc->r_w; g.name = "codec_xv";
-        g.src_rows = desc->h; g.w_rows = desc->r_w; g.part = at<float>(ws, w.gpart); g.max_split = kMaxSplit;
+        g.tok = static_cast<const char*>(x) + c0 * slice_bytes; g.row_index = nullptr; g.w = vt;
+        g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
+        g.rows = int64_t(nc) * desc->h; g.K = desc->w; g.N = desc->r_w; g.out = p; g.ldo = desc->r_w;
+        g.name = "codec_xv";
+        g.src_rows = g.rows; g.w_rows = desc->r_w; g.part = at<float>(ws, w.gpart); g.max_split = kMaxSplit;
         e = launch_gemm(dt, Epilogue::Store, OutType::F32, g, stream);
         if (e != hipSuccess) break;
-        // Z = U^T P  [r_h][r_w], float32 over token chunks, reduced in chunk order
-        UtpArgs s{};
-        s.u = u; s.p = p; s.T = desc->h; s.rh = desc->r_h; s.rw = desc->r_w; s.tc = w.tc;
-        s.part = at<float>(ws, w.epart); s.z = z + static_cast<size_t>(c) * desc->r_h * desc->r_w;
-        e = launch_utp(dt, s, stream);
+        // Z[s] = U^T P[s]  [r_h][r_w] per slice, float32 over token chunks, reduced in chunk order
+        UtpArgs a{};
+        a.u = u; a.p = p; a.T = desc->h; a.rh = desc->r_h; a.rw = desc->r_w; a.tc = w.tc; a.slices = nc;
+        a.part = at<float>(ws, w.epart); a.z = z + static_cast<size_t>(c0) * desc->r_h * desc->r_w;
+        e = launch_utp(dt, a, stream);
     }
     return hip_status(e, "lowrank_encode launch");
 }
@@ -449,28 +469,59 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
     const size_t eb = elem_bytes(dt);
     void* wt = at<void>(ws, w.wt);
     hipError_t e = hipSuccess;
-    for (int c = 0; c < desc->n_slices && e == hipSuccess; ++c) {
+    const int64_t zn = static_cast<int64_t>(desc->r_h) * desc->r_w;
+    if (desc->n_slices == 1) {
         // Wt = V_hat Z^T  [w][r_h]: both operands are K-contiguous rows (V_hat [w][r_w], Z [r_h][r_w]).
         // In bf16 layers Z is rounded to bf16 first (the product runs on the bf16 matrix cores;
         // Wt itself is rounded to bf16 anyway).
-        const float* zc = z + static_cast<size_t>(c) * desc->r_h * desc->r_w;
-        const void* zop = zc;
+        const void* zop = z;
         if (dt == DType::BF16) {
-            e = launch_f32_to_bf16(zc, static_cast<int64_t>(desc->r_h) * desc->r_w, at<void>(ws, w.zb), stream);
-            if (e != hipSuccess) break;
+            e = launch_f32_to_bf16(z, zn, at<void>(ws, w.zb), stream);
             zop = at<void>(ws, w.zb);
         }
+        if (e == hipSuccess) {
+            GemmArgs gw{};
+            gw.tok = v_hat; gw.row_index = nullptr; gw.w = zop; gw.w_group_stride = 0; gw.seg = nullptr;
+            gw.n_groups = 1; gw.rows = desc->w; gw.K = desc->r_w; gw.N = desc->r_h; gw.out = wt; gw.ldo = desc->r_h;
+            gw.name = "codec_vzt";
+            gw.src_rows = desc->w; gw.w_rows = desc->r_h; gw.part = at<float>(ws, w.gpart); gw.max_split = kMaxSplit;
+            e = launch_gemm(dt, Epilogue::Store, OutType::Same, gw, stream);
+        }
+        if (e == hipSuccess) {
+            // X_hat = U_hat Wt^T  [h][w]
+            GemmArgs g{};
+            g.tok = u_hat; g.row_index = nullptr; g.w = wt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
+            g.rows = desc->h; g.K = desc->r_h; g.N = desc->w; g.out = x_hat; g.ldo = desc->w; g.name = "codec_uw";
+            g.src_rows = desc->h; g.w_rows = desc->w; g.part = at<float>(ws, w.gpart); g.max_split = kMaxSplit;
+            e = launch_gemm(dt, Epilogue::Store, OutType::Same, g, stream);
+        }
+        return hip_status(e, "lowrank_decode launch");
+    }
+    // Several slices: the same two products as grouped GEMMs with one group per slice of a
+    // batch (the token-side operand V_hat or U_hat gathered through a row map p -> p mod rows).
+    int32_t* seg_w = at<int32_t>(ws, w.seg_w);
+    int32_t* rows_w = at<int32_t>(ws, w.rows_w);
+    int32_t* seg_h = at<int32_t>(ws, w.seg_h);
+    int32_t* rows_h = at<int32_t>(ws, w.rows_h);
+    for (int c0 = 0; c0 < desc->n_slices && e == hipSuccess; c0 += w.batch) {
+        const int nc = std::min(w.batch, desc->n_slices - c0);
+        const float* zc = z + static_cast<size_t>(c0) * zn;
+        void* zb = dt == DType::BF16 ? at<void>(ws, w.zb) : nullptr;
+        e = launch_codec_prep(zc, nc * zn, zb, nc, desc->w, desc->h, seg_w, rows_w, seg_h, rows_h, stream);
+        if (e != hipSuccess) break;
+        // Wt[s] = V_hat Z[s]^T  [w][r_h]
         GemmArgs gw{};
-        gw.tok = v_hat; gw.row_index = nullptr; gw.w = zop; gw.w_group_stride = 0; gw.seg = nullptr; gw.n_groups = 1;
-        gw.rows = desc->w; gw.K = desc->r_w; gw.N = desc->r_h; gw.out = wt; gw.ldo = desc->r_h; gw.name = "codec_vzt";
+        gw.tok = v_hat; gw.row_index = rows_w; gw.w = zb ? zb : static_cast<const void*>(zc); gw.w_group_stride = zn;
+        gw.seg = seg_w; gw.n_groups = nc; gw.rows = int64_t(nc) * desc->w; gw.K = desc->r_w; gw.N = desc->r_h;
+        gw.out = wt; gw.ldo = desc->r_h; gw.name = "codec_vzt";
         gw.src_rows = desc->w; gw.w_rows = desc->r_h; gw.part = at<float>(ws, w.gpart); gw.max_split = kMaxSplit;
         e = launch_gemm(dt, Epilogue::Store, OutType::Same, gw, stream);
         if (e != hipSuccess) break;
-        // X_hat = U_hat Wt^T  [h][w]
+        // X_hat[s] = U_hat Wt[s]^T  [h][w]
         GemmArgs g{};
-        g.tok = u_hat; g.row_index = nullptr; g.w = wt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
-        g.rows = desc->h; g.K = desc->r_h; g.N = desc->w;
-        g.out = static_cast<char*>(x_hat) + static_cast<size_t>(c) * desc->h * desc->w * eb; g.ldo = desc->w;
+        g.tok = u_hat; g.row_index = rows_h; g.w = wt; g.w_group_stride = int64_t(desc->w) * desc->r_h;
+        g.seg = seg_h; g.n_groups = nc; g.rows = int64_t(nc) * desc->h; g.K = desc->r_h; g.N = desc->w;
+        g.out = static_cast<char*>(x_hat) + static_cast<size_t>(c0) * desc->h * desc->w * eb; g.ldo = desc->w;
         g.name = "codec_uw";
         g.src_rows = desc->h; g.w_rows = desc->w; g.part = at<float>(ws, w.gpart); g.max_split = kMaxSplit;
         e = launch_gemm(dt, Epilogue::Store, OutType::Same, g, stream);

@@ -58,7 +58,8 @@ constexpr int kUtpUP = 272;  // LDS pitch of the staged U rows (floats; 272 % 64
 constexpr int kUtpPP = 80;   // LDS pitch of the staged P rows (80 % 64 = 16)
 
 // One token chunk of Z = U^T P: part[s][r][c] = sum over t in chunk s of U[t][r] P[t][c], for
-// the 64 columns c0.. of this workgroup and all r_h <= 256 rows, on the float32 matrix cores
+// the 64 columns c0.. of this workgroup and all r_h <= 256 rows (blockIdx.z: the slice, whose
+// P rows, partials and Z follow the previous slice's), on the float32 matrix cores
 // (v_mfma_f32_16x16x4f32: lane l feeds A[l % 16][l / 16] and B[l / 16][l % 16] and holds
 // D[4 (l / 16) + i][l % 16]). Each stage loads 64 token rows of U (converted to float32) and of
 // P with 16-byte loads into LDS; rows past the chunk are zero. Wave w owns rows w*64 .. w*64+63.
@@ -69,6 +70,7 @@ __global__ __launch_bounds__(256) void utp_kernel(UtpArgs g) {
     constexpr int EPC = 16 / static_cast<int>(sizeof(TU));
     const int c0 = blockIdx.x * kUtpC;
     const int tb = blockIdx.y * g.tc;
+    const float* pin_ = g.p + static_cast<int64_t>(blockIdx.z) * g.T * g.rw;
     const int te = min(g.T, tb + g.tc);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
@@ -107,7 +109,7 @@ __global__ __launch_bounds__(256) void utp_kernel(UtpArgs g) {
             const int i = threadIdx.x + 256 * j;
             const int r = i / 16, c = c0 + (i % 16) * 4;
             pq[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (r < nt && c < g.rw) pq[j] = *reinterpret_cast<const f32x4*>(g.p + static_cast<int64_t>(t0 + r) * g.rw + c);
+            if (r < nt && c < g.rw) pq[j] = *reinterpret_cast<const f32x4*>(pin_ + static_cast<int64_t>(t0 + r) * g.rw + c);
         }
 #pragma unroll
         for (int j = 0; j < UPT; ++j) {
@@ -149,7 +151,7 @@ __global__ __launch_bounds__(256) void utp_kernel(UtpArgs g) {
         }
         __syncthreads();
     }
-    float* part = g.part + static_cast<int64_t>(blockIdx.y) * g.rh * g.rw;
+    float* part = g.part + (static_cast<int64_t>(blockIdx.z) * gridDim.y + blockIdx.y) * g.rh * g.rw;
 #pragma unroll
     for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
@@ -175,6 +177,32 @@ __global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restric
     }
 }
 
+// Decoder set-up for n slices at once: Z rounded to bfloat16 (when zb is given), and the
+// segment offsets and row maps of the two grouped products (slice s owns rows s*w .. of
+// V_hat Z^T, gathered from row p - s*w of V_hat, and rows s*h .. of X_hat, from row p - s*h
+// of U_hat).
+__global__ __launch_bounds__(256) void codec_prep_kernel(const float* __restrict__ z, int64_t nz,
+                                                         bf16_t* __restrict__ zb, int n, int w, int h,
+                                                         int32_t* __restrict__ seg_w, int32_t* __restrict__ rows_w,
+                                                         int32_t* __restrict__ seg_h, int32_t* __restrict__ rows_h) {
+    const int64_t tid = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+    if (zb)
+        for (int64_t i = tid * 4; i < nz; i += stride * 4) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(z + i);
+            uint2 o;
+            o.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+            o.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+            *reinterpret_cast<uint2*>(zb + i) = o;
+        }
+    for (int64_t i = tid; i < static_cast<int64_t>(n) * w; i += stride) rows_w[i] = static_cast<int32_t>(i % w);
+    for (int64_t i = tid; i < static_cast<int64_t>(n) * h; i += stride) rows_h[i] = static_cast<int32_t>(i % h);
+    for (int64_t i = tid; i <= n; i += stride) {
+        seg_w[i] = static_cast<int32_t>(i * w);
+        seg_h[i] = static_cast<int32_t>(i * h);
+    }
+}
+
 template <typename TO>
 __device__ __forceinline__ void put4(TO* dst, f32x4 v) {
 #pragma unroll
@@ -183,11 +211,14 @@ __device__ __forceinline__ void put4(TO* dst, f32x4 v) {
 
 // out[i] = sum over p of part[p][i] (deterministic): four groups of threads each add a quarter
 // of the partials in order with up to 16 loads in flight, and the group sums are added in
-// group order. A workgroup owns 64 runs of four consecutive elements (mn a multiple of 4).
+// group order. A workgroup owns 64 runs of four consecutive elements (mn a multiple of 4);
+// blockIdx.y is the slice (its partials and outputs follow the previous slice's).
 template <typename TO>
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part, int64_t mn, int splits,
                                                            TO* __restrict__ out) {
     __shared__ f32x4 grp[4][64];
+    part += static_cast<int64_t>(blockIdx.y) * splits * mn;
+    out += static_cast<int64_t>(blockIdx.y) * mn;
     const int col = threadIdx.x & 63, g = threadIdx.x >> 6;
     const int per = (splits + 3) / 4;
     const int p0 = g * per, p1 = min(splits, p0 + per);
@@ -228,7 +259,7 @@ hipError_t launch_transpose(DType dt, const void* src, int rows, int cols, void*
 
 hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s) {
     const int chunks = (g.T + g.tc - 1) / g.tc;
-    dim3 grid((g.rw + kUtpC - 1) / kUtpC, chunks);
+    dim3 grid((g.rw + kUtpC - 1) / kUtpC, chunks, g.slices);
     {
         ProfileScope prof("codec_utp", s);
         if (udt == DType::BF16) hipLaunchKernelGGL(utp_kernel<bf16_t>, grid, dim3(256), 0, s, g);
@@ -239,7 +270,17 @@ hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s) {
     const int64_t mn = static_cast<int64_t>(g.rh) * g.rw;
     const int rgrid = static_cast<int>(std::min<int64_t>((mn + 255) / 256, 4096));
     ProfileScope prof("codec_utp_reduce", s);
-    hipLaunchKernelGGL(split_reduce_kernel<float>, dim3(rgrid), dim3(256), 0, s, g.part, mn, chunks, g.z);
+    hipLaunchKernelGGL(split_reduce_kernel<float>, dim3(rgrid, g.slices), dim3(256), 0, s, g.part, mn, chunks, g.z);
+    return hipGetLastError();
+}
+
+hipError_t launch_codec_prep(const float* z, int64_t nz, void* zb, int n, int w, int h, int32_t* seg_w,
+                             int32_t* rows_w, int32_t* seg_h, int32_t* rows_h, hipStream_t s) {
+    const int64_t work = std::max<int64_t>({nz / 4, static_cast<int64_t>(n) * std::max(w, h), n + 1});
+    const int grid = static_cast<int>(std::min<int64_t>((work + 255) / 256, 4096));
+    ProfileScope prof("codec_prep", s);
+    hipLaunchKernelGGL(codec_prep_kernel, dim3(grid), dim3(256), 0, s, z, nz, static_cast<bf16_t*>(zb), n, w, h,
+                       seg_w, rows_w, seg_h, rows_h);
     return hipGetLastError();
 }
 

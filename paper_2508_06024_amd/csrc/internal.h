@@ -93,18 +93,23 @@ hipError_t launch_combine(DType dt, const void* y_perm, const int32_t* inv_perm,
 // dst[c][r] = src[r][c] for a rows x cols matrix
 hipError_t launch_transpose(DType dt, const void* src, int rows, int cols, void* dst, hipStream_t s);
 
-// Z[r][c] = sum_t U[t][r] P[t][c] (r < rh, c < rw, t < T): float32 partial sums over token
-// chunks of tc rows go to part ([ceil(T / tc)][rh][rw] float32), then are added in chunk
-// order into z (deterministic). U has the layer dtype, P and Z are float32. rh <= 256;
-// rh and rw are multiples of 16; every row is 16-byte aligned.
+// Z[s][r][c] = sum_t U[t][r] P[s][t][c] (r < rh, c < rw, t < T, s < slices): float32
+// partial sums over token chunks of tc rows go to part ([slices][ceil(T / tc)][rh][rw]
+// float32), then are added in chunk order into z ([slices][rh][rw]; deterministic). U has
+// the layer dtype, P and Z are float32. rh <= 256; rh and rw are multiples of 16; every row
+// is 16-byte aligned.
 struct UtpArgs {
     const void* u;
     const float* p;
-    int T, rh, rw, tc;
+    int T, rh, rw, tc, slices;
     float* part;
     float* z;
 };
 hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s);
+// Decoder set-up of n slices: zb = bfloat16(z) (nz elements, a multiple of 4; skipped when zb is
+// null); seg_w[s] = s*w, rows_w[p] = p % w, seg_h[s] = s*h, rows_h[p] = p % h (s <= n).
+hipError_t launch_codec_prep(const float* z, int64_t nz, void* zb, int n, int w, int h, int32_t* seg_w,
+                             int32_t* rows_w, int32_t* seg_h, int32_t* rows_h, hipStream_t s);
 // dst = bfloat16(src) with round-to-nearest-even, n a multiple of 4
 hipError_t launch_f32_to_bf16(const float* src, int64_t n, void* dst, hipStream_t s);
 
