@@ -20,7 +20,12 @@ Sources (EC2MoE, arXiv 2508.06024):
 Readings where the paper is silent (each is also listed with the design notes):
   * the candidate filter acts before both softmaxes: non-candidates get no
     probability and a group without candidates drops out of the group softmax;
-  * experts are grouped contiguously: group k holds experts [k*M/K, (k+1)*M/K);
+  * experts are grouped contiguously: group k holds experts [k*M/K, (k+1)*M/K), or
+    groups of given sizes M_k in order (Eq. 5 allows unequal groups);
+  * group-focused evaluation (the closing remark of HL-GGN) as an option: per token only
+    the top-G groups by p_group keep their experts (ties to the lower group index), more
+    groups in the same order while the kept ones hold fewer than k candidates; p_group
+    stays the softmax over all groups with a candidate;
   * top-k orders by descending g, exact ties going to the lower expert index;
     the selected weights are renormalised to sum to 1 (Eq. (1)'s constraint
     applied to the sparse gate) unless renormalize=False;
@@ -52,12 +57,18 @@ def candidate_set(mask_words, n_experts):
     return [e for e in range(n_experts) if (int(mask_words[e // 64]) >> (e % 64)) & 1]
 
 
-def expert_groups(n_experts, n_groups):
-    """Contiguous equal groups: group k = experts [k*M/K, (k+1)*M/K)."""
-    if n_experts % n_groups:
-        raise ValueError("the number of groups must divide the number of experts")
-    size = n_experts // n_groups
-    return [list(range(k * size, (k + 1) * size)) for k in range(n_groups)]
+def expert_groups(n_experts, n_groups, group_sizes=None):
+    """Contiguous groups: equal, group k = experts [k*M/K, (k+1)*M/K), or of the given
+    sizes M_k (Eq. 5: M = sum_k M_k), group k starting after groups 0..k-1."""
+    if group_sizes is None:
+        if n_experts % n_groups:
+            raise ValueError("the number of groups must divide the number of experts")
+        group_sizes = [n_experts // n_groups] * n_groups
+    group_sizes = [int(m) for m in group_sizes]
+    if len(group_sizes) != n_groups or min(group_sizes) < 1 or sum(group_sizes) != n_experts:
+        raise ValueError("group sizes must be K positive counts summing to M")
+    starts = np.concatenate([[0], np.cumsum(group_sizes)])
+    return [list(range(int(starts[k]), int(starts[k + 1]))) for k in range(n_groups)]
 
 
 def softmax(v):
@@ -69,33 +80,69 @@ def softmax(v):
 
 # ----------------------------------------------------------------------------- Eq. (5)-(7)
 
-def group_gate_probs(x, w_global, b_global, w_local, b_local, mask_words, n_groups):
-    """Fused expert distribution g [T][M] of the lightweight group gate.
+def _token_gate(group_logits_t, local_logits_t, cand_in_group, active, top_groups, min_candidates):
+    """Eq. 5-7 for one token: (p_group over the active groups, {expert: g} of the kept groups).
 
-    Stage 1 (Eq. 6): p_group = Softmax(W_global x + b_global) over the groups that
-    hold at least one candidate. Stage 2 (Eq. 5): inside group k,
-    p_local^(k) = Softmax(W_k x + b_k) over the group's candidates. Fusion (Eq. 7):
-    g_i = p_group^(k) * p_local,i^(k). Non-candidates get g = 0.
-    """
+    top_groups = G > 0 (group-focused evaluation, HL-GGN): only the groups ranked first by
+    p_group (ties to the lower group index) keep their experts; groups are kept in that order
+    until G are kept and together they hold at least min_candidates candidates. p_group is
+    the softmax over all active groups either way."""
+    p_group = softmax(group_logits_t[active])
+    kept = list(active)
+    if top_groups and top_groups < len(active):
+        order = sorted(range(len(active)), key=lambda a: (-p_group[a], active[a]))
+        kept, held = [], 0
+        for a in order:
+            if len(kept) >= top_groups and held >= min_candidates:
+                break
+            kept.append(active[a])
+            held += len(cand_in_group[active[a]])
+    g = {}
+    for a, k in enumerate(active):
+        if k not in kept:
+            continue
+        members = cand_in_group[k]
+        p_local = softmax(local_logits_t[members])
+        for i, pl in zip(members, p_local):
+            g[i] = p_group[a] * pl
+    return g
+
+
+def _gate_all(x, w_global, b_global, w_local, b_local, mask_words, n_groups, group_sizes,
+              top_groups, min_candidates):
+    """(g [T][M], per token the sorted candidates of its kept groups)."""
     x = np.asarray(x, dtype=np.float64)
     T = x.shape[0]
     M = w_local.shape[0]
     local_logits = x @ np.asarray(w_local, np.float64).T + np.asarray(b_local, np.float64)
     group_logits = x @ np.asarray(w_global, np.float64).T + np.asarray(b_global, np.float64)
     cand = set(candidate_set(mask_words, M))
-    groups = expert_groups(M, n_groups)
+    groups = expert_groups(M, n_groups, group_sizes)
     cand_in_group = [[i for i in grp if i in cand] for grp in groups]
     active = [k for k in range(n_groups) if cand_in_group[k]]
 
     g = np.zeros((T, M), dtype=np.float64)
+    kept = []
     for t in range(T):
-        p_group = softmax(group_logits[t, active])
-        for a, k in enumerate(active):
-            members = cand_in_group[k]
-            p_local = softmax(local_logits[t, members])
-            for i, p in zip(members, p_local):
-                g[t, i] = p_group[a] * p
-    return g
+        gt = _token_gate(group_logits[t], local_logits[t], cand_in_group, active, top_groups, min_candidates)
+        for i, v in gt.items():
+            g[t, i] = v
+        kept.append(sorted(gt))
+    return g, kept
+
+
+def group_gate_probs(x, w_global, b_global, w_local, b_local, mask_words, n_groups,
+                     group_sizes=None, top_groups=0, min_candidates=1):
+    """Fused expert distribution g [T][M] of the lightweight group gate.
+
+    Stage 1 (Eq. 6): p_group = Softmax(W_global x + b_global) over the groups that
+    hold at least one candidate. Stage 2 (Eq. 5): inside group k,
+    p_local^(k) = Softmax(W_k x + b_k) over the group's candidates. Fusion (Eq. 7):
+    g_i = p_group^(k) * p_local,i^(k). Non-candidates get g = 0, and so do the experts of
+    groups left out by top_groups (see _token_gate).
+    """
+    return _gate_all(x, w_global, b_global, w_local, b_local, mask_words, n_groups, group_sizes,
+                     top_groups, min_candidates)[0]
 
 
 def topk_select(g_row, cand, k):
@@ -108,21 +155,23 @@ def topk_select(g_row, cand, k):
 
 
 def group_gate(x, w_global, b_global, w_local, b_local, mask_words, n_groups, top_k,
-               renormalize=True):
+               renormalize=True, group_sizes=None, top_groups=0):
     """Routing of every token: (idx int32 [T][k], w float64 [T][k], g float64 [T][M]).
 
-    w holds g of the selected experts, divided by their sum when renormalize is set.
+    w holds g of the selected experts, divided by their sum when renormalize is set. With
+    top_groups = G > 0 the top-k is taken among the candidates of the kept groups only.
     """
     M = w_local.shape[0]
     cand = candidate_set(mask_words, M)
     if len(cand) < top_k:
         raise TooFewCandidates(f"{len(cand)} candidates for top-{top_k}")
-    g = group_gate_probs(x, w_global, b_global, w_local, b_local, mask_words, n_groups)
+    g, kept = _gate_all(x, w_global, b_global, w_local, b_local, mask_words, n_groups, group_sizes,
+                        top_groups, top_k)
     T = g.shape[0]
     idx = np.zeros((T, top_k), dtype=np.int32)
     w = np.zeros((T, top_k), dtype=np.float64)
     for t in range(T):
-        sel = topk_select(g[t], cand, top_k)
+        sel = topk_select(g[t], kept[t], top_k)
         idx[t] = sel
         w[t] = g[t, sel]
         if renormalize:

@@ -223,6 +223,112 @@ def test_permutation_matches_brute_force(T, M, k, keep, skew):
             assert seg[e] == seg[e + 1]
 
 
+# ----------------------------------------------------------------------------- unequal groups, group pruning
+
+def test_unequal_groups_hand_example():
+    c = _load("gate_unequal_hand.json")
+    M, K, d = 4, 2, c["d"]
+    x = np.ones((1, d))
+    z = lambda *shape: np.zeros(shape)
+    for top_groups in (0, 1, 2):
+        idx, w, g = O.group_gate(x, z(K, d), z(K), z(M, d), z(M), [0b1111], K, c["top_k"],
+                                 group_sizes=c["group_sizes"], top_groups=top_groups)
+        np.testing.assert_allclose(g[0], [value(v) for v in c["g"]], rtol=1e-15)
+        assert idx[0].tolist() == c["idx"]
+        np.testing.assert_allclose(w[0], [value(v) for v in c["w"]], rtol=1e-15)
+
+
+def test_unequal_groups_reduce_to_known_cases():
+    rng = np.random.default_rng(40)
+    T, d, M, K = 9, 24, 12, 3
+    x, wg, bg, wl, bl = _rand_gate(rng, T, d, M, K)
+    mask, _ = _random_mask(rng, M, 10)
+    # equal sizes given explicitly: the default grouping
+    a = O.group_gate_probs(x, wg, bg, wl, bl, mask, K)
+    b = O.group_gate_probs(x, wg, bg, wl, bl, mask, K, group_sizes=[4, 4, 4])
+    np.testing.assert_array_equal(a, b)
+    # one group of all experts: scipy's softmax over the candidates
+    g1 = O.group_gate_probs(x, wg[:1], bg[:1], wl, bl, mask, 1, group_sizes=[M])
+    cand = O.candidate_set(mask, M)
+    ref = scipy.special.softmax(x @ wl[cand].T + bl[cand], axis=1)
+    np.testing.assert_allclose(g1[:, cand], ref, rtol=1e-12)
+    # sizes (5, 2, 5): each group's g sums to its p_group; in-group odds are exp(logit gaps)
+    sizes = [5, 2, 5]
+    g = O.group_gate_probs(x, wg, bg, wl, bl, W.mask_words(range(M), M), K, group_sizes=sizes)
+    pg = scipy.special.softmax(x @ wg.T + bg, axis=1)
+    starts = np.cumsum([0] + sizes)
+    for k in range(K):
+        np.testing.assert_allclose(g[:, starts[k]:starts[k + 1]].sum(1), pg[:, k], rtol=1e-12)
+    l = x @ wl.T + bl
+    np.testing.assert_allclose(g[:, 6] / g[:, 5], np.exp(l[:, 6] - l[:, 5]), rtol=1e-12)
+    with pytest.raises(ValueError):
+        O.group_gate_probs(x, wg, bg, wl, bl, mask, K, group_sizes=[5, 5, 5])
+
+
+def test_group_pruning_keeps_all_groups_when_g_covers_them():
+    rng = np.random.default_rng(41)
+    T, d, M, K, k = 20, 16, 16, 4, 3
+    x, wg, bg, wl, bl = _rand_gate(rng, T, d, M, K)
+    mask, _ = _random_mask(rng, M, 13)
+    dense = O.group_gate(x, wg, bg, wl, bl, mask, K, k)
+    for G in (K, K + 3):
+        pruned = O.group_gate(x, wg, bg, wl, bl, mask, K, k, top_groups=G)
+        for a, b in zip(dense, pruned):
+            np.testing.assert_array_equal(a, b)
+
+
+def test_top1_group_is_the_in_group_softmax():
+    """top_groups = 1 and a top group with at least k candidates: the selected experts come from
+    the group with the largest p_group, and their renormalised weights are the in-group
+    softmax's (p_group cancels)."""
+    rng = np.random.default_rng(42)
+    T, d, M, K, k = 30, 20, 24, 4, 2
+    x, wg, bg, wl, bl = _rand_gate(rng, T, d, M, K, scale=3.0)
+    mask = W.mask_words(range(M), M)
+    idx, w, g = O.group_gate(x, wg, bg, wl, bl, mask, K, k, top_groups=1)
+    top = np.argmax(x @ wg.T + bg, axis=1)
+    l = x @ wl.T + bl
+    for t in range(T):
+        members = np.arange(top[t] * 6, top[t] * 6 + 6)
+        assert set(idx[t].tolist()) <= set(members.tolist())
+        pl = scipy.special.softmax(l[t, members])
+        best = members[np.argsort(-pl, kind="stable")[:k]]
+        assert idx[t].tolist() == best.tolist()
+        np.testing.assert_allclose(w[t], pl[best - top[t] * 6] / pl[best - top[t] * 6].sum(), rtol=1e-12)
+        assert np.count_nonzero(g[t]) == 6
+        # p_group stays the softmax over all groups: the kept group's g sums to its p_group
+        np.testing.assert_allclose(g[t].sum(), scipy.special.softmax(x[t] @ wg.T + bg)[top[t]], rtol=1e-12)
+
+
+def test_group_pruning_extends_until_k_candidates():
+    """The kept groups are taken in p_group order until they hold k candidates; ties between
+    groups go to the lower group index."""
+    rng = np.random.default_rng(43)
+    T, d, M, K, k = 25, 12, 16, 8, 5
+    x, wg, bg, wl, bl = _rand_gate(rng, T, d, M, K)
+    wg[5] = wg[2]
+    bg[5] = bg[2]  # groups 2 and 5 always tie
+    keep = [0, 2, 3, 4, 5, 9, 10, 11, 12, 14]  # candidates per group of 2: 1 2 2 0 1 2 1 1
+    mask = W.mask_words(keep, M)
+    idx, w, g = O.group_gate(x, wg, bg, wl, bl, mask, K, k, top_groups=2)
+    gl = x @ wg.T + bg
+    cand_g = {kk: [i for i in keep if i // 2 == kk] for kk in range(K)}
+    active = [kk for kk in range(K) if cand_g[kk]]
+    for t in range(T):
+        order = sorted(active, key=lambda kk: (-gl[t, kk], kk))
+        kept, held = [], 0
+        for kk in order:
+            if len(kept) >= 2 and held >= k:
+                break
+            kept.append(kk)
+            held += len(cand_g[kk])
+        assert {int(i) // 2 for i in idx[t]} <= set(kept)
+        assert {int(i) // 2 for i in np.nonzero(g[t])[0]} == set(kept)
+        if 2 in kept and 5 in kept:
+            continue
+        assert not (5 in kept and 2 not in kept), "tie between groups 2 and 5 must keep group 2 first"
+
+
 # ----------------------------------------------------------------------------- experts, Eq. (1)
 
 def test_silu_pins():
