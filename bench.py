@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral", choices=ALL_ORDER)
     ap.add_argument("--rotate", type=int, default=4, help="distinct copies of X cycled through the steps")
+    ap.add_argument("--top-groups", type=int, default=0,
+                    help="group-focused gate: keep the top G groups per token (0: every group)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -56,7 +58,7 @@ def blas_threads():
         return 1
 
 
-def cpu_baseline(inp, cfg, target_s):
+def cpu_baseline(inp, cfg, target_s, top_groups=0):
     """The oracle's step (gate, encode, decode, experts, combine) on the first S tokens,
     with U restricted to those rows (one codec slice) or on the first S / h whole slices
     (several slices); weights are upcast to float64 before timing."""
@@ -74,7 +76,8 @@ def cpu_baseline(inp, cfg, target_s):
         t = time.perf_counter()
         uu = u[:S] if c == 1 else u
         O.layer(x[:S], inp.mask, wg, inp.b_global, wl, inp.b_local, gu, dn, uu, v, uu, v,
-                cfg.n_groups, cfg.top_k, activation=cfg.activation, codec_slices=max(1, S // h) if c > 1 else 1)
+                cfg.n_groups, cfg.top_k, activation=cfg.activation, codec_slices=max(1, S // h) if c > 1 else 1,
+                top_groups=top_groups)
         return time.perf_counter() - t
 
     T = cfg.n_tokens
@@ -130,7 +133,7 @@ def main():
     layer = Ec2moeLayer(xs[0], masks[0], up(inp.w_global), f32(inp.b_global), up(inp.w_local), f32(inp.b_local),
                         up(inp.w_gate_up), up(inp.w_down), up(inp.u), up(inp.v),
                         n_groups=cfg.n_groups, top_k=cfg.top_k, activation=cfg.activation,
-                        codec_slices=cfg.codec_slices)
+                        codec_slices=cfg.codec_slices, top_groups=args.top_groups)
 
     def step(i):
         layer.set_input(xs[i % len(xs)], masks[i % len(masks)])
@@ -236,7 +239,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
-        cpu = cpu_baseline(inp, cfg, args.cpu_seconds)
+        cpu = cpu_baseline(inp, cfg, args.cpu_seconds, args.top_groups)
         log(f"[bench] oracle: {cpu['value']:.4g} tokens/s on {cpu['cores']} threads")
 
     out = {
@@ -256,7 +259,8 @@ def main():
                                f"groups={cfg.n_groups} {'ReLU' if cfg.activation == 'relu' else 'SwiGLU'} "
                                f"H={cfg.ffn_hidden} top-{cfg.top_k} codec {cfg.r_h}x{cfg.r_w}"
                                + (f" on {cfg.codec_slices} slices of {cfg.codec_h} tokens" if cfg.codec_slices > 1
-                                  else "") + f", mask={cfg.mask}" + (f" keeping {cfg.n_keep}" if cfg.n_keep else ""),
+                                  else "") + f", mask={cfg.mask}" + (f" keeping {cfg.n_keep}" if cfg.n_keep else "")
+                               + (f", gate keeps the top {args.top_groups} groups" if args.top_groups else ""),
                    "tokens_per_step": cfg.n_tokens},
         "roofline": roof,
         "layer_roofline_frac": round(step_roof_ms / ms_step, 4),

@@ -102,6 +102,31 @@ ec2moe_status ec2moe_group_gate(const ec2moe_moe_desc* desc, const uint64_t* can
                                 int32_t* topk_idx, float* topk_w, float* probs,
                                 hipStream_t stream);
 
+/* Options of ec2moe_group_gate_ex. */
+typedef struct {
+    int32_t top_groups;         /* G > 0: group-focused evaluation (the closing remark of the
+                                   Lightweight Group Gate Network section): per token only the
+                                   groups ranked first by p_group (ties to the lower group
+                                   index) keep their experts; more groups are kept in that
+                                   order while the kept ones hold fewer than k candidates.
+                                   p_group stays the softmax over every group with a candidate;
+                                   left-out experts get g = 0. 0 (or G >= K): every group, Eq. 7. */
+    const int32_t* group_sizes; /* [host] K group sizes M_k >= 1 summing to M (Eq. 5: M = sum
+                                   of M_k), group k = the next M_k experts; NULL: K equal
+                                   groups (K must divide M). Read during the call only. */
+} ec2moe_gate_opts;
+
+/*
+ * ec2moe_group_gate with options (opts may be NULL: the same as ec2moe_group_gate).
+ * Unequal groups relax the rule that K divides M. The candidate set must still hold at
+ * least k experts. Logits of every group are computed either way (the gate reads X once;
+ * the pruning changes which experts may be selected, not the memory traffic).
+ */
+ec2moe_status ec2moe_group_gate_ex(const ec2moe_moe_desc* desc, const ec2moe_gate_opts* opts,
+                                   const uint64_t* cand_mask, const void* x, const void* w_global,
+                                   const float* b_global, const void* w_local, const float* b_local,
+                                   int32_t* topk_idx, float* topk_w, float* probs, hipStream_t stream);
+
 /* Workspace bytes needed by ec2moe_permute, ec2moe_expert_ffn and ec2moe_moe_forward
  * for this descriptor (a superset for all three). */
 ec2moe_status ec2moe_moe_workspace_size(const ec2moe_moe_desc* desc, size_t* bytes /*[host]*/);

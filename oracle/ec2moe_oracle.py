@@ -272,12 +272,12 @@ def lowrank_decode(z, u_hat, v_hat):
 
 def layer(x, mask_words, w_global, b_global, w_local, b_local, w_gate_up, w_down,
           u, v, u_hat, v_hat, n_groups, top_k, renormalize=True, activation="swiglu",
-          codec_slices=1):
+          codec_slices=1, top_groups=0):
     """Routing is taken on the end side from X; the experts run in the cloud on the
     reconstruction X_hat = decode(encode(X)), slice by slice. Returns a dict of every
     stage output (z is [r_h][r_w] for one slice, [c][r_h][r_w] for c > 1)."""
     idx, w, g = group_gate(x, w_global, b_global, w_local, b_local, mask_words,
-                           n_groups, top_k, renormalize)
+                           n_groups, top_k, renormalize, top_groups=top_groups)
     x = np.asarray(x, np.float64)
     h = x.shape[0] // codec_slices
     zs = [lowrank_encode(x[s * h:(s + 1) * h], u, v) for s in range(codec_slices)]

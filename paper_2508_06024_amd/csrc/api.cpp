@@ -56,15 +56,18 @@ constexpr int kMaxExperts = 256;
 constexpr int kMaxGateRows = 320;
 constexpr int kMaxTopK = 16;
 
-ec2moe_status check_moe_desc(const ec2moe_moe_desc* d) {
+// equal_groups: K must divide M (every entry point but ec2moe_group_gate_ex with group sizes)
+ec2moe_status check_moe_desc(const ec2moe_moe_desc* d, bool equal_groups = true) {
     REQUIRE(d != nullptr, EC2MOE_ERR_INVALID_ARGUMENT, "desc is NULL");
     REQUIRE(d->dtype == EC2MOE_F32 || d->dtype == EC2MOE_BF16, EC2MOE_ERR_INVALID_ARGUMENT, "unknown dtype %d",
             d->dtype);
     REQUIRE(d->n_tokens >= 0, EC2MOE_ERR_INVALID_ARGUMENT, "n_tokens %d < 0", d->n_tokens);
     REQUIRE(d->n_experts > 0 && d->n_groups > 0 && d->d_model > 0 && d->ffn_hidden > 0 && d->top_k > 0,
             EC2MOE_ERR_INVALID_ARGUMENT, "n_experts, n_groups, d_model, ffn_hidden and top_k must be positive");
-    REQUIRE(d->n_experts % d->n_groups == 0, EC2MOE_ERR_INVALID_ARGUMENT,
+    REQUIRE(!equal_groups || d->n_experts % d->n_groups == 0, EC2MOE_ERR_INVALID_ARGUMENT,
             "n_groups %d does not divide n_experts %d", d->n_groups, d->n_experts);
+    REQUIRE(d->n_groups <= d->n_experts, EC2MOE_ERR_INVALID_ARGUMENT, "n_groups %d > n_experts %d", d->n_groups,
+            d->n_experts);
     REQUIRE(d->top_k <= d->n_experts, EC2MOE_ERR_INVALID_ARGUMENT, "top_k %d > n_experts %d", d->top_k,
             d->n_experts);
     REQUIRE((d->flags & ~(EC2MOE_GATE_RENORMALIZE | EC2MOE_EXPERT_RELU)) == 0, EC2MOE_ERR_INVALID_ARGUMENT,
@@ -272,13 +275,27 @@ const char* ec2moe_status_string(ec2moe_status s) {
 
 const char* ec2moe_last_error(void) { return g_last_error.c_str(); }
 
-ec2moe_status ec2moe_group_gate(const ec2moe_moe_desc* desc, const uint64_t* cand_mask, const void* x,
-                                const void* w_global, const float* b_global, const void* w_local,
-                                const float* b_local, int32_t* topk_idx, float* topk_w, float* probs,
-                                hipStream_t stream) {
-    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+ec2moe_status ec2moe_group_gate_ex(const ec2moe_moe_desc* desc, const ec2moe_gate_opts* opts,
+                                   const uint64_t* cand_mask, const void* x, const void* w_global,
+                                   const float* b_global, const void* w_local, const float* b_local,
+                                   int32_t* topk_idx, float* topk_w, float* probs, hipStream_t stream) {
+    const bool sized = opts && opts->group_sizes;
+    if (ec2moe_status st = check_moe_desc(desc, !sized); st != EC2MOE_OK) return st;
     REQUIRE_PTR(cand_mask);
-    const int M = desc->n_experts;
+    const int M = desc->n_experts, K = desc->n_groups;
+    const int top_groups = opts ? opts->top_groups : 0;
+    REQUIRE(top_groups >= 0, EC2MOE_ERR_INVALID_ARGUMENT, "top_groups %d < 0", top_groups);
+    GateArgs a{};
+    a.top_groups = top_groups;
+    a.equal_groups = sized ? 0 : 1;
+    a.goff[0] = 0;
+    for (int k = 0; k < K; ++k) {
+        const int mk = sized ? opts->group_sizes[k] : M / K;
+        REQUIRE(mk >= 1, EC2MOE_ERR_INVALID_ARGUMENT, "group %d has %d experts", k, mk);
+        a.goff[k + 1] = a.goff[k] + mk;
+        REQUIRE(a.goff[k + 1] <= M, EC2MOE_ERR_INVALID_ARGUMENT, "group sizes exceed n_experts %d", M);
+    }
+    REQUIRE(a.goff[K] == M, EC2MOE_ERR_INVALID_ARGUMENT, "group sizes sum to %d, not n_experts %d", a.goff[K], M);
     const int words = (M + 63) / 64;
     int pop = 0;
     for (int i = 0; i < words; ++i) {
@@ -293,13 +310,20 @@ ec2moe_status ec2moe_group_gate(const ec2moe_moe_desc* desc, const uint64_t* can
     if (desc->n_tokens == 0) return ok();
     REQUIRE_PTR(x); REQUIRE_PTR(w_global); REQUIRE_PTR(w_local); REQUIRE_PTR(topk_idx); REQUIRE_PTR(topk_w);
     REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(w_global); REQUIRE_ALIGNED(w_local);
-    GateArgs a{};
     a.x = x; a.w_global = w_global; a.b_global = b_global; a.w_local = w_local; a.b_local = b_local;
     a.topk_idx = topk_idx; a.topk_w = topk_w; a.probs = probs;
-    a.n_tokens = desc->n_tokens; a.d = desc->d_model; a.n_experts = M; a.n_groups = desc->n_groups;
+    a.n_tokens = desc->n_tokens; a.d = desc->d_model; a.n_experts = M; a.n_groups = K;
     a.top_k = desc->top_k; a.renormalize = (desc->flags & EC2MOE_GATE_RENORMALIZE) != 0;
     for (int i = 0; i < 4; ++i) a.mask[i] = i < words ? cand_mask[i] : 0;
     return hip_status(launch_gate(static_cast<DType>(desc->dtype), a, stream), "gate launch");
+}
+
+ec2moe_status ec2moe_group_gate(const ec2moe_moe_desc* desc, const uint64_t* cand_mask, const void* x,
+                                const void* w_global, const float* b_global, const void* w_local,
+                                const float* b_local, int32_t* topk_idx, float* topk_w, float* probs,
+                                hipStream_t stream) {
+    return ec2moe_group_gate_ex(desc, nullptr, cand_mask, x, w_global, b_global, w_local, b_local, topk_idx,
+                                topk_w, probs, stream);
 }
 
 ec2moe_status ec2moe_moe_workspace_size(const ec2moe_moe_desc* desc, size_t* bytes) {

@@ -72,6 +72,9 @@ __device__ __forceinline__ float seg_sum(float v, int width) {
 // probabilities are kept in LDS (wave 1's partials, free after phase 2) for the outputs.
 //   stage 2: group max and sum of e^(l - max), lane-local then across the group's lanes;
 //   stage 1: softmax over the groups that hold a candidate, across the 8 lanes;
+//   with top_groups, each lane ranks its group among the groups' logits and leaves it out
+//   unless fewer than top_groups groups, or groups holding fewer than k candidates, rank
+//   before it;
 //   fusion (Eq. 7) and top-k: every lane keeps its experts' keys (g truncated to its
 //   top 24 bits, then 255 - i) sorted, then three bitonic merges across the lanes leave
 //   the token's first KP keys in every lane. Distinct truncated values order as the
@@ -80,7 +83,7 @@ __device__ __forceinline__ float seg_sum(float v, int width) {
 template <int KP>
 __device__ __forceinline__ void route_octet(float* part, int n_el, int TT, int tl, int s, int t0, int n_tokens,
                                             int M, int Mk, int KT, bool renormalize, float* probs,
-                                            int32_t* topk_idx, float* topk_w) {
+                                            int32_t* topk_idx, float* topk_w, int top_groups, const short* gcand) {
     const int EPL = M >> 3;
     const int LG = Mk / EPL;
     const int t = t0 + tl;
@@ -113,6 +116,23 @@ __device__ __forceinline__ void route_octet(float* part, int n_el, int TT, int t
     const float gsum = seg_sum(leader && active ? fast_exp(G - gmax) : 0.f, 8);
     const float pg = fast_exp(G - gmax) * __builtin_amdgcn_rcpf(gsum);
     const float rs = __builtin_amdgcn_rcpf(sum);
+    // Group-focused evaluation: this lane's group is kept if fewer than top_groups active groups
+    // rank before it (larger logit, or equal at a lower index) or those hold fewer than k
+    // candidates. Every group's logit comes from its first lane.
+    bool kept = active;
+    if (top_groups > 0) {
+        const int K = M / Mk;
+        int rank = 0, before = 0;
+        for (int kk = 0; kk < K; ++kk) {
+            const float Gk = __shfl(G, (kk * Mk / EPL) & 7, 8);
+            const bool ak = gcand[kk] > 0;
+            if (ak && (Gk > G || (Gk == G && kk < grp))) {
+                ++rank;
+                before += gcand[kk];
+            }
+        }
+        kept = active && (rank < top_groups || before < KT);
+    }
 
     uint32_t sk[KP];
 #pragma unroll
@@ -123,7 +143,7 @@ __device__ __forceinline__ void route_octet(float* part, int n_el, int TT, int t
         if (j < EPL) {
             const int i = i0 + j;
             float g = -1.f;
-            if (v[j] != -INFINITY) {
+            if (kept && v[j] != -INFINITY) {
                 g = pg * (fast_exp(v[j] - m) * rs);
                 const uint32_t key = ((__float_as_uint(g) << 2) & 0xffffff00u) | static_cast<uint32_t>(255 - i);
 #pragma unroll
@@ -216,6 +236,8 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     __shared__ float s_bl[kMaxExperts];            // b_local (0 if absent)
     __shared__ float s_bg[kMaxGroups];             // b_global (0 if absent)
     __shared__ unsigned char s_cand[kMaxExperts];  // candidate flags of the mask
+    __shared__ unsigned char s_grp[kMaxExperts];   // group of each expert
+    __shared__ short s_gcand[kMaxGroups];          // candidates per group
 
     constexpr int EPC = Elem<T>::kPerChunk;
     constexpr int SLICE = 4 * EPC;  // k covered by one matrix-core step
@@ -237,7 +259,15 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
         s_bl[i] = p.b_local ? p.b_local[i] : 0.f;
         s_cand[i] = (p.mask[i >> 6] >> (i & 63)) & 1ull ? 1 : 0;
     }
-    for (int kk = threadIdx.x; kk < K; kk += THREADS) s_bg[kk] = p.b_global ? p.b_global[kk] : 0.f;
+    for (int kk = threadIdx.x; kk < K; kk += THREADS) {
+        s_bg[kk] = p.b_global ? p.b_global[kk] : 0.f;
+        int n = 0;
+        for (int i = p.goff[kk]; i < p.goff[kk + 1]; ++i) {
+            s_grp[i] = static_cast<unsigned char>(kk);
+            n += static_cast<int>((p.mask[i >> 6] >> (i & 63)) & 1ull);
+        }
+        s_gcand[kk] = static_cast<short>(n);
+    }
 
     // ---------------- phase 1: partial logits over this wave's share of d
     const T* xrow[NB];
@@ -319,14 +349,16 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     // group, whose lanes are a power of two): 8 lanes per token.
     const int EPL = M >> 3;
     const int LG = EPL > 0 ? Mk / EPL : 0;
-    if ((M & 7) == 0 && M <= 64 && Mk % EPL == 0 && (LG & (LG - 1)) == 0 && KT < KP) {
+    const int top_groups = pin(p.top_groups);
+    const bool prune = top_groups > 0 && top_groups < K;
+    if (p.equal_groups && (M & 7) == 0 && M <= 64 && Mk % EPL == 0 && (LG & (LG - 1)) == 0 && KT < KP) {
         if (wave * 8 >= TT) return;
         route_octet<KP>(part, N_EL, TT, wave * 8 + (lane >> 3), lane & 7, t0, n_tokens, M, Mk, KT, renormalize,
-                        probs, p.topk_idx, p.topk_w);
+                        probs, p.topk_idx, p.topk_w, prune ? top_groups : 0, s_gcand);
         return;
     }
 
-    // General shapes: one lane per token of the tile.
+    // General shapes (unequal groups and top-G groups included): one lane per token of the tile.
     if (wave != 0) return;
     const int tl = lane;
     const int t = t0 + tl;
@@ -339,13 +371,14 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     // expert order; stage 1 maximum over the groups that hold a candidate
     float gmax = -INFINITY;
     for (int kk = 0; kk < K; ++kk) {
-        const int i0 = kk * Mk;
+        const int i0 = p.goff[kk];
+        const int mk = p.goff[kk + 1] - i0;
         const float G = lg[(M + kk) * TT + tl];
         float m = -INFINITY, s = 0.f;
-        if (Mk <= kChunk) {
+        if (mk <= kChunk) {
             float v[kChunk];
 #pragma unroll
-            for (int u = 0; u < kChunk; ++u) v[u] = u < Mk ? lg[(i0 + u) * TT + tl] : -INFINITY;
+            for (int u = 0; u < kChunk; ++u) v[u] = u < mk ? lg[(i0 + u) * TT + tl] : -INFINITY;
 #pragma unroll
             for (int u = 0; u < kChunk; ++u) m = fmaxf(m, v[u]);
             if (m != -INFINITY) {
@@ -354,18 +387,18 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
                     if (v[u] != -INFINITY) s += fast_exp(v[u] - m);
             }
         } else {
-            for (int c = 0; c < Mk; c += kChunk) {
+            for (int c = 0; c < mk; c += kChunk) {
                 float v[kChunk];
 #pragma unroll
-                for (int u = 0; u < kChunk; ++u) v[u] = c + u < Mk ? lg[(i0 + c + u) * TT + tl] : -INFINITY;
+                for (int u = 0; u < kChunk; ++u) v[u] = c + u < mk ? lg[(i0 + c + u) * TT + tl] : -INFINITY;
 #pragma unroll
                 for (int u = 0; u < kChunk; ++u) m = fmaxf(m, v[u]);
             }
             if (m != -INFINITY)
-                for (int c = 0; c < Mk; c += kChunk) {
+                for (int c = 0; c < mk; c += kChunk) {
                     float v[kChunk];
 #pragma unroll
-                    for (int u = 0; u < kChunk; ++u) v[u] = c + u < Mk ? lg[(i0 + c + u) * TT + tl] : -INFINITY;
+                    for (int u = 0; u < kChunk; ++u) v[u] = c + u < mk ? lg[(i0 + c + u) * TT + tl] : -INFINITY;
 #pragma unroll
                     for (int u = 0; u < kChunk; ++u)
                         if (v[u] != -INFINITY) s += fast_exp(v[u] - m);
@@ -380,6 +413,34 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     for (int kk = 0; kk < K; ++kk)
         if (gst[kk * TT + tl] != -INFINITY) gsum += fast_exp(lg[(M + kk) * TT + tl] - gmax);
     const float rgsum = __builtin_amdgcn_rcpf(gsum);
+
+    // Group-focused evaluation: keep the groups with the largest group logits (the order of
+    // p_group; ties to the lower group index) until top_groups are kept and they hold at
+    // least k candidates; the others leave the fusion (their statistics row becomes -inf,
+    // after p_group has been formed over all of them).
+    if (prune) {
+        float* taken = part + 2 * N_EL;  // this lane's flags [kk][TT] (wave 2's partials, free after phase 2)
+        for (int kk = 0; kk < K; ++kk) taken[kk * TT + tl] = 0.f;
+        int kept = 0, held = 0;
+        for (int n = 0; n < K && (kept < top_groups || held < KT); ++n) {
+            float best = -INFINITY;
+            int bk = -1;
+            for (int kk = 0; kk < K; ++kk) {
+                if (gst[kk * TT + tl] == -INFINITY || taken[kk * TT + tl] != 0.f) continue;
+                const float G = lg[(M + kk) * TT + tl];
+                if (bk < 0 || G > best) {
+                    best = G;
+                    bk = kk;
+                }
+            }
+            if (bk < 0) break;
+            taken[bk * TT + tl] = 1.f;
+            ++kept;
+            held += s_gcand[bk];
+        }
+        for (int kk = 0; kk < K; ++kk)
+            if (taken[kk * TT + tl] == 0.f) gst[kk * TT + tl] = -INFINITY;
+    }
 
     // Fusion (Eq. 7) of expert i of group kk: g_i = p_group^(kk) * p_local,i^(kk). The same
     // expression everywhere below, so a recomputed g has the same bits.
@@ -401,14 +462,15 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
 #pragma unroll
         for (int j = 0; j < KP; ++j) sk[j] = 0;
         for (int kk = 0; kk < K; ++kk) {
-            const int i0 = kk * Mk;
-            for (int c = 0; c < Mk; c += kChunk) {
+            const int i0 = p.goff[kk];
+            const int mk = p.goff[kk + 1] - i0;
+            for (int c = 0; c < mk; c += kChunk) {
                 float v[kChunk];
 #pragma unroll
-                for (int u = 0; u < kChunk; ++u) v[u] = c + u < Mk ? lg[(i0 + c + u) * TT + tl] : -INFINITY;
-                if (gst[kk * TT + tl] == -INFINITY) {  // no candidate in this group
+                for (int u = 0; u < kChunk; ++u) v[u] = c + u < mk ? lg[(i0 + c + u) * TT + tl] : -INFINITY;
+                if (gst[kk * TT + tl] == -INFINITY) {  // no candidate in this group, or a group left out
                     if (prow)
-                        for (int u = 0; u < kChunk && c + u < Mk; ++u) prow[i0 + c + u] = 0.f;
+                        for (int u = 0; u < kChunk && c + u < mk; ++u) prow[i0 + c + u] = 0.f;
                     continue;
                 }
                 const float pg = fast_exp(lg[(M + kk) * TT + tl] - gmax) * rgsum;
@@ -416,7 +478,7 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
                 const float rs = __builtin_amdgcn_rcpf(gst[(K + kk) * TT + tl]);
 #pragma unroll
                 for (int u = 0; u < kChunk; ++u) {
-                    if (c + u >= Mk) break;
+                    if (c + u >= mk) break;
                     const int i = i0 + c + u;
                     float g = 0.f;
                     if (v[u] != -INFINITY) {
@@ -440,7 +502,7 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
             for (int j = 0; j < KP; ++j) {
                 if (j < KT) {
                     const int i = 255 - static_cast<int>(sk[j] & 0xffu);
-                    gs[j] = fused(i / Mk, lg[i * TT + tl]);
+                    gs[j] = fused(s_grp[i], lg[i * TT + tl]);
                     denom += gs[j];
                     oi[j] = i;
                 }
@@ -462,9 +524,9 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     }
     const bool write_probs = prow && KT >= KP;  // the fast pass has written them otherwise
     for (int kk = 0; kk < K; ++kk) {
-        const int i0 = kk * Mk;
+        const int i0 = p.goff[kk];
         const bool active = gst[kk * TT + tl] != -INFINITY;
-        for (int i = i0; i < i0 + Mk; ++i) {
+        for (int i = i0; i < p.goff[kk + 1]; ++i) {
             const float v = lg[i * TT + tl];
             float g = 0.f;
             if (active && v != -INFINITY) {

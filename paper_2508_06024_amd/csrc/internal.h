@@ -34,6 +34,9 @@ struct GateArgs {
     int n_tokens, d, n_experts, n_groups, top_k;
     bool renormalize;
     uint64_t mask[4];
+    int top_groups;    // > 0: keep the top_groups groups of largest p_group (more while < k candidates)
+    int equal_groups;  // goff[k] = k * M / K
+    int32_t goff[161]; // group k = experts goff[k] .. goff[k + 1] - 1 (K <= 160)
 };
 hipError_t launch_gate(DType dt, const GateArgs& a, hipStream_t s);
 

@@ -44,6 +44,10 @@ class CodecDesc(ctypes.Structure):
                 ("r_h", ctypes.c_int32), ("r_w", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
+class GateOpts(ctypes.Structure):
+    _fields_ = [("top_groups", ctypes.c_int32), ("group_sizes", ctypes.POINTER(ctypes.c_int32))]
+
+
 class KernelStat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int64), ("total_ms", ctypes.c_double)]
 
@@ -60,6 +64,8 @@ _lib = _load()
 _P = ctypes.c_void_p
 _SIGS = {
     "ec2moe_group_gate": [ctypes.POINTER(MoeDesc), ctypes.POINTER(ctypes.c_uint64), _P, _P, _P, _P, _P, _P, _P, _P, _P],
+    "ec2moe_group_gate_ex": [ctypes.POINTER(MoeDesc), ctypes.POINTER(GateOpts), ctypes.POINTER(ctypes.c_uint64),
+                             _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "ec2moe_moe_workspace_size": [ctypes.POINTER(MoeDesc), ctypes.POINTER(ctypes.c_size_t)],
     "ec2moe_permute": [ctypes.POINTER(MoeDesc), _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
     "ec2moe_expert_ffn": [ctypes.POINTER(MoeDesc), _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
@@ -143,8 +149,24 @@ def group_gate(desc: MoeDesc, mask_words, x, w_global, b_global, w_local, b_loca
                                   _ptr(topk_w), _ptr(probs), _stream()))
 
 
+def gate_opts(top_groups: int = 0, group_sizes: Optional[Sequence[int]] = None) -> GateOpts:
+    sizes = None if group_sizes is None else (ctypes.c_int32 * len(group_sizes))(*[int(m) for m in group_sizes])
+    opts = GateOpts(int(top_groups), ctypes.cast(sizes, ctypes.POINTER(ctypes.c_int32)) if sizes is not None else None)
+    opts._sizes = sizes  # keeps the array alive with the options
+    return opts
+
+
+def group_gate_ex(desc: MoeDesc, opts: Optional[GateOpts], mask_words, x, w_global, b_global, w_local, b_local,
+                  topk_idx, topk_w, probs=None):
+    """Raw call with options (top-G groups, unequal group sizes)."""
+    _check(_lib.ec2moe_group_gate_ex(ctypes.byref(desc), ctypes.byref(opts) if opts is not None else None,
+                                     mask_array(mask_words), _ptr(x), _ptr(w_global), _ptr(b_global),
+                                     _ptr(w_local), _ptr(b_local), _ptr(topk_idx), _ptr(topk_w), _ptr(probs),
+                                     _stream()))
+
+
 def gate(x, mask_words, w_global, b_global, w_local, b_local, n_groups, top_k, renormalize=True,
-         with_probs=False):
+         with_probs=False, top_groups=0, group_sizes=None):
     T, d = x.shape
     M = w_local.shape[0]
     dt = x.dtype
@@ -158,7 +180,11 @@ def gate(x, mask_words, w_global, b_global, w_local, b_local, n_groups, top_k, r
     idx = torch.empty((T, top_k), dtype=torch.int32, device=x.device)
     w = torch.empty((T, top_k), dtype=torch.float32, device=x.device)
     probs = torch.empty((T, M), dtype=torch.float32, device=x.device) if with_probs else None
-    group_gate(desc, mask_words, x, w_global, b_global, w_local, b_local, idx, w, probs)
+    if top_groups or group_sizes is not None:
+        group_gate_ex(desc, gate_opts(top_groups, group_sizes), mask_words, x, w_global, b_global, w_local,
+                      b_local, idx, w, probs)
+    else:
+        group_gate(desc, mask_words, x, w_global, b_global, w_local, b_local, idx, w, probs)
     return (idx, w, probs) if with_probs else (idx, w)
 
 

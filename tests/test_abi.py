@@ -84,6 +84,28 @@ def test_descriptor_flags():
         _desc(activation="gelu")
 
 
+def _gate_ex(desc, words, top_groups=0, sizes=None, ptr=1 << 20):
+    arr = E.mask_array(words)
+    p = ctypes.c_void_p(ptr)
+    opts = E.gate_opts(top_groups, sizes)
+    return E._lib.ec2moe_group_gate_ex(ctypes.byref(desc), ctypes.byref(opts), arr, p, p, None, p, None, p, p,
+                                       None, None)
+
+
+def test_gate_options_validation():
+    d0 = _desc(n_tokens=0, n_experts=12, n_groups=5)  # K does not divide M: fine with sizes
+    assert _gate_ex(d0, [0xFFF], sizes=[2, 3, 1, 4, 2]) == OK
+    assert _gate_ex(d0, [0xFFF], sizes=[2, 3, 1, 4, 3]) == INVALID and "exceed" in E.last_error()
+    assert _gate_ex(d0, [0xFFF], sizes=[2, 3, 1, 4, 1]) == INVALID and "sum" in E.last_error()
+    assert _gate_ex(d0, [0xFFF], sizes=[2, 3, 0, 5, 2]) == INVALID
+    assert _gate_ex(d0, [0xFFF]) == INVALID  # equal groups need K | M
+    d1 = _desc(n_tokens=0)
+    assert _gate_ex(d1, [0xFF], top_groups=-1) == INVALID
+    assert _gate_ex(d1, [0xFF], top_groups=1) == OK
+    assert E._lib.ec2moe_group_gate_ex(ctypes.byref(d1), None, E.mask_array([0xFF]), None, None, None, None,
+                                       None, None, None, None, None) == OK
+
+
 def test_workspace_size_grows_with_tokens():
     _, a = _ws_size(_desc(n_tokens=64))
     _, b = _ws_size(_desc(n_tokens=4096))

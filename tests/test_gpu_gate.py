@@ -127,6 +127,84 @@ def test_gate_single_token_and_empty():
     assert idx.shape == (0, 2)
 
 
+# ----------------------------------------------------------------------------- group options
+
+def _gate_inputs(T, d, M, K, seed, keep=None, scale=1.0):
+    rng = np.random.default_rng(seed)
+    bf = lambda a: W.f32_to_bf16_bits(np.asarray(a, np.float32))
+    x = bf(rng.standard_normal((T, d)))
+    wg = bf(rng.standard_normal((K, d)) * scale / np.sqrt(d))
+    wl = bf(rng.standard_normal((M, d)) * scale / np.sqrt(d))
+    bg = (rng.standard_normal(K) * 0.3).astype(np.float32)
+    bl = (rng.standard_normal(M) * 0.3).astype(np.float32)
+    members = sorted(rng.choice(M, keep, replace=False).tolist()) if keep else list(range(M))
+    return x, wg, bg, wl, bl, W.mask_words(members, M), members
+
+
+def _group_cut_near_ties(x, wg, bg, members, M, K, k, sizes, top_groups):
+    """Tokens whose kept groups are not fixed by the float32 logits: the last kept and the first
+    left-out group (in the oracle's float64 order) have logits within 1e-4."""
+    gl = W.to_f64(x, W.BF16) @ W.to_f64(wg, W.BF16).T + bg
+    groups = O.expert_groups(M, K, sizes)
+    held = [len(set(g) & set(members)) for g in groups]
+    active = [kk for kk in range(K) if held[kk]]
+    amb = []
+    for t in range(gl.shape[0]):
+        order = sorted(active, key=lambda kk: (-gl[t, kk], kk))
+        n, h = 0, 0
+        while n < len(order) and (n < top_groups or h < k):
+            h += held[order[n]]
+            n += 1
+        if n < len(order) and gl[t, order[n - 1]] - gl[t, order[n]] < 1e-4:
+            amb.append(t)
+    return np.array(amb, dtype=int)
+
+
+@pytest.mark.parametrize("T,d,M,K,k,keep,sizes,top_groups", [
+    (300, 256, 24, 5, 3, 18, (2, 7, 3, 8, 4), 0),      # unequal groups
+    (300, 256, 64, 8, 6, 48, None, 1),                  # top-1 group, extended while < 6 candidates
+    (300, 256, 64, 8, 6, 48, None, 3),
+    (257, 512, 40, 6, 4, 30, (1, 9, 10, 5, 12, 3), 2),  # both, ragged token count
+    (64, 128, 8, 2, 2, None, None, 1),
+    (100, 256, 256, 64, 16, 200, None, 5),              # the maximum gate, top-16
+])
+def test_gate_options_match_oracle(T, d, M, K, k, keep, sizes, top_groups):
+    say(f"gate options T={T} M={M} K={K} k={k} sizes={sizes} top_groups={top_groups}")
+    x, wg, bg, wl, bl, mask, members = _gate_inputs(T, d, M, K, seed=T + M + top_groups, keep=keep)
+    idx, w, probs = E.gate(up(x, W.BF16), mask, up(wg, W.BF16), up_f32(bg), up(wl, W.BF16), up_f32(bl), K, k,
+                           with_probs=True, top_groups=top_groups, group_sizes=sizes)
+    torch.cuda.synchronize()
+    f = lambda a: W.to_f64(a, W.BF16)
+    ridx, rw, g = O.group_gate(f(x), f(wg), bg, f(wl), bl, mask, K, k, group_sizes=sizes, top_groups=top_groups)
+    gidx, gw, gp = down(idx), down(w), down(probs)
+    # tokens whose kept groups hang on a near tie of group logits: valid picks only
+    amb = _group_cut_near_ties(x, wg, bg, members, M, K, k, sizes, top_groups) if top_groups else np.array([], int)
+    assert amb.size <= 0.05 * T, f"{amb.size} tokens with near-tied groups at the cut"
+    for t in amb:
+        assert len(set(gidx[t].tolist())) == k and set(gidx[t].tolist()) <= set(members)
+    ok = np.setdiff1d(np.arange(T), amb)
+    n_cert = check_routing(gidx[ok], gw[ok], ridx[ok], rw[ok], g[ok], members, k)
+    assert_close(gp[ok], g[ok], TOL_F32, "probs")
+    say(f"  certified near-ties: {n_cert}; tokens with near-tied groups at the cut: {amb.size}")
+
+
+def test_gate_top_groups_exact_ties():
+    """Integer-valued inputs with duplicated groups: ties between groups go to the lower group."""
+    inp = _exact_inputs(48, 256, 16, 4, 3, seed=5)
+    cfg = inp.cfg
+    f = inp.f64
+    for G in (1, 2):
+        idx, w, probs = E.gate(up(inp.x, cfg.dtype), inp.mask, up(inp.w_global, cfg.dtype), None,
+                               up(inp.w_local, cfg.dtype), None, cfg.n_groups, cfg.top_k, with_probs=True,
+                               top_groups=G)
+        torch.cuda.synchronize()
+        ridx, rw, g = O.group_gate(f("x"), f("w_global"), inp.b_global, f("w_local"), inp.b_local, inp.mask,
+                                   cfg.n_groups, cfg.top_k, top_groups=G)
+        check_routing(down(idx), down(w), ridx, rw, g, W.mask_members(inp.mask, cfg.n_experts), cfg.top_k,
+                      strict=True)
+        assert_close(down(probs), g, TOL_F32, "probs")
+
+
 def test_gate_is_deterministic():
     inp = W.gen_layer(W.CONFIGS["finegrained"], experts=False)
     a = run_gate(inp)
