@@ -238,6 +238,70 @@ ec2moe_status ec2moe_profile_collect(ec2moe_kernel_stat* out, int32_t max_entrie
  */
 ec2moe_status ec2moe_profile_select(const char* name);
 
+/* ---------------------------------------------------------------- host planner
+ * Producers of the candidate mask and of the end/cloud placement of pipeline tasks, run
+ * on the host (no GPU work, no stream). The paper leaves the capability function H, the
+ * complexity matching function f and their thresholds open; the forms below are this
+ * library's stated choices. All arrays are [host]; nothing is kept after a call.
+ */
+
+/* Device state S_device (Eq. 2): available compute, memory, power budget and network
+ * bandwidth, each >= 0 in the caller's units. */
+typedef struct {
+    double cpu, mem, power, bandwidth;
+} ec2moe_device_state;
+
+typedef struct {
+    double w_cpu, w_mem, w_power, w_bandwidth; /* H (Eq. 3): T_capability = w_cpu cpu + w_mem mem +
+                                                  w_power power + w_bandwidth bandwidth, weights >= 0 */
+    double epsilon;      /* tolerance of Eq. 4, >= 0 */
+    double max_fraction; /* cap on |E_local| / M in [0, 1] (Parameter Selection caps the candidate
+                            set at 40% of the experts); 1 = no cap */
+} ec2moe_selection_params;
+
+/*
+ * Hardware-aware local expert selection (Local Expert Selection, Eq. 2-4) with the
+ * matching function f(V_i, T) = V_i / T_capability: E_local = { i : f <= epsilon };
+ * when more than floor(max_fraction * M) experts qualify, the ones of smallest f are kept
+ * (equal f: the lower index). T_capability <= 0 selects nothing.
+ *   complexity [M] values V_i >= 0; mask_out ceil(M/64) words (bit i set <=> i selected,
+ *   bits >= M clear), the format of ec2moe_group_gate's candidate mask; n_selected out.
+ *   1 <= M <= 256. Errors: EC2MOE_ERR_INVALID_ARGUMENT for NULL pointers, negative or
+ *   non-finite inputs, M out of range.
+ */
+ec2moe_status ec2moe_select_candidates(const ec2moe_device_state* state, const ec2moe_selection_params* params,
+                                       const double* complexity, int32_t n_experts, uint64_t* mask_out,
+                                       int32_t* n_selected);
+
+typedef struct {
+    double alpha;       /* Eq. 9: weight of execution time (1 - alpha: of communication), in [0, 1] */
+    double beta;        /* Eq. 11: priority threshold for local execution */
+    double epsilon;     /* Eq. 10: guard of the priority's denominator, > 0 */
+    double t_end;       /* Eq. 11: computation threshold T_end of the end device */
+    double load_end;    /* initial Load_end */
+    double load_cloud;  /* initial Load_cloud */
+    double speed_end;   /* ExecTime = C / speed_end on the end device, > 0 */
+    double speed_cloud; /* ExecTime = C / speed_cloud in the cloud, > 0 */
+} ec2moe_schedule_params;
+
+/*
+ * Route-aware heuristic pipeline scheduling (Eq. 9-11), greedy: tasks are taken in
+ * descending priority P = C / (Comm + epsilon) (equal P: the lower index); a task runs on
+ * the end device iff Load_end + C <= T_end and P >= beta, and then Load_end grows by C;
+ * otherwise it runs in the cloud and Load_cloud grows by C. The objective of Eq. 9 is
+ * sum over tasks (in index order) of alpha ExecTime + (1 - alpha) Comm, with ExecTime
+ * = C / speed of the chosen side and Comm counted for cloud tasks only (a task run on
+ * the end device transmits nothing).
+ *   complexity, comm [n_tasks] values >= 0; location [n_tasks] out: 0 end, 1 cloud;
+ *   order [n_tasks] out or NULL: the tasks in processing order; summary [3] out or
+ *   NULL: objective, final Load_end, final Load_cloud. n_tasks == 0 is valid.
+ * Errors: EC2MOE_ERR_INVALID_ARGUMENT for NULL pointers, negative or non-finite inputs,
+ * parameters out of range.
+ */
+ec2moe_status ec2moe_schedule_tasks(const ec2moe_schedule_params* params, const double* complexity,
+                                    const double* comm, int32_t n_tasks, int32_t* location, int32_t* order,
+                                    double* summary);
+
 #ifdef __cplusplus
 }
 #endif

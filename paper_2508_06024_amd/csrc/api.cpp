@@ -37,6 +37,16 @@ ec2moe_status ok() {
     return EC2MOE_OK;
 }
 
+}  // namespace
+
+ec2moe_status report_error(ec2moe_status st, const char* detail) {
+    if (st == EC2MOE_OK) return ok();
+    g_last_error = detail;
+    return st;
+}
+
+namespace {
+
 ec2moe_status hip_status(hipError_t e, const char* what) {
     if (e == hipSuccess) return ok();
     return fail(EC2MOE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));

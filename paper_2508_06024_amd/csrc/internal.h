@@ -6,9 +6,14 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "ec2moe.h"
+
 namespace ec2moe {
 
 enum class DType : int32_t { F32 = 0, BF16 = 1 };
+
+// Records the detail of a failing call for ec2moe_last_error() and returns st (api.cpp).
+ec2moe_status report_error(ec2moe_status st, const char* detail);
 
 inline size_t elem_bytes(DType t) { return t == DType::F32 ? 4 : 2; }
 

@@ -48,6 +48,21 @@ class GateOpts(ctypes.Structure):
     _fields_ = [("top_groups", ctypes.c_int32), ("group_sizes", ctypes.POINTER(ctypes.c_int32))]
 
 
+class DeviceState(ctypes.Structure):
+    _fields_ = [("cpu", ctypes.c_double), ("mem", ctypes.c_double), ("power", ctypes.c_double),
+                ("bandwidth", ctypes.c_double)]
+
+
+class SelectionParams(ctypes.Structure):
+    _fields_ = [("w_cpu", ctypes.c_double), ("w_mem", ctypes.c_double), ("w_power", ctypes.c_double),
+                ("w_bandwidth", ctypes.c_double), ("epsilon", ctypes.c_double), ("max_fraction", ctypes.c_double)]
+
+
+class ScheduleParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("alpha", "beta", "epsilon", "t_end", "load_end", "load_cloud",
+                                                "speed_end", "speed_cloud")]
+
+
 class KernelStat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int64), ("total_ms", ctypes.c_double)]
 
@@ -79,6 +94,9 @@ _SIGS = {
     "ec2moe_profile_enable": [ctypes.c_int32],
     "ec2moe_profile_collect": [ctypes.POINTER(KernelStat), ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)],
     "ec2moe_profile_select": [ctypes.c_char_p],
+    "ec2moe_select_candidates": [ctypes.POINTER(DeviceState), ctypes.POINTER(SelectionParams), _P, ctypes.c_int32,
+                                 ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_int32)],
+    "ec2moe_schedule_tasks": [ctypes.POINTER(ScheduleParams), _P, _P, ctypes.c_int32, _P, _P, _P],
 }
 for _name, _args in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -362,3 +380,34 @@ def last_error() -> str:
 
 def status_string(code: int) -> str:
     return _lib.ec2moe_status_string(code).decode()
+
+
+# ----------------------------------------------------------------------------- host planner
+
+def _f64(a):
+    import numpy as np
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def select_candidates(state: DeviceState, params: SelectionParams, complexity):
+    """Candidate mask words of the experts the end device may run (host call; no GPU)."""
+    v = _f64(complexity)
+    M = int(v.size)
+    words = (ctypes.c_uint64 * max(1, (M + 63) // 64))()
+    n = ctypes.c_int32(0)
+    _check(_lib.ec2moe_select_candidates(ctypes.byref(state), ctypes.byref(params), v.ctypes.data_as(_P), M, words,
+                                         ctypes.byref(n)))
+    return [int(w) for w in words][: (M + 63) // 64], n.value
+
+
+def schedule_tasks(params: ScheduleParams, complexity, comm):
+    """(location int32 [N]: 0 end, 1 cloud; order int32 [N]; (objective, load_end, load_cloud))."""
+    import numpy as np
+    c, m = _f64(complexity), _f64(comm)
+    n = int(c.size)
+    loc = np.zeros(n, np.int32)
+    order = np.zeros(n, np.int32)
+    summary = np.zeros(3, np.float64)
+    _check(_lib.ec2moe_schedule_tasks(ctypes.byref(params), c.ctypes.data_as(_P), m.ctypes.data_as(_P), n,
+                                      loc.ctypes.data_as(_P), order.ctypes.data_as(_P), summary.ctypes.data_as(_P)))
+    return loc, order, tuple(float(x) for x in summary)
