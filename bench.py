@@ -236,6 +236,23 @@ def main():
             "frac": round(achieved / peak, 4), "traffic": traffic,
             "algorithmic": {"flop": flop, "bytes": byt}, "avg_launch_us": round(avg_s * 1e6, 1)}
 
+    # host planner (candidate mask producer and task scheduler): host time per call
+    rng = np.random.default_rng(0)
+    comp = rng.gamma(2.0, 2.0, cfg.n_experts)
+    st, sp = E.DeviceState(4, 4, 4, 4), E.SelectionParams(1, 1, 1, 1, 1.0, 0.4)
+    tc, tm = rng.gamma(2.0, 1.0, 1024), rng.gamma(1.5, 1.0, 1024)
+    sch = E.ScheduleParams(0.5, 1.0, 1e-3, 200.0, 0.0, 0.0, 1.0, 4.0)
+    t0 = time.perf_counter()
+    for _ in range(200):
+        E.select_candidates(st, sp, comp)
+    t1 = time.perf_counter()
+    for _ in range(200):
+        E.schedule_tasks(sch, tc, tm)
+    t2 = time.perf_counter()
+    planner = {"select_candidates_us": round((t1 - t0) / 200 * 1e6, 2), "experts": cfg.n_experts,
+               "schedule_tasks_us": round((t2 - t1) / 200 * 1e6, 2), "tasks": 1024,
+               "note": "host calls through the Python binding (marshalling included)"}
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
@@ -267,6 +284,7 @@ def main():
         "kernels": kernels,
         "kernels_pass": f"separate pass of {prof_steps} steps with HIP events around every kernel",
         "cpu_baseline": cpu,
+        "planner": planner,
     }
     print(json.dumps(out), flush=True)
 

@@ -38,7 +38,7 @@
 // applied to the float32 sums before rounding, in every store path including the split-K
 // reduction.
 #include "device_common.h"
-#include "internal.h"
+#include "gemm.h"
 
 #include <algorithm>
 #include <string>
