@@ -16,6 +16,8 @@ Sources (EC2MoE, arXiv 2508.06024):
   * Encoder-Decoder based on Low-Rank Compression: Z = U^T X V at the end,
     X_hat = U_hat Z V_hat^T in the cloud.
   * Parameter Selection: top-1 routing in the paper's runs; top-k in general.
+  * Eq. (8): the codec's reconstruction loss; with lambda = 0 (no task loss) its
+    minimiser for one slice is the truncated SVD (codec_fit_hosvd).
 
 Readings where the paper is silent (each is also listed with the design notes):
   * the candidate filter acts before both softmaxes: non-candidates get no
@@ -285,3 +287,55 @@ def layer(x, mask_words, w_global, b_global, w_local, b_local, w_gate_up, w_down
     z = zs[0] if codec_slices == 1 else np.stack(zs)
     y = moe_forward(x_hat, idx, w, w_gate_up, w_down, activation)
     return {"idx": idx, "w": w, "g": g, "z": z, "x_hat": x_hat, "y": y}
+
+
+# ----------------------------------------------------------------------------- codec fitting, Eq. (8) with lambda = 0
+
+def _unfold_rows(xs):
+    """Mode-1 unfolding [X_1 X_2 ... X_c] (h x c*w) of slices xs [c][h][w]."""
+    xs = np.asarray(xs, np.float64)
+    return np.concatenate(list(xs), axis=1)
+
+
+def _unfold_cols(xs):
+    """Mode-2 unfolding [X_1^T X_2^T ... X_c^T] (w x c*h)."""
+    xs = np.asarray(xs, np.float64)
+    return np.concatenate([x.T for x in xs], axis=1)
+
+
+def codec_fit_hosvd(xs, r_h, r_w):
+    """Data-free fit of the codec projections (Eq. 8 with lambda = 0): U = the r_h leading left
+    singular vectors of the mode-1 unfolding of the calibration slices, V = the r_w leading
+    left singular vectors of the mode-2 unfolding (the truncated higher-order SVD). For one
+    slice this is the truncated SVD of X, the minimiser of ||X - U U^T X V V^T||^2
+    (Eckart-Young)."""
+    u = np.linalg.svd(_unfold_rows(xs), full_matrices=False)[0][:, :r_h]
+    v = np.linalg.svd(_unfold_cols(xs), full_matrices=False)[0][:, :r_w]
+    return u, v
+
+
+def orthonormal_basis(y):
+    """Q of the QR factorisation y = Q R with R's diagonal positive (unique for full column rank)."""
+    q, r = np.linalg.qr(np.asarray(y, np.float64))
+    s = np.sign(np.diag(r))
+    s[s == 0] = 1.0
+    return q * s
+
+
+def codec_fit_subspace(xs, omega_u, omega_v, iters):
+    """The same projections by subspace iteration on the Gram matrices (Halko, Martinsson and
+    Tropp, 2011, Alg. 4.4 applied to a symmetric matrix): A = sum_s X_s X_s^T, B = sum_s X_s^T X_s;
+    Q_0 = orth(Omega), Q_i = orth(A Q_{i-1}) (resp. B) for i = 1..iters; U = Q_iters for A, V for B.
+    The returned bases span the leading subspaces once iters is large enough for the spectral gap;
+    the projector U U^T does not depend on the basis chosen inside the subspace."""
+    xs = np.asarray(xs, np.float64)
+    a = sum(x @ x.T for x in xs)
+    b = sum(x.T @ x for x in xs)
+
+    def iterate(g, omega):
+        q = orthonormal_basis(omega)
+        for _ in range(iters):
+            q = orthonormal_basis(g @ q)
+        return q
+
+    return iterate(a, omega_u), iterate(b, omega_v)

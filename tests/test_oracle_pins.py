@@ -568,3 +568,67 @@ def test_layer_routes_on_x_and_runs_experts_on_reconstruction():
     np.testing.assert_allclose(out["x_hat"], xh, atol=1e-14)
     assert out["y"].shape == (cfg.n_tokens, cfg.d_model)
     assert not set(out["idx"].ravel().tolist()) & set(cfg.masked_out)
+
+
+# ----------------------------------------------------------------------------- codec fitting (Eq. 8, lambda = 0)
+
+def _spectrum_matrix(rng, h, w, sv):
+    """X = P diag(sv) Q^T with Haar P [h][n], Q [w][n]."""
+    p = W.haar_orthonormal(int(rng.integers(1 << 30)), (1,), h, len(sv))
+    q = W.haar_orthonormal(int(rng.integers(1 << 30)), (2,), w, len(sv))
+    return (p * np.asarray(sv)) @ q.T
+
+
+def test_fit_one_slice_reaches_eckart_young():
+    rng = np.random.default_rng(50)
+    h, w, r = 40, 56, 7
+    sv = np.linspace(5.0, 0.2, 30)
+    x = _spectrum_matrix(rng, h, w, sv)
+    u, v = O.codec_fit_hosvd(x[None], r, r)
+    xh = O.lowrank_decode(O.lowrank_encode(x, u, v), u, v)
+    np.testing.assert_allclose(np.sum((x - xh) ** 2), np.sum(sv[r:] ** 2), rtol=1e-10)
+    np.testing.assert_allclose(u.T @ u, np.eye(r), atol=1e-12)
+    np.testing.assert_allclose(v.T @ v, np.eye(r), atol=1e-12)
+
+
+def test_fit_recovers_low_rank_slices_exactly():
+    """Slices sharing row and column spaces of rank <= r are reconstructed exactly."""
+    rng = np.random.default_rng(51)
+    c, h, w, r = 3, 30, 44, 6
+    p = W.haar_orthonormal(3, (1,), h, 4)
+    q = W.haar_orthonormal(3, (2,), w, 5)
+    xs = np.stack([p @ rng.standard_normal((4, 5)) @ q.T for _ in range(c)])
+    for u, v in (O.codec_fit_hosvd(xs, r, r),
+                 O.codec_fit_subspace(xs, rng.standard_normal((h, r)), rng.standard_normal((w, r)), 2)):
+        for s in range(c):
+            xh = O.lowrank_decode(O.lowrank_encode(xs[s], u, v), u, v)
+            np.testing.assert_allclose(xh, xs[s], atol=1e-10)
+
+
+def test_subspace_iteration_converges_to_the_hosvd_subspace():
+    rng = np.random.default_rng(52)
+    c, h, w, r = 2, 48, 64, 5
+    sv = np.concatenate([np.linspace(10, 6, r), np.linspace(1.0, 0.1, 20)])  # gap after r
+    # slices sharing their singular vectors (per-slice scales): the Gram sums keep the gap
+    p = W.haar_orthonormal(7, (1,), h, sv.size)
+    q = W.haar_orthonormal(7, (2,), w, sv.size)
+    xs = np.stack([(p * (sv * rng.uniform(0.9, 1.1, sv.size))) @ q.T for _ in range(c)])
+    u0, v0 = O.codec_fit_hosvd(xs, r, r)
+    u, v = O.codec_fit_subspace(xs, rng.standard_normal((h, r)), rng.standard_normal((w, r)), 12)
+    np.testing.assert_allclose(u @ u.T, u0 @ u0.T, atol=1e-9)
+    np.testing.assert_allclose(v @ v.T, v0 @ v0.T, atol=1e-9)
+    np.testing.assert_allclose(u.T @ u, np.eye(r), atol=1e-12)
+
+
+def test_orthonormal_basis_is_the_positive_diagonal_qr():
+    rng = np.random.default_rng(53)
+    y = rng.standard_normal((30, 6))
+    q = O.orthonormal_basis(y)
+    r = q.T @ y
+    np.testing.assert_allclose(np.tril(r, -1), 0.0, atol=1e-12)
+    assert np.all(np.diag(r) > 0)
+    # Gram-Schmidt by hand on the first two columns
+    e1 = y[:, 0] / np.linalg.norm(y[:, 0])
+    t = y[:, 1] - (e1 @ y[:, 1]) * e1
+    np.testing.assert_allclose(q[:, 0], e1, atol=1e-12)
+    np.testing.assert_allclose(q[:, 1], t / np.linalg.norm(t), atol=1e-12)
