@@ -238,6 +238,32 @@ ec2moe_status ec2moe_profile_collect(ec2moe_kernel_stat* out, int32_t max_entrie
  */
 ec2moe_status ec2moe_profile_select(const char* name);
 
+/* Workspace bytes needed by ec2moe_lowrank_fit. */
+ec2moe_status ec2moe_lowrank_fit_workspace_size(const ec2moe_codec_desc* desc, size_t* bytes /*[host]*/);
+
+/*
+ * Data-free fitting of the codec projections (Encoder-Decoder based on Low-Rank
+ * Compression, Eq. 8 with lambda = 0: the reconstruction loss alone). The target is the
+ * truncated higher-order SVD of the calibration slices: U spans the r_h leading left
+ * singular vectors of [X_1 ... X_c], V the r_w leading ones of [X_1^T ... X_c^T] (for one
+ * slice, the truncated SVD of X, the Eckart-Young minimiser of ||X - U U^T X V V^T||).
+ * Computed by subspace iteration on the Gram matrices A = sum X_s X_s^T and B = sum
+ * X_s^T X_s, starting from the given blocks and orthonormalising every iterate (the
+ * positive-diagonal QR, by CholeskyQR2 with a float64 Gram matrix and factor).
+ *   x [c][h][w] calibration slices (layer dtype; c*h a multiple of 8);
+ *   omega_u [h][r_h], omega_v [w][r_w] float32 start blocks of full column rank (random,
+ *   drawn by the caller); iters >= 0 (at most 64) steps: the columns converge to the
+ *   leading subspaces at the rate of the spectral gap;
+ *   u [h][r_h], v [w][r_w] out, layer dtype, orthonormal columns (to the layer precision);
+ *   status device int32 out or NULL: 0, or 1 if a Cholesky pivot was not positive (a start
+ *   block or data of rank below r: the outputs are then not orthonormal);
+ *   ws of ec2moe_lowrank_fit_workspace_size bytes (two float32 Gram matrices of the larger
+ *   of h and w, among others).
+ */
+ec2moe_status ec2moe_lowrank_fit(const ec2moe_codec_desc* desc, const void* x, const float* omega_u,
+                                 const float* omega_v, int32_t iters, void* u, void* v, int32_t* status,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* ---------------------------------------------------------------- host planner
  * Producers of the candidate mask and of the end/cloud placement of pipeline tasks, run
  * on the host (no GPU work, no stream). The paper leaves the capability function H, the

@@ -563,6 +563,132 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
     return hip_status(e, "lowrank_decode launch");
 }
 
+namespace {
+
+struct FitWs {
+    size_t gpart, gram, xt, q, y, q1, qt, g64, rinv64, rinv_t, total;
+};
+
+FitWs fit_ws(const ec2moe_codec_desc* d) {
+    const size_t eb = elem_bytes(static_cast<DType>(d->dtype));
+    const size_t n = static_cast<size_t>(std::max(d->h, d->w));
+    const size_t r = static_cast<size_t>(std::max(d->r_h, d->r_w));
+    const size_t cells = static_cast<size_t>(std::max(1, d->n_slices)) * d->h * d->w;
+    FitWs w{};
+    size_t o = 0;
+    w.gpart = o; o += up(gemm_split_scratch_bytes());
+    w.gram = o; o += up(n * n * 4);
+    w.xt = o; o += up(cells * eb);
+    w.q = o; o += up(n * r * 4);
+    w.y = o; o += up(n * r * 4);
+    w.q1 = o; o += up(n * r * 4);
+    w.qt = o; o += up(n * r * 4);
+    w.g64 = o; o += up(r * r * 8);
+    w.rinv64 = o; o += up(r * r * 8);
+    w.rinv_t = o; o += up(r * r * 4);
+    w.total = o;
+    return w;
+}
+
+hipError_t dense_gemm(DType dt, OutType ot, const void* tok, const void* wt, int64_t rows, int K, int N, void* out,
+                      const char* name, float* part, hipStream_t s) {
+    GemmArgs g{};
+    g.tok = tok; g.row_index = nullptr; g.w = wt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;
+    g.rows = rows; g.K = K; g.N = N; g.out = out; g.ldo = N; g.name = name;
+    g.src_rows = rows; g.w_rows = N; g.part = part; g.max_split = kMaxSplit;
+    return launch_gemm(dt, Epilogue::Store, ot, g, s);
+}
+
+// Q = orth(Y) for Y [n][r] float32 (CholeskyQR2, the first pass into q1); q receives the result.
+hipError_t orthonormalise(float* y, int n, int r, float* q1, float* q, const FitWs& w, void* ws, int32_t* status,
+                          bool& reset, hipStream_t s) {
+    double* g64 = at<double>(ws, w.g64);
+    float* rinv_t = at<float>(ws, w.rinv_t);
+    float* part = at<float>(ws, w.gpart);
+    const float* src = y;
+    for (int pass = 0; pass < 2; ++pass) {
+        float* dst = pass == 0 ? q1 : q;
+        hipError_t e = launch_gram64(src, n, r, g64, s);
+        if (e == hipSuccess) e = launch_chol_inv(g64, r, rinv_t, at<double>(ws, w.rinv64), status, reset, s);
+        reset = false;
+        if (e == hipSuccess) e = dense_gemm(DType::F32, OutType::Same, src, rinv_t, n, r, r, dst, "fit_qr", part, s);
+        if (e != hipSuccess) return e;
+        src = dst;
+    }
+    return hipSuccess;
+}
+
+// Subspace iteration of one side: gram [n][n] float32, omega [n][r]; the result in q.
+hipError_t fit_side(const float* gram, const float* omega, int n, int r, int iters, const FitWs& w, void* ws,
+                    int32_t* status, bool& reset, hipStream_t s) {
+    float* q = at<float>(ws, w.q);
+    float* y = at<float>(ws, w.y);
+    float* q1 = at<float>(ws, w.q1);
+    float* qt = at<float>(ws, w.qt);
+    hipError_t e = orthonormalise(const_cast<float*>(omega), n, r, q1, q, w, ws, status, reset, s);
+    for (int it = 0; it < iters && e == hipSuccess; ++it) {
+        e = launch_transpose(DType::F32, q, n, r, qt, s);  // Q^T [r][n]: the GEMM's weight rows
+        if (e == hipSuccess) e = dense_gemm(DType::F32, OutType::Same, gram, qt, n, n, r, y, "fit_power", at<float>(ws, w.gpart), s);
+        if (e == hipSuccess) e = orthonormalise(y, n, r, q1, q, w, ws, status, reset, s);
+    }
+    return e;
+}
+
+}  // namespace
+
+ec2moe_status ec2moe_lowrank_fit_workspace_size(const ec2moe_codec_desc* desc, size_t* bytes) {
+    if (ec2moe_status st = check_codec_desc(desc); st != EC2MOE_OK) return st;
+    REQUIRE_PTR(bytes);
+    *bytes = fit_ws(desc).total;
+    return ok();
+}
+
+ec2moe_status ec2moe_lowrank_fit(const ec2moe_codec_desc* desc, const void* x, const float* omega_u,
+                                 const float* omega_v, int32_t iters, void* u, void* v, int32_t* status,
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (ec2moe_status st = check_codec_desc(desc); st != EC2MOE_OK) return st;
+    const FitWs w = fit_ws(desc);
+    if (ec2moe_status st = check_ws(ws, ws_bytes, w.total); st != EC2MOE_OK) return st;
+    REQUIRE(desc->n_slices >= 1 && desc->h >= 1, EC2MOE_ERR_INVALID_ARGUMENT, "fitting needs at least one slice of one row");
+    REQUIRE(iters >= 0 && iters <= 64, EC2MOE_ERR_INVALID_ARGUMENT, "iters %d outside [0, 64]", iters);
+    REQUIRE(static_cast<int64_t>(desc->n_slices) * desc->h % 8 == 0, EC2MOE_ERR_UNSUPPORTED,
+            "c*h = %lld is not a multiple of 8", static_cast<long long>(desc->n_slices) * desc->h);
+    REQUIRE(static_cast<int64_t>(desc->n_slices) * desc->h * desc->w * elem_bytes(static_cast<DType>(desc->dtype)) <
+                (int64_t(1) << 32), EC2MOE_ERR_UNSUPPORTED, "calibration block too large for 32-bit byte offsets");
+    REQUIRE_PTR(x); REQUIRE_PTR(omega_u); REQUIRE_PTR(omega_v); REQUIRE_PTR(u); REQUIRE_PTR(v);
+    REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(omega_u); REQUIRE_ALIGNED(omega_v); REQUIRE_ALIGNED(u); REQUIRE_ALIGNED(v);
+    const DType dt = static_cast<DType>(desc->dtype);
+    const int c = desc->n_slices, h = desc->h, wd = desc->w;
+    float* gram = at<float>(ws, w.gram);
+    void* xt = at<void>(ws, w.xt);
+    float* part = at<float>(ws, w.gpart);
+    bool reset = true;
+    // A = sum_s X_s X_s^T [h][h]: the mode-1 unfolding times itself (K = c*w)
+    const void* xu = x;
+    hipError_t e = hipSuccess;
+    if (c > 1) {
+        e = launch_unfold(dt, x, c, h, wd, xt, stream);
+        xu = xt;
+    }
+    if (e == hipSuccess) e = dense_gemm(dt, OutType::F32, xu, xu, h, c * wd, h, gram, "fit_gram_a", part, stream);
+    if (e == hipSuccess) e = fit_side(gram, omega_u, h, desc->r_h, iters, w, ws, status, reset, stream);
+    if (e == hipSuccess) {
+        const int64_t nu = static_cast<int64_t>(h) * desc->r_h;
+        e = dt == DType::BF16 ? launch_f32_to_bf16(at<float>(ws, w.q), nu, u, stream)
+                              : hipMemcpyAsync(u, at<float>(ws, w.q), nu * 4, hipMemcpyDeviceToDevice, stream);
+    }
+    // B = sum_s X_s^T X_s [w][w]: X^T [w][c*h] times itself (K = c*h)
+    if (e == hipSuccess) e = launch_transpose(dt, x, c * h, wd, xt, stream);
+    if (e == hipSuccess) e = dense_gemm(dt, OutType::F32, xt, xt, wd, c * h, wd, gram, "fit_gram_b", part, stream);
+    if (e == hipSuccess) e = fit_side(gram, omega_v, wd, desc->r_w, iters, w, ws, status, reset, stream);
+    if (e == hipSuccess) {
+        const int64_t nv = static_cast<int64_t>(wd) * desc->r_w;
+        e = dt == DType::BF16 ? launch_f32_to_bf16(at<float>(ws, w.q), nv, v, stream)
+                              : hipMemcpyAsync(v, at<float>(ws, w.q), nv * 4, hipMemcpyDeviceToDevice, stream);
+    }
+    return hip_status(e, "lowrank_fit launch");
+}
+
 ec2moe_status ec2moe_profile_enable(int32_t enable) {
     Profiler& p = prof();
     std::lock_guard<std::mutex> lk(p.mu);

@@ -72,6 +72,15 @@ hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s);
 // null); seg_w[s] = s*w, rows_w[p] = p % w, seg_h[s] = s*h, rows_h[p] = p % h (s <= n).
 hipError_t launch_codec_prep(const float* z, int64_t nz, void* zb, int n, int w, int h, int32_t* seg_w,
                              int32_t* rows_w, int32_t* seg_h, int32_t* rows_h, hipStream_t s);
+// ---------------------------------------------------------------- codec fitting
+// g = y^T y in float64 (y [n][r] float32, g [r][r])
+hipError_t launch_gram64(const float* y, int n, int r, double* g, hipStream_t s);
+// g = R^T R (Cholesky, in place, float64) and rinv_t[n][k] = (R^-1)[k][n] in float32; rinv is a
+// float64 [r][r] scratch. *status: 1 if a pivot was not positive (set to 0 first when reset).
+hipError_t launch_chol_inv(double* g, int r, float* rinv_t, double* rinv, int32_t* status, bool reset, hipStream_t s);
+// xu [h][c*w] = the slices [c][h][w] side by side (w a multiple of 16 bytes)
+hipError_t launch_unfold(DType dt, const void* x, int c, int h, int w, void* xu, hipStream_t s);
+
 // dst = bfloat16(src) with round-to-nearest-even, n a multiple of 4
 hipError_t launch_f32_to_bf16(const float* src, int64_t n, void* dst, hipStream_t s);
 

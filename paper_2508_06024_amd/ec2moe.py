@@ -89,6 +89,8 @@ _SIGS = {
     "ec2moe_lowrank_workspace_size": [ctypes.POINTER(CodecDesc), ctypes.POINTER(ctypes.c_size_t)],
     "ec2moe_lowrank_encode": [ctypes.POINTER(CodecDesc), _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
     "ec2moe_lowrank_decode": [ctypes.POINTER(CodecDesc), _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
+    "ec2moe_lowrank_fit_workspace_size": [ctypes.POINTER(CodecDesc), ctypes.POINTER(ctypes.c_size_t)],
+    "ec2moe_lowrank_fit": [ctypes.POINTER(CodecDesc), _P, _P, _P, ctypes.c_int32, _P, _P, _P, _P, ctypes.c_size_t, _P],
     "ec2moe_status_string": [ctypes.c_int],
     "ec2moe_last_error": [],
     "ec2moe_profile_enable": [ctypes.c_int32],
@@ -353,6 +355,27 @@ def lowrank_decode(z, u_hat, v_hat, ws=None):
     x_hat = torch.empty((c, h, w), dtype=dt, device=z.device)
     lowrank_decode_into(desc, zs, u_hat, v_hat, x_hat, ws)
     return x_hat[0] if squeeze else x_hat
+
+
+def lowrank_fit(x, omega_u, omega_v, iters, ws=None):
+    """Fit U [h][r_h], V [w][r_w] to calibration slices x [h][w] or [c][h][w] (layer dtype) from
+    float32 start blocks; returns (u, v, status) with status a device int32 (0 = ok)."""
+    xs = x if x.dim() == 3 else x.unsqueeze(0)
+    c, h, w = xs.shape
+    rh, rw = omega_u.shape[1], omega_v.shape[1]
+    _dev(xs, "x")
+    _dev(omega_u, "omega_u", torch.float32, (h, rh))
+    _dev(omega_v, "omega_v", torch.float32, (w, rw))
+    desc = codec_desc(h, w, rh, rw, xs.dtype, c)
+    n = ctypes.c_size_t(0)
+    _check(_lib.ec2moe_lowrank_fit_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    ws = ws if ws is not None else workspace(n.value, xs.device)
+    u = torch.empty((h, rh), dtype=xs.dtype, device=xs.device)
+    v = torch.empty((w, rw), dtype=xs.dtype, device=xs.device)
+    status = torch.empty((1,), dtype=torch.int32, device=xs.device)
+    _check(_lib.ec2moe_lowrank_fit(ctypes.byref(desc), _ptr(xs), _ptr(omega_u), _ptr(omega_v), int(iters), _ptr(u),
+                                   _ptr(v), _ptr(status), _ptr(ws), ws.numel(), _stream()))
+    return u, v, status
 
 
 # ----------------------------------------------------------------------------- kernel timing
