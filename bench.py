@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral", choices=ALL_ORDER)
     ap.add_argument("--rotate", type=int, default=4, help="distinct copies of X cycled through the steps")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of HIP graphs of the step (one per input copy) instead of eager launches")
     ap.add_argument("--top-groups", type=int, default=0,
                     help="group-focused gate: keep the top G groups per token (0: every group)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -158,16 +160,46 @@ def main():
     dom = max((n for n in stats if n in work), key=lambda n: stats[n][1])
 
     # Timed region: events only around the dominant kernel, so the others run back to back.
-    E.profile_select(dom)
-    E.profile_enable(True)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for i in range(steps):
-        step(i)
-    end.record()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end)
+    if args.graph and not per_call:
+        # one graph per input copy (captured on a side stream after a warm-up there); the
+        # dominant kernel's time comes from an eager pass with its events right after
+        graphs = []
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for i in range(len(xs)):
+                step(i)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        for i in range(len(xs)):
+            layer.set_input(xs[i], masks[i % len(masks)])
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                layer.step()
+            graphs.append(g)
+        torch.cuda.synchronize()
+        start.record()
+        for i in range(steps):
+            graphs[i % len(graphs)].replay()
+        end.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end)
+        E.profile_select(dom)
+        E.profile_enable(True)
+        for i in range(prof_steps):
+            step(i)
+        torch.cuda.synchronize()
+    else:
+        E.profile_select(dom)
+        E.profile_enable(True)
+        torch.cuda.synchronize()
+        start.record()
+        for i in range(steps):
+            step(i)
+        end.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end)
     dom_stats = E.profile_collect()[dom]
     E.profile_enable(False)
     E.profile_select(None)
@@ -283,6 +315,8 @@ def main():
         "layer_roofline_frac": round(step_roof_ms / ms_step, 4),
         "kernels": kernels,
         "kernels_pass": f"separate pass of {prof_steps} steps with HIP events around every kernel",
+        "launch": ("HIP graph replays of the step (the dominant kernel's time from an eager pass)"
+                   if args.graph and not per_call else "eager launches"),
         "cpu_baseline": cpu,
         "planner": planner,
     }
