@@ -73,8 +73,10 @@ hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s);
 hipError_t launch_codec_prep(const float* z, int64_t nz, void* zb, int n, int w, int h, int32_t* seg_w,
                              int32_t* rows_w, int32_t* seg_h, int32_t* rows_h, hipStream_t s);
 // ---------------------------------------------------------------- codec fitting
-// g = y^T y in float64 (y [n][r] float32, g [r][r])
-hipError_t launch_gram64(const float* y, int n, int r, double* g, hipStream_t s);
+// g = y^T y in float64 (y [n][r] float32, g [r][r]) through per-chunk partials part
+// ([gram64_chunks(n, r)][r][r] float64) added in chunk order
+int gram64_chunks(int n, int r);
+hipError_t launch_gram64(const float* y, int n, int r, double* part, double* g, hipStream_t s);
 // g = R^T R (Cholesky, in place, float64) and rinv_t[n][k] = (R^-1)[k][n] in float32; rinv is a
 // float64 [r][r] scratch. *status: 1 if a pivot was not positive (set to 0 first when reset).
 hipError_t launch_chol_inv(double* g, int r, float* rinv_t, double* rinv, int32_t* status, bool reset, hipStream_t s);
