@@ -211,3 +211,22 @@ def test_gate_is_deterministic():
     b = run_gate(inp)
     for u, v in zip(a, b):
         assert torch.equal(u, v)
+
+
+def test_planner_mask_feeds_the_gate():
+    """The host planner's candidate set (device state -> capability -> complexity match, at
+    most 40% of the experts) drives the gate: every pick is a planner candidate, and the
+    routing matches the oracle's on the same mask (the paper-shaped 64-expert layer)."""
+    cfg = W.CONFIGS["switch64"]
+    inp = W.gen_layer(cfg, experts=False)
+    rng = np.random.default_rng(21)
+    complexity = [float(v) for v in rng.gamma(2.0, 2.0, cfg.n_experts)]
+    words, n = E.select_candidates(E.DeviceState(3.0, 2.0, 1.0, 0.5), E.SelectionParams(1, 1, 1, 1, 2.0, 0.4),
+                                   complexity)
+    assert cfg.top_k <= n <= int(0.4 * cfg.n_experts)
+    inp.mask = words
+    idx, w, probs = run_gate(inp)
+    torch.cuda.synchronize()
+    members = set(W.mask_members(words, cfg.n_experts))
+    assert set(down(idx).ravel().tolist()) <= members
+    compare(inp)
