@@ -218,7 +218,7 @@ def main():
         del a, b
 
     # per-kernel algorithmic work at the realised routing
-    base = {"perm_small": "permute", "perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
+    base = {"gate_split": "gate", "perm_small": "permute", "perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
             "transpose": "encode", "codec_xv": "encode", "codec_utp": "encode",
             "codec_z_bf16": "decode", "codec_prep": "decode", "codec_vzt": "decode", "codec_uw": "decode"}
 

@@ -114,7 +114,16 @@ typedef struct {
     const int32_t* group_sizes; /* [host] K group sizes M_k >= 1 summing to M (Eq. 5: M = sum
                                    of M_k), group k = the next M_k experts; NULL: K equal
                                    groups (K must divide M). Read during the call only. */
+    void* workspace;            /* [device] or NULL: scratch of ec2moe_gate_workspace_size bytes
+                                   (16-byte aligned, no initial contents) that lets a small
+                                   batch split d over more workgroups; NULL runs unsplit.
+                                   Calls that overlap on one workspace race. */
+    size_t workspace_bytes;     /* size of workspace; an error if below the required size */
 } ec2moe_gate_opts;
+
+/* Gate workspace bytes for this descriptor (0: the batch is large enough to run unsplit,
+ * and the gate ignores a workspace). */
+ec2moe_status ec2moe_gate_workspace_size(const ec2moe_moe_desc* desc, size_t* bytes /*[host]*/);
 
 /*
  * ec2moe_group_gate with options (opts may be NULL: the same as ec2moe_group_gate).

@@ -325,7 +325,26 @@ ec2moe_status ec2moe_group_gate_ex(const ec2moe_moe_desc* desc, const ec2moe_gat
     a.n_tokens = desc->n_tokens; a.d = desc->d_model; a.n_experts = M; a.n_groups = K;
     a.top_k = desc->top_k; a.renormalize = (desc->flags & EC2MOE_GATE_RENORMALIZE) != 0;
     for (int i = 0; i < 4; ++i) a.mask[i] = i < words ? cand_mask[i] : 0;
-    return hip_status(launch_gate(static_cast<DType>(desc->dtype), a, stream), "gate launch");
+    const DType dt = static_cast<DType>(desc->dtype);
+    if (opts && opts->workspace) {
+        const size_t need = gate_split_bytes(dt, desc->n_tokens, desc->d_model, M + K);
+        REQUIRE(opts->workspace_bytes >= need, EC2MOE_ERR_WORKSPACE_TOO_SMALL,
+                "gate workspace of %zu bytes, %zu needed", opts->workspace_bytes, need);
+        REQUIRE(aligned16(opts->workspace), EC2MOE_ERR_INVALID_ARGUMENT, "gate workspace is not 16-byte aligned");
+        if (need > 0) {
+            a.ws = static_cast<float*>(opts->workspace);
+            a.nsplit = gate_split_count(dt, desc->n_tokens, desc->d_model);
+        }
+    }
+    return hip_status(launch_gate(dt, a, stream), "gate launch");
+}
+
+ec2moe_status ec2moe_gate_workspace_size(const ec2moe_moe_desc* desc, size_t* bytes) {
+    if (ec2moe_status st = check_moe_desc(desc, false); st != EC2MOE_OK) return st;
+    REQUIRE_PTR(bytes);
+    *bytes = gate_split_bytes(static_cast<DType>(desc->dtype), desc->n_tokens, desc->d_model,
+                              desc->n_experts + desc->n_groups);
+    return ok();
 }
 
 ec2moe_status ec2moe_group_gate(const ec2moe_moe_desc* desc, const uint64_t* cand_mask, const void* x,

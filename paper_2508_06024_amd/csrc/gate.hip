@@ -27,6 +27,11 @@ constexpr int kMaxRowBlocks = 20;   // M + K <= 320 gate rows
 constexpr int kMaxGroups = 160;
 constexpr int kMaxExperts = 256;
 constexpr int kChunk = 8;           // logits of one group read together in phase 3
+constexpr int kSplitWaves = 4;      // waves of the split-d workgroups (small batches)
+constexpr int kSplitMaxTiles = 64;  // 16-token tiles below which d is split (given a workspace)
+constexpr int kMaxSplit = 32;       // d-splits per tile at most
+constexpr int kSplitMinD = 2048;    // narrower gates run unsplit (the second launch costs more)
+constexpr int kRouteWaves = 8;      // waves of the routing workgroups after a split
 
 // Keeps a kernel-argument value in a scalar register: left alone, the compiler may reload
 // it from the argument segment at every use, and each reload waits on that memory.
@@ -69,7 +74,7 @@ __device__ __forceinline__ float seg_sum(float v, int width) {
 // Routing of token tl of the tile by its 8 lanes (sub-lane s holds experts s*EPL ..
 // s*EPL + EPL - 1, EPL = M / 8, all in group (s*EPL) / Mk, whose LG = Mk / EPL lanes are
 // aligned). Logits come from the summed, biased, masked rows in LDS; the token's fused
-// probabilities are kept in LDS (wave 1's partials, free after phase 2) for the outputs.
+// probabilities are kept in the second tile-sized slot of the LDS for the outputs.
 //   stage 2: group max and sum of e^(l - max), lane-local then across the group's lanes;
 //   stage 1: softmax over the groups that hold a candidate, across the 8 lanes;
 //   with top_groups, each lane ranks its group among the groups' logits and leaves it out
@@ -228,7 +233,11 @@ __device__ __forceinline__ void route_octet(float* part, int n_el, int TT, int t
 
 // NRB: blocks of 16 gate rows (M + K <= 16 * NRB); NB: 16-token blocks per tile;
 // WAVES: waves splitting d; KP: top-k list length (>= k).
-template <typename T, int NRB, int NB, int WAVES, int KP>
+// MODE 0: the whole gate for a tile. MODE 1 (small batches): phase 1 over the d-range
+// blockIdx.y of p.nsplit, the waves' partials summed in order and written to p.ws
+// ([tile][split][row][token]). MODE 2: phase 1 replaced by the sum of a tile's split
+// partials from p.ws in split order, then phases 2 and 3.
+template <typename T, int NRB, int NB, int WAVES, int KP, int MODE>
 __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     constexpr int TT = kBlock * NB;
     static_assert(TT <= 64, "phase 3 gives each token one lane of wave 0");
@@ -269,6 +278,8 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
         s_gcand[kk] = static_cast<short>(n);
     }
 
+    constexpr int N_EL = NRB * 16 * TT;
+    if constexpr (MODE != 2) {
     // ---------------- phase 1: partial logits over this wave's share of d
     const T* xrow[NB];
 #pragma unroll
@@ -287,8 +298,9 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
         wrow[rb] = (rr < M ? static_cast<const T*>(p.w_local) + static_cast<size_t>(rr) * d
                            : static_cast<const T*>(p.w_global) + static_cast<size_t>(rr - M) * d) + g4 * EPC;
     }
-    const int kq = d / WAVES;
-    const int kbeg = wave * kq;
+    const int dsplit = MODE == 1 ? d / p.nsplit : d;  // d-range of this workgroup
+    const int kq = dsplit / WAVES;
+    const int kbeg = (MODE == 1 ? blockIdx.y * dsplit : 0) + wave * kq;
 
     f32x4 acc[NRB][NB];
 #pragma unroll
@@ -318,7 +330,6 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
                 for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = Mfma<T>::step(aw[u][rb], bx[u][nb], acc[rb][nb]);
     }
 
-    constexpr int N_EL = NRB * 16 * TT;
     float* mine = part + static_cast<size_t>(wave) * N_EL;
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
@@ -327,13 +338,38 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) mine[(rb * 16 + g4 * 4 + i) * TT + nb * kBlock + (lane & 15)] = acc[rb][nb][i];
     __syncthreads();
+    if constexpr (MODE == 1) {
+        float* out = p.ws + (static_cast<size_t>(blockIdx.x) * p.nsplit + blockIdx.y) * N_EL;
+        for (int i = threadIdx.x; i < N_EL; i += THREADS) {
+            float sum = part[i];
+#pragma unroll
+            for (int w = 1; w < WAVES; ++w) sum += part[w * N_EL + i];
+            out[i] = sum;
+        }
+        return;
+    }
+    }
 
+    if constexpr (MODE == 2) __syncthreads();  // the staged mask and biases
     // ---------------- phase 2: fixed-order sum of the partials, then the biases; local
     // logits off the candidate set become -inf (Eq. 4 applied before both softmaxes)
     for (int i = threadIdx.x; i < N_EL; i += THREADS) {
-        float sum = part[i];
+        float sum;
+        if constexpr (MODE == 2) {
+            // all the split partials of this logit loaded together, then added in split order
+            const float* src = p.ws + static_cast<size_t>(blockIdx.x) * p.nsplit * N_EL + i;
+            float v[kMaxSplit];
 #pragma unroll
-        for (int w = 1; w < WAVES; ++w) sum += part[w * N_EL + i];
+            for (int q = 0; q < kMaxSplit; ++q) v[q] = q < p.nsplit ? src[static_cast<size_t>(q) * N_EL] : 0.f;
+            sum = v[0];
+#pragma unroll
+            for (int q = 1; q < kMaxSplit; ++q)
+                if (q < p.nsplit) sum += v[q];
+        } else {
+            sum = part[i];
+#pragma unroll
+            for (int w = 1; w < WAVES; ++w) sum += part[w * N_EL + i];
+        }
         const int r = i / TT;
         if (r < M) sum = s_cand[r] ? sum + s_bl[r] : -INFINITY;
         else if (r < R) sum += s_bg[r - M];
@@ -365,7 +401,7 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     if (tl >= TT || t >= n_tokens) return;
     const float* lg = part;    // biased logits [row][TT], -inf off the candidate set
     float* gst = part + N_EL;  // this lane's stage-2 statistics: max at [kk][TT], sum at [K + kk][TT]
-                               // (wave 1's partials, free after phase 2; N_EL >= 2 K TT since M >= K)
+                               // (the second tile-sized slot of the LDS; N_EL >= 2 K TT since M >= K)
 
     // stage 2 statistics per group: max over its candidates and the sum of e^(l - max) in
     // expert order; stage 1 maximum over the groups that hold a candidate
@@ -419,7 +455,7 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     // least k candidates; the others leave the fusion (their statistics row becomes -inf,
     // after p_group has been formed over all of them).
     if (prune) {
-        float* taken = part + 2 * N_EL;  // this lane's flags [kk][TT] (wave 2's partials, free after phase 2)
+        float* taken = part + 2 * N_EL;  // this lane's flags [kk][TT] (the third slot)
         for (int kk = 0; kk < K; ++kk) taken[kk * TT + tl] = 0.f;
         int kept = 0, held = 0;
         for (int n = 0; n < K && (kept < top_groups || held < KT); ++n) {
@@ -549,30 +585,33 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     }
 }
 
-template <typename T, int NRB, int NB, int WAVES, int KP>
+template <typename T, int NRB, int NB, int WAVES, int KP, int MODE>
 hipError_t launch_cfg(const GateArgs& a, hipStream_t s) {
     constexpr int TT = kBlock * NB;
-    const size_t lds = static_cast<size_t>(WAVES) * NRB * 16 * TT * sizeof(float);
+    // MODE 2 keeps no per-wave partials: the logits, the routing statistics and the flags of
+    // top-G pruning take three tile-sized slots
+    const size_t lds = static_cast<size_t>(MODE == 2 ? 3 : WAVES) * NRB * 16 * TT * sizeof(float);
     static bool attr_set = false;  // once per instantiation: allow the partials beside the static arrays
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gate_kernel<T, NRB, NB, WAVES, KP>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gate_kernel<T, NRB, NB, WAVES, KP, MODE>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const int grid = (a.n_tokens + TT - 1) / TT;
-    ProfileScope prof("gate", s);
-    hipLaunchKernelGGL((gate_kernel<T, NRB, NB, WAVES, KP>), dim3(grid), dim3(64 * WAVES), lds, s, a);
+    ProfileScope prof(MODE == 1 ? "gate_split" : "gate", s);
+    hipLaunchKernelGGL((gate_kernel<T, NRB, NB, WAVES, KP, MODE>), dim3(grid, MODE == 1 ? a.nsplit : 1),
+                       dim3(64 * WAVES), lds, s, a);
     return hipGetLastError();
 }
 
 // KP > k lets the fast top-k see the (k+1)-th key; k = 16 runs the exact pass only
-template <typename T, int NRB, int NB, int WAVES>
+template <typename T, int NRB, int NB, int WAVES, int MODE = 0>
 hipError_t launch_kp(const GateArgs& a, hipStream_t s) {
-    if (a.top_k <= 1) return launch_cfg<T, NRB, NB, WAVES, 2>(a, s);
-    if (a.top_k <= 3) return launch_cfg<T, NRB, NB, WAVES, 4>(a, s);
-    if (a.top_k <= 7) return launch_cfg<T, NRB, NB, WAVES, 8>(a, s);
-    return launch_cfg<T, NRB, NB, WAVES, 16>(a, s);
+    if (a.top_k <= 1) return launch_cfg<T, NRB, NB, WAVES, 2, MODE>(a, s);
+    if (a.top_k <= 3) return launch_cfg<T, NRB, NB, WAVES, 4, MODE>(a, s);
+    if (a.top_k <= 7) return launch_cfg<T, NRB, NB, WAVES, 8, MODE>(a, s);
+    return launch_cfg<T, NRB, NB, WAVES, 16, MODE>(a, s);
 }
 
 // Tile and wave split:
@@ -585,6 +624,12 @@ template <typename T, int NRB>
 hipError_t launch_nrb(const GateArgs& a, hipStream_t s) {
     constexpr int SLICE = 4 * Elem<T>::kPerChunk;
     const int tiles16 = (a.n_tokens + kBlock - 1) / kBlock;
+    if (a.ws && a.nsplit > 1) {
+        // small batch with a workspace: d split over nsplit workgroups per tile, then routing
+        hipError_t e = launch_cfg<T, NRB, 1, kSplitWaves, 2, 1>(a, s);
+        if (e != hipSuccess) return e;
+        return launch_kp<T, NRB, 1, kRouteWaves, 2>(a, s);
+    }
     if constexpr (NRB <= 6)
         if (tiles16 < 256 && a.d % (16 * SLICE) == 0) return launch_kp<T, NRB, 1, 16>(a, s);
     if constexpr (NRB >= 3 && NRB <= 8)
@@ -614,6 +659,26 @@ hipError_t launch_gate_t(const GateArgs& a, hipStream_t s) {
 
 hipError_t launch_gate(DType dt, const GateArgs& a, hipStream_t s) {
     return dt == DType::BF16 ? launch_gate_t<bf16_t>(a, s) : launch_gate_t<float>(a, s);
+}
+
+int gate_split_count(DType dt, int n_tokens, int d) {
+    const int tiles16 = (n_tokens + kBlock - 1) / kBlock;
+    if (n_tokens <= 0 || tiles16 >= kSplitMaxTiles || d < kSplitMinD) return 1;
+    const int slice = 4 * (dt == DType::BF16 ? Elem<bf16_t>::kPerChunk : Elem<float>::kPerChunk);
+    // powers of two dividing the number of kSplitWaves-wave slices of d, up to about
+    // 256 workgroups and kMaxSplit splits
+    int n = 1;
+    while (n < kMaxSplit && tiles16 * n * 2 <= 256 && d % (2 * n * kSplitWaves * slice) == 0) n *= 2;
+    return n;
+}
+
+size_t gate_split_bytes(DType dt, int n_tokens, int d, int gate_rows) {
+    const int n = gate_split_count(dt, n_tokens, d);
+    if (n <= 1) return 0;
+    const int nrb = (gate_rows + 15) / 16;
+    const int padded = nrb <= 6 ? nrb : (nrb <= 8 ? 8 : (nrb <= 12 ? 12 : (nrb <= 16 ? 16 : kMaxRowBlocks)));
+    const size_t tiles16 = (static_cast<size_t>(n_tokens) + kBlock - 1) / kBlock;
+    return tiles16 * n * static_cast<size_t>(padded) * 16 * kBlock * sizeof(float);
 }
 
 }  // namespace ec2moe

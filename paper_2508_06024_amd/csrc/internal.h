@@ -28,11 +28,17 @@ struct GateArgs {
     int n_tokens, d, n_experts, n_groups, top_k;
     bool renormalize;
     uint64_t mask[4];
+    float* ws;         // split-d partials of small batches, or null
+    int nsplit;        // d-splits per tile (> 1 only with ws)
     int top_groups;    // > 0: keep the top_groups groups of largest p_group (more while < k candidates)
     int equal_groups;  // goff[k] = k * M / K
     int32_t goff[161]; // group k = experts goff[k] .. goff[k + 1] - 1 (K <= 160)
 };
 hipError_t launch_gate(DType dt, const GateArgs& a, hipStream_t s);
+// d-splits per 16-token tile for a small batch (1: no split) and the workspace bytes of the
+// split partials (0 when there is no split)
+int gate_split_count(DType dt, int n_tokens, int d);
+size_t gate_split_bytes(DType dt, int n_tokens, int d, int gate_rows);
 
 // ---------------------------------------------------------------- permutation
 // Work split of the permutation kernels: assignments are processed in chunks of

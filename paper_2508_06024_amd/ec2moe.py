@@ -45,7 +45,8 @@ class CodecDesc(ctypes.Structure):
 
 
 class GateOpts(ctypes.Structure):
-    _fields_ = [("top_groups", ctypes.c_int32), ("group_sizes", ctypes.POINTER(ctypes.c_int32))]
+    _fields_ = [("top_groups", ctypes.c_int32), ("group_sizes", ctypes.POINTER(ctypes.c_int32)),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
 
 
 class DeviceState(ctypes.Structure):
@@ -81,6 +82,7 @@ _SIGS = {
     "ec2moe_group_gate": [ctypes.POINTER(MoeDesc), ctypes.POINTER(ctypes.c_uint64), _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "ec2moe_group_gate_ex": [ctypes.POINTER(MoeDesc), ctypes.POINTER(GateOpts), ctypes.POINTER(ctypes.c_uint64),
                              _P, _P, _P, _P, _P, _P, _P, _P, _P],
+    "ec2moe_gate_workspace_size": [ctypes.POINTER(MoeDesc), ctypes.POINTER(ctypes.c_size_t)],
     "ec2moe_moe_workspace_size": [ctypes.POINTER(MoeDesc), ctypes.POINTER(ctypes.c_size_t)],
     "ec2moe_permute": [ctypes.POINTER(MoeDesc), _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
     "ec2moe_expert_ffn": [ctypes.POINTER(MoeDesc), _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
@@ -169,11 +171,22 @@ def group_gate(desc: MoeDesc, mask_words, x, w_global, b_global, w_local, b_loca
                                   _ptr(topk_w), _ptr(probs), _stream()))
 
 
-def gate_opts(top_groups: int = 0, group_sizes: Optional[Sequence[int]] = None) -> GateOpts:
+def gate_opts(top_groups: int = 0, group_sizes: Optional[Sequence[int]] = None, workspace=None) -> GateOpts:
+    """Options of group_gate_ex; workspace: a device tensor of gate_workspace_size bytes
+    (small batches split d over more workgroups) or None."""
     sizes = None if group_sizes is None else (ctypes.c_int32 * len(group_sizes))(*[int(m) for m in group_sizes])
-    opts = GateOpts(int(top_groups), ctypes.cast(sizes, ctypes.POINTER(ctypes.c_int32)) if sizes is not None else None)
-    opts._sizes = sizes  # keeps the array alive with the options
+    opts = GateOpts(int(top_groups), ctypes.cast(sizes, ctypes.POINTER(ctypes.c_int32)) if sizes is not None else None,
+                    None if workspace is None else workspace.data_ptr(),
+                    0 if workspace is None else workspace.numel() * workspace.element_size())
+    opts._sizes = sizes  # keeps the array and the workspace alive with the options
+    opts._ws = workspace
     return opts
+
+
+def gate_workspace_size(desc: MoeDesc) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.ec2moe_gate_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
 
 
 def group_gate_ex(desc: MoeDesc, opts: Optional[GateOpts], mask_words, x, w_global, b_global, w_local, b_local,
@@ -186,7 +199,8 @@ def group_gate_ex(desc: MoeDesc, opts: Optional[GateOpts], mask_words, x, w_glob
 
 
 def gate(x, mask_words, w_global, b_global, w_local, b_local, n_groups, top_k, renormalize=True,
-         with_probs=False, top_groups=0, group_sizes=None):
+         with_probs=False, top_groups=0, group_sizes=None, split=False):
+    """Group gate of x [T][d]; split: pass a gate workspace (small batches then split d)."""
     T, d = x.shape
     M = w_local.shape[0]
     dt = x.dtype
@@ -200,8 +214,11 @@ def gate(x, mask_words, w_global, b_global, w_local, b_local, n_groups, top_k, r
     idx = torch.empty((T, top_k), dtype=torch.int32, device=x.device)
     w = torch.empty((T, top_k), dtype=torch.float32, device=x.device)
     probs = torch.empty((T, M), dtype=torch.float32, device=x.device) if with_probs else None
-    if top_groups or group_sizes is not None:
-        group_gate_ex(desc, gate_opts(top_groups, group_sizes), mask_words, x, w_global, b_global, w_local,
+    if top_groups or group_sizes is not None or split:
+        ws = None
+        if split:
+            ws = workspace(gate_workspace_size(desc), x.device)
+        group_gate_ex(desc, gate_opts(top_groups, group_sizes, ws), mask_words, x, w_global, b_global, w_local,
                       b_local, idx, w, probs)
     else:
         group_gate(desc, mask_words, x, w_global, b_global, w_local, b_local, idx, w, probs)

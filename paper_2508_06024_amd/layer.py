@@ -35,8 +35,10 @@ class Ec2moeLayer:
         if tuple(w_gate_up.shape) != (M, E.w_in_rows(H, activation), d):
             raise ValueError(f"w_gate_up has shape {tuple(w_gate_up.shape)} for {activation} experts of width {H}")
         self.moe_desc = E.moe_desc(T, M, n_groups, d, H, top_k, dt, renormalize, activation)
-        # gate options (top-G groups, unequal groups): None for the plain gate call
-        self.gate_opts = E.gate_opts(top_groups, group_sizes) if top_groups or group_sizes is not None else None
+        # gate options: top-G groups, unequal groups and the gate workspace that lets a small
+        # batch split d over more workgroups
+        self.gate_ws = E.workspace(E.gate_workspace_size(self.moe_desc), dev)
+        self.gate_opts = E.gate_opts(top_groups, group_sizes, self.gate_ws)
         if T % codec_slices or u.shape[0] != T // codec_slices:
             raise ValueError(f"u has {u.shape[0]} rows for {codec_slices} slices of {T} tokens")
         self.codec_desc = E.codec_desc(T // codec_slices, d, u.shape[1], v.shape[1], dt, codec_slices)
@@ -56,12 +58,8 @@ class Ec2moeLayer:
             self.mask = list(mask_words)
 
     def step(self):
-        if self.gate_opts is None:
-            E.group_gate(self.moe_desc, self.mask, self.x, self.w_global, self.b_global, self.w_local,
-                         self.b_local, self.topk_idx, self.topk_w)
-        else:
-            E.group_gate_ex(self.moe_desc, self.gate_opts, self.mask, self.x, self.w_global, self.b_global,
-                            self.w_local, self.b_local, self.topk_idx, self.topk_w)
+        E.group_gate_ex(self.moe_desc, self.gate_opts, self.mask, self.x, self.w_global, self.b_global,
+                        self.w_local, self.b_local, self.topk_idx, self.topk_w)
         E.lowrank_encode_into(self.codec_desc, self.x, self.u, self.v, self.z, self.codec_ws)
         E.lowrank_decode_into(self.codec_desc, self.z, self.u_hat, self.v_hat, self.x_hat, self.codec_ws)
         E.moe_forward_into(self.moe_desc, self.x_hat, self.topk_idx, self.topk_w, self.w_gate_up,

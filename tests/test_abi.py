@@ -106,6 +106,40 @@ def test_gate_options_validation():
                                        None, None, None, None, None) == OK
 
 
+def _gate_ws_size(desc):
+    n = ctypes.c_size_t(0)
+    st = E._lib.ec2moe_gate_workspace_size(ctypes.byref(desc), ctypes.byref(n))
+    return st, n.value
+
+
+def test_gate_workspace_size():
+    """Small batches (under 64 tiles of 16 tokens) with d >= 2048 get d split over up to 32
+    workgroups per tile, about 256 workgroups in all; the partials are float32
+    [tile][split][16 * padded row blocks][16]."""
+    dec = dict(n_tokens=32, n_experts=64, n_groups=8, d_model=4096, top_k=8)
+    assert _gate_ws_size(_desc(**dec)) == (OK, 2 * 32 * 80 * 16 * 4)
+    assert _gate_ws_size(_desc(**dict(dec, dtype=E.F32))) == (OK, 2 * 32 * 80 * 16 * 4)
+    assert _gate_ws_size(_desc(**dict(dec, n_tokens=33))) == (OK, 3 * 32 * 80 * 16 * 4)
+    assert _gate_ws_size(_desc(**dict(dec, n_tokens=160))) == (OK, 10 * 16 * 80 * 16 * 4)  # 10 tiles: 16 splits
+    assert _gate_ws_size(_desc(**dict(dec, n_tokens=1024))) == (OK, 0)   # 64 tiles: unsplit
+    assert _gate_ws_size(_desc(**dict(dec, n_tokens=0))) == (OK, 0)
+    assert _gate_ws_size(_desc(n_tokens=64, d_model=1024)) == (OK, 0)   # narrow gates run unsplit
+    # 320 gate rows pad to 20 blocks of 16; 2048 = 16 splits of 128
+    assert _gate_ws_size(_desc(n_tokens=53, n_experts=256, n_groups=64, d_model=2048, top_k=16)) == \
+        (OK, 4 * 16 * 320 * 16 * 4)
+
+
+def test_gate_workspace_validation():
+    desc = _desc(n_tokens=32, n_experts=64, n_groups=8, d_model=4096, top_k=8)
+    need = _gate_ws_size(desc)[1]
+    arr = E.mask_array([(1 << 64) - 1])
+    p = ctypes.c_void_p(1 << 20)
+    call = lambda opts: E._lib.ec2moe_group_gate_ex(ctypes.byref(desc), ctypes.byref(opts), arr, p, p, None, p,
+                                                    None, p, p, None, None)
+    assert call(E.GateOpts(0, None, 1 << 20, need - 1)) == WS_SMALL and "gate workspace" in E.last_error()
+    assert call(E.GateOpts(0, None, (1 << 20) + 8, need)) == INVALID and "aligned" in E.last_error()
+
+
 def test_workspace_size_grows_with_tokens():
     _, a = _ws_size(_desc(n_tokens=64))
     _, b = _ws_size(_desc(n_tokens=4096))

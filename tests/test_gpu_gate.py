@@ -12,12 +12,12 @@ from tests.gpu_common import NEAR_TIE, TOL_F32, assert_close, check_routing, dow
 pytestmark = pytest.mark.gpu
 
 
-def run_gate(inp, with_probs=True, renormalize=True, top_k=None):
+def run_gate(inp, with_probs=True, renormalize=True, top_k=None, split=False):
     cfg = inp.cfg
     k = top_k or cfg.top_k
     return E.gate(up(inp.x, cfg.dtype), inp.mask, up(inp.w_global, cfg.dtype), up_f32(inp.b_global),
                   up(inp.w_local, cfg.dtype), up_f32(inp.b_local), cfg.n_groups, k, renormalize,
-                  with_probs=with_probs)
+                  with_probs=with_probs, split=split)
 
 
 def oracle_gate(inp, renormalize=True, top_k=None):
@@ -27,10 +27,10 @@ def oracle_gate(inp, renormalize=True, top_k=None):
                         cfg.n_groups, top_k or cfg.top_k, renormalize)
 
 
-def compare(inp, renormalize=True, top_k=None, strict=False):
+def compare(inp, renormalize=True, top_k=None, strict=False, split=False):
     cfg = inp.cfg
     k = top_k or cfg.top_k
-    idx, w, probs = run_gate(inp, True, renormalize, k)
+    idx, w, probs = run_gate(inp, True, renormalize, k, split)
     torch.cuda.synchronize()
     ridx, rw, g = oracle_gate(inp, renormalize, k)
     cand = W.mask_members(inp.mask, cfg.n_experts)
@@ -50,6 +50,64 @@ def test_gate_matches_oracle_at_full_size(name, call):
     inp = W.gen_layer(cfg, call_seed=call, experts=False)
     n_cert = compare(inp)
     say(f"  certified near-ties: {n_cert}")
+
+
+def _split_count(cfg, k=None):
+    dt = E.BF16 if cfg.dtype == W.BF16 else E.F32
+    desc = E.moe_desc(cfg.n_tokens, cfg.n_experts, cfg.n_groups, cfg.d_model, 128, k or cfg.top_k, dt)
+    return E.gate_workspace_size(desc)
+
+
+SPLIT_CASES = [("decode", 4, {}), ("decode", 1003, {"n_tokens": 37}), ("tiny", None, {"d_model": 2048}),
+               ("tiny", None, {"d_model": 2048, "n_tokens": 1, "r_h": 1}), ("small", None, {"n_tokens": 100, "d_model": 2048, "r_h": 16}),
+               ("finegrained", None, {"n_tokens": 300}), ("mixtral", None, {"n_tokens": 200, "r_h": 64})]
+
+
+@pytest.mark.parametrize("name,call,kw", SPLIT_CASES, ids=[f"{n}-{c}-{i}" for i, (n, c, _) in enumerate(SPLIT_CASES)])
+def test_gate_split_d_matches_oracle(name, call, kw):
+    """Small batches with a gate workspace: d split over many workgroups, the partials
+    summed in a fixed order by the routing kernel (float32 and bfloat16, ragged and single
+    tokens)."""
+    cfg = W.CONFIGS[name].scaled(**kw)
+    assert _split_count(cfg) > 0, "the case must take the split path"
+    say(f"gate split {name} call {call}: T={cfg.n_tokens} d={cfg.d_model} M={cfg.n_experts} k={cfg.top_k}")
+    inp = W.gen_layer(cfg, call_seed=call, experts=False)
+    say(f"  certified near-ties: {compare(inp, split=True)}")
+    # the split sums in another order: same routing as the unsplit gate up to near-ties
+    a = run_gate(inp, split=True)
+    b = run_gate(inp, split=True)
+    for u, v in zip(a, b):
+        assert torch.equal(u, v), "the split gate must be deterministic"
+
+
+def test_gate_split_exact_ties_and_options():
+    """Integer-valued inputs stay bit-exact with the split; unequal groups, top-G groups and
+    the 320-row maximum gate take the split as well."""
+    inp = _exact_inputs(37, 2048, 64, 8, 8, seed=101)
+    assert _split_count(inp.cfg) > 0
+    _, _, g = oracle_gate(inp)
+    for t in range(37):  # precondition: every near-tie of the oracle is an exact tie
+        gs = np.sort(g[t])[::-1][:9]
+        gaps = (gs[:-1] - gs[1:]) / gs[:-1]
+        assert np.all((gaps == 0) | (gaps > NEAR_TIE)), "seeded input has a non-structural near-tie"
+    assert compare(inp, strict=True, split=True) == 0
+    T, d, M, K, k, keep, sizes, G = 257, 2048, 40, 6, 4, 30, (1, 9, 10, 5, 12, 3), 2
+    x, wg, bg, wl, bl, mask, members = _gate_inputs(T, d, M, K, seed=T + M + G, keep=keep)
+    args = (up(x, W.BF16), mask, up(wg, W.BF16), up_f32(bg), up(wl, W.BF16), up_f32(bl), K, k)
+    r_split = E.gate(*args, with_probs=True, top_groups=G, group_sizes=sizes, split=True)
+    r_plain = E.gate(*args, with_probs=True, top_groups=G, group_sizes=sizes)
+    torch.cuda.synchronize()
+    f = lambda a: W.to_f64(a, W.BF16)
+    ridx, rw, g = O.group_gate(f(x), f(wg), bg, f(wl), bl, mask, K, k, group_sizes=sizes, top_groups=G)
+    amb = _group_cut_near_ties(x, wg, bg, members, M, K, k, sizes, G)
+    ok = np.setdiff1d(np.arange(T), amb)
+    for idx, w, probs in (r_split, r_plain):
+        check_routing(down(idx)[ok], down(w)[ok], ridx[ok], rw[ok], g[ok], members, k)
+        assert_close(down(probs)[ok], g[ok], TOL_F32, "probs")
+    cfg = W.LayerConfig("maxgate", W.BF16, 53, 2048, 256, 64, 128, 16, 16, 16, seed=11, mask="random",
+                        n_keep=200, x_dist="rms", gate_std=0.05)
+    assert _split_count(cfg) > 0
+    compare(W.gen_layer(cfg, experts=False), split=True)
 
 
 def test_gate_without_renormalisation_and_top1():
