@@ -19,7 +19,9 @@
  *     launched and no output is written; ec2moe_last_error() returns the detail
  *     (thread-local). No C++ exception crosses this interface.
  *   - Supported shapes: d_model and ffn_hidden multiples of 128, 1 <= top_k <= 16,
- *     n_experts <= 256, n_experts + n_groups <= 320, n_groups dividing n_experts;
+ *     n_experts <= 256, n_experts + n_groups <= 320, n_groups <= n_experts (and
+ *     dividing it for the gate without group sizes; the calls after the gate never
+ *     read the group structure);
  *     codec ranks r_h, r_w multiples of 16 and at most 256, w a multiple of 128.
  *     Others return EC2MOE_ERR_UNSUPPORTED. n_tokens == 0 is valid and launches nothing.
  */

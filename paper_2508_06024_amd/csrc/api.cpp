@@ -66,7 +66,8 @@ constexpr int kMaxExperts = 256;
 constexpr int kMaxGateRows = 320;
 constexpr int kMaxTopK = 16;
 
-// equal_groups: K must divide M (every entry point but ec2moe_group_gate_ex with group sizes)
+// equal_groups: K must divide M (the gate without group sizes; the entry points after the
+// gate never read the group structure)
 ec2moe_status check_moe_desc(const ec2moe_moe_desc* d, bool equal_groups = true) {
     REQUIRE(d != nullptr, EC2MOE_ERR_INVALID_ARGUMENT, "desc is NULL");
     REQUIRE(d->dtype == EC2MOE_F32 || d->dtype == EC2MOE_BF16, EC2MOE_ERR_INVALID_ARGUMENT, "unknown dtype %d",
@@ -356,7 +357,7 @@ ec2moe_status ec2moe_group_gate(const ec2moe_moe_desc* desc, const uint64_t* can
 }
 
 ec2moe_status ec2moe_moe_workspace_size(const ec2moe_moe_desc* desc, size_t* bytes) {
-    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    if (ec2moe_status st = check_moe_desc(desc, false); st != EC2MOE_OK) return st;
     REQUIRE_PTR(bytes);
     *bytes = moe_ws(desc).total;
     return ok();
@@ -365,7 +366,7 @@ ec2moe_status ec2moe_moe_workspace_size(const ec2moe_moe_desc* desc, size_t* byt
 ec2moe_status ec2moe_permute(const ec2moe_moe_desc* desc, const int32_t* topk_idx, const void* x,
                              int32_t* seg_offsets, int32_t* perm_src, int32_t* inv_perm, void* x_perm, void* ws,
                              size_t ws_bytes, hipStream_t stream) {
-    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    if (ec2moe_status st = check_moe_desc(desc, false); st != EC2MOE_OK) return st;
     const MoeWs w = moe_ws(desc);
     if (ec2moe_status st = check_ws(ws, ws_bytes, w.total); st != EC2MOE_OK) return st;
     REQUIRE_PTR(seg_offsets);
@@ -415,7 +416,7 @@ hipError_t run_experts(const ec2moe_moe_desc* desc, const void* x, const int32_t
 ec2moe_status ec2moe_expert_ffn(const ec2moe_moe_desc* desc, const void* x, const int32_t* seg_offsets,
                                 const int32_t* perm_src, const void* w_gate_up, const void* w_down, void* act,
                                 void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
-    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    if (ec2moe_status st = check_moe_desc(desc, false); st != EC2MOE_OK) return st;
     const MoeWs w = moe_ws(desc);
     if (ec2moe_status st = check_ws(ws, ws_bytes, w.total); st != EC2MOE_OK) return st;
     if (desc->n_tokens == 0) return ok();
@@ -431,7 +432,7 @@ ec2moe_status ec2moe_expert_ffn(const ec2moe_moe_desc* desc, const void* x, cons
 
 ec2moe_status ec2moe_combine(const ec2moe_moe_desc* desc, const void* y_perm, const int32_t* inv_perm,
                              const float* topk_w, void* y, hipStream_t stream) {
-    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    if (ec2moe_status st = check_moe_desc(desc, false); st != EC2MOE_OK) return st;
     if (desc->n_tokens == 0) return ok();
     REQUIRE_PTR(y_perm); REQUIRE_PTR(inv_perm); REQUIRE_PTR(topk_w); REQUIRE_PTR(y);
     REQUIRE_ALIGNED(y_perm); REQUIRE_ALIGNED(y);
@@ -443,7 +444,7 @@ ec2moe_status ec2moe_combine(const ec2moe_moe_desc* desc, const void* y_perm, co
 ec2moe_status ec2moe_moe_forward(const ec2moe_moe_desc* desc, const void* x, const int32_t* topk_idx,
                                  const float* topk_w, const void* w_gate_up, const void* w_down, void* y, void* ws,
                                  size_t ws_bytes, hipStream_t stream) {
-    if (ec2moe_status st = check_moe_desc(desc); st != EC2MOE_OK) return st;
+    if (ec2moe_status st = check_moe_desc(desc, false); st != EC2MOE_OK) return st;
     const MoeWs w = moe_ws(desc);
     if (ec2moe_status st = check_ws(ws, ws_bytes, w.total); st != EC2MOE_OK) return st;
     if (desc->n_tokens == 0) return ok();

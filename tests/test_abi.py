@@ -54,7 +54,8 @@ def _ws_size(desc):
 
 
 @pytest.mark.parametrize("kw,status", [
-    (dict(n_groups=3), INVALID),            # K does not divide M
+    (dict(n_groups=3), OK),                 # K need not divide M after the gate
+    (dict(n_groups=9), INVALID),            # K > M
     (dict(top_k=9), INVALID),               # k > M
     (dict(n_tokens=-1), INVALID),
     (dict(d_model=0), INVALID),
@@ -152,6 +153,10 @@ def _gate(desc, words, ptr=1 << 20):
     arr = E.mask_array(words)
     p = ctypes.c_void_p(ptr)
     return E._lib.ec2moe_group_gate(ctypes.byref(desc), arr, p, p, None, p, None, p, p, None, None)
+
+
+def test_plain_gate_needs_equal_groups():
+    assert _gate(_desc(n_groups=3), [0xFF]) == INVALID and "divide" in E.last_error()
 
 
 def test_gate_rejects_too_few_candidates_before_launch():

@@ -11,23 +11,23 @@ from tests.gpu_common import assert_close, check_routing, down, say, tol, up, up
 pytestmark = pytest.mark.gpu
 
 
-def build(inp):
+def build(inp, top_groups=0, group_sizes=None):
     cfg = inp.cfg
     dt = cfg.dtype
     return Ec2moeLayer(up(inp.x, dt), inp.mask, up(inp.w_global, dt), up_f32(inp.b_global), up(inp.w_local, dt),
                        up_f32(inp.b_local), up(inp.w_gate_up, dt), up(inp.w_down, dt), up(inp.u, dt),
                        up(inp.v, dt), n_groups=cfg.n_groups, top_k=cfg.top_k, activation=cfg.activation,
-                       codec_slices=cfg.codec_slices)
+                       codec_slices=cfg.codec_slices, top_groups=top_groups, group_sizes=group_sizes)
 
 
-def oracle_sampled(inp, toks):
+def oracle_sampled(inp, toks, top_groups=0, group_sizes=None):
     """Oracle layer outputs of the sampled tokens: the gate and the experts act per token;
     the codec's Z couples all tokens of a slice and is computed in full, slice by slice."""
     cfg = inp.cfg
     f = inp.f64
     x, u, v = f("x"), f("u"), f("v")
     idx, w, g = O.group_gate(x[toks], f("w_global"), inp.b_global, f("w_local"), inp.b_local, inp.mask,
-                             cfg.n_groups, cfg.top_k)
+                             cfg.n_groups, cfg.top_k, group_sizes=group_sizes, top_groups=top_groups)
     h = cfg.codec_h
     z = np.stack([O.lowrank_encode(x[s * h:(s + 1) * h], u, v) for s in range(cfg.codec_slices)])
     xh = np.stack([O.lowrank_decode(z[t // h], u[[t % h]], v)[0] for t in toks])
@@ -71,3 +71,31 @@ def test_layer_step_matches_oracle(name, call, sample):
     y1 = lay.y.clone()
     lay.step()
     assert torch.equal(lay.y, y1)
+
+
+def test_layer_step_with_unequal_groups_and_top_groups():
+    """The whole step with groups of unequal sizes (K does not divide M) and group-focused
+    evaluation (the top 2 groups per token): the calls after the gate take any K <= M."""
+    from tests.test_gpu_gate import _group_cut_near_ties
+    cfg = W.LayerConfig("unequal", W.BF16, 300, 1024, 24, 5, 256, 3, 32, 32, seed=17, mask="random", n_keep=18,
+                        x_dist="rms", gate_std=0.05)
+    sizes, G = (2, 7, 3, 8, 4), 2
+    say(f"layer unequal groups {sizes} top_groups {G}")
+    inp = W.gen_layer(cfg)
+    lay = build(inp, top_groups=G, group_sizes=sizes)
+    lay.step()
+    torch.cuda.synchronize()
+    toks = np.arange(cfg.n_tokens)
+    idx, w, g, z, xh, y = oracle_sampled(inp, toks, top_groups=G, group_sizes=sizes)
+    members = W.mask_members(inp.mask, cfg.n_experts)
+    amb = _group_cut_near_ties(inp.x, inp.w_global, inp.b_global, members, cfg.n_experts, cfg.n_groups, cfg.top_k,
+                               sizes, G)
+    assert amb.size <= 0.05 * cfg.n_tokens
+    ok = np.setdiff1d(toks, amb)
+    gidx, gw = down(lay.topk_idx), down(lay.topk_w)
+    check_routing(gidx[ok], gw[ok], idx[ok], w[ok], g[ok], members, cfg.top_k)
+    assert_close(down(lay.z).reshape(z.shape), z, 1e-5, "Z")
+    same = ~(gidx != idx).any(axis=1)
+    same[amb] = False
+    e = assert_close(down(lay.y)[same], y[same], tol(cfg.dtype), "y")
+    say(f"  y rel err {e:.2e}; tokens with near-tied groups at the cut {amb.size}")
