@@ -89,10 +89,16 @@ def cpu_baseline(inp, cfg, target_s, top_groups=0):
     S = int(min(T, max(S0, S0 * target_s / max(t0, 1e-6))))
     S = max(S0, (S // quantum) * quantum) if S < T else T
     t = run(S) if S != S0 else t0
-    return {"value": S / t, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
+    # the whole workload finishes under the target: repeat it until the target is reached
+    reps = 1
+    while S == T and t < target_s:
+        t += run(S)
+        reps += 1
+    return {"value": S * reps / t, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
             "sample": f"oracle step (gate, encode, decode, experts, combine) on the first {S} of {T} tokens "
                       f"of the same inputs" + (", U restricted to those rows" if c == 1 else
-                                                f", {S // h} of {c} codec slices") + f", float64, {t:.1f} s",
+                                                f", {S // h} of {c} codec slices") +
+                      (f", {reps} runs" if reps > 1 else "") + f", float64, {t:.1f} s",
             "seconds": round(t, 2)}
 
 
