@@ -181,7 +181,10 @@ __device__ __forceinline__ SplitPlan split_plan(int total, int slots, int max_sp
     sp.tail = total - sp.full;
     int S = 1;
     if (sp.tail > 0 && max_split > 1)
-        S = std::max(1, std::min(std::min(std::min(max_split, kMaxSplitChunks), slots / sp.tail), nk / 2));
+        // at most one split workgroup per CU: more (two 128x128 tiles fit a CU) only adds
+        // partial-sum traffic (the fine-grained encoder's X V: 18.0 against 21.7 us)
+        S = std::max(1, std::min(std::min(std::min(max_split, kMaxSplitChunks), std::min(slots, 256) / sp.tail),
+                                 nk / 2));
     sp.S = S;
     sp.chunk_slabs = ((nk + S - 1) / S + 1) / 2 * 2;
     return sp;
