@@ -6,16 +6,21 @@
 // token rows the B operand, and each of the WAVES waves contracts its share of d (all
 // its loads of a batch issued before the first MFMA). Phase 2 adds the partial sums in a
 // fixed order (deterministic) and the biases, and sets the local logits of non-candidates
-// to -inf. Phase 3 gives every token one lane of the first wave: the lane reads a group's
-// logits from LDS in one batch (its own column, no cross-lane traffic) and computes the
-// masked in-group softmax statistics (stage 2), the masked group softmax (stage 1), the
-// product g_i = p_group^(k) * p_local,i^(k) and a running top-k in registers (ties to the
-// lower expert index), then renormalises the selected weights. The other waves leave
-// after phase 2.
+// to -inf. Phase 3 routes the tokens from the logits in LDS:
+//   * regular shapes (M a multiple of 8 up to 64, each lane's M/8 experts inside one
+//     group): 8 lanes per token, segmented shuffles for the two softmaxes (stage 2 inside
+//     the groups, stage 1 over the groups), per-lane top-k lists of packed keys merged
+//     bitonically, with an exact re-selection for keys that collide after truncation;
+//   * other shapes (unequal groups, more than 64 experts, k = 16): one lane per token,
+//     the group statistics in LDS and a running top-k in registers.
+// Either way ties go to the lower expert index and the selected weights are renormalised
+// on request.
 //
-// Tiles of two 16-token blocks (NB = 2) halve the gate-weight reads per
-// token; they pay off when the gate has many rows and there are enough tokens to give
-// every CU a tile.
+// Tiles of two 16-token blocks (NB = 2) halve the gate-weight reads per token; they pay
+// off when the gate has many rows and there are enough tokens to give every CU a tile.
+// Small batches with a caller-given workspace split d over several workgroups per tile
+// (MODE 1, partial logits to the workspace) and route in a second launch (MODE 2, the
+// partials summed in split order in place of phase 1).
 #include "device_common.h"
 #include "internal.h"
 
