@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral", choices=ALL_ORDER)
     ap.add_argument("--rotate", type=int, default=4, help="distinct copies of X cycled through the steps")
+    ap.add_argument("--overlap", action="store_true",
+                    help="run the routing (gate, permutation) on a second stream, overlapping the codec")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of HIP graphs of the step (one per input copy) instead of eager launches")
     ap.add_argument("--top-groups", type=int, default=0,
@@ -141,7 +143,7 @@ def main():
     layer = Ec2moeLayer(xs[0], masks[0], up(inp.w_global), f32(inp.b_global), up(inp.w_local), f32(inp.b_local),
                         up(inp.w_gate_up), up(inp.w_down), up(inp.u), up(inp.v),
                         n_groups=cfg.n_groups, top_k=cfg.top_k, activation=cfg.activation,
-                        codec_slices=cfg.codec_slices, top_groups=args.top_groups)
+                        codec_slices=cfg.codec_slices, top_groups=args.top_groups, overlap=args.overlap)
 
     def step(i):
         layer.set_input(xs[i % len(xs)], masks[i % len(masks)])
@@ -322,7 +324,8 @@ def main():
         "kernels": kernels,
         "kernels_pass": f"separate pass of {prof_steps} steps with HIP events around every kernel",
         "launch": ("HIP graph replays of the step (the dominant kernel's time from an eager pass)"
-                   if args.graph and not per_call else "eager launches"),
+                   if args.graph and not per_call else "eager launches")
+                  + (", routing on a second stream" if args.overlap else ""),
         "cpu_baseline": cpu,
         "planner": planner,
     }

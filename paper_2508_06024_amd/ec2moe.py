@@ -295,6 +295,25 @@ def combine(y_perm, inv_perm, topk_w):
     return y
 
 
+def permute_into(desc: MoeDesc, topk_idx, seg_offsets, perm_src, inv_perm, ws, x=None, x_perm=None):
+    """Raw call with caller-owned outputs and workspace (no allocation)."""
+    _check(_lib.ec2moe_permute(ctypes.byref(desc), _ptr(topk_idx), _ptr(x), _ptr(seg_offsets), _ptr(perm_src),
+                               _ptr(inv_perm), _ptr(x_perm), _ptr(ws), ws.numel(), _stream()))
+
+
+def expert_ffn_into(desc: MoeDesc, x, seg_offsets, perm_src, w_gate_up, w_down, y_perm, ws, act=None):
+    """Raw call with caller-owned outputs and workspace (no allocation)."""
+    _check(_lib.ec2moe_expert_ffn(ctypes.byref(desc), _ptr(x), _ptr(seg_offsets), _ptr(perm_src),
+                                  _ptr(w_gate_up), _ptr(w_down), _ptr(act), _ptr(y_perm), _ptr(ws),
+                                  ws.numel(), _stream()))
+
+
+def combine_into(desc: MoeDesc, y_perm, inv_perm, topk_w, y):
+    """Raw call with a caller-owned output."""
+    _check(_lib.ec2moe_combine(ctypes.byref(desc), _ptr(y_perm), _ptr(inv_perm), _ptr(topk_w), _ptr(y),
+                               _stream()))
+
+
 def moe_forward_into(desc: MoeDesc, x, topk_idx, topk_w, w_gate_up, w_down, y, ws):
     """Raw call with caller-owned output and workspace (no allocation)."""
     _check(_lib.ec2moe_moe_forward(ctypes.byref(desc), _ptr(x), _ptr(topk_idx), _ptr(topk_w),

@@ -13,21 +13,22 @@ from tests.gpu_common import say, up, up_f32
 pytestmark = pytest.mark.gpu
 
 
-def _layer(cfg):
+def _layer(cfg, overlap=False):
     inp = W.gen_layer(cfg)
     dt = cfg.dtype
     lay = Ec2moeLayer(up(inp.x, dt), inp.mask, up(inp.w_global, dt), up_f32(inp.b_global), up(inp.w_local, dt),
                       up_f32(inp.b_local), up(inp.w_gate_up, dt), up(inp.w_down, dt), up(inp.u, dt), up(inp.v, dt),
                       n_groups=cfg.n_groups, top_k=cfg.top_k, activation=cfg.activation,
-                      codec_slices=cfg.codec_slices)
+                      codec_slices=cfg.codec_slices, overlap=overlap)
     return inp, lay
 
 
-@pytest.mark.parametrize("name", ["small", "switch16"])
-def test_graph_replays_match_eager(name):
+@pytest.mark.parametrize("name,overlap", [("small", False), ("switch16", False), ("small", True)])
+def test_graph_replays_match_eager(name, overlap):
+    """overlap=True captures the routing stream's fork and join as graph dependencies."""
     cfg = W.CONFIGS[name]
-    say(f"graph capture {name}")
-    inp, lay = _layer(cfg)
+    say(f"graph capture {name} overlap={overlap}")
+    inp, lay = _layer(cfg, overlap)
     x2 = up(W.gen_call(cfg.scaled(seed=cfg.seed + 1))[0], cfg.dtype)
     x1 = lay.x
     # eager reference for both inputs

@@ -99,3 +99,31 @@ def test_layer_step_with_unequal_groups_and_top_groups():
     same[amb] = False
     e = assert_close(down(lay.y)[same], y[same], tol(cfg.dtype), "y")
     say(f"  y rel err {e:.2e}; tokens with near-tied groups at the cut {amb.size}")
+
+
+@pytest.mark.parametrize("name", ["small", "decode"])
+def test_overlapped_routing_matches_one_stream_order(name):
+    """The routing on its own stream (the default) gives the one-stream order's bits, step
+    after step, with the input and the candidate mask changing between steps."""
+    cfg = W.CONFIGS[name]
+    say(f"overlapped routing {name}")
+    inp = W.gen_layer(cfg, call_seed=5 if cfg.mask == "per_call" else None)
+    dt = cfg.dtype
+    per_call = cfg.mask == "per_call"
+    calls = [W.gen_call(cfg, call_seed=10 + j) if per_call else W.gen_call(cfg.scaled(seed=cfg.seed + j))
+             for j in (1, 2, 3)]
+    xs = [up(c[0], dt) for c in calls]
+    masks = [c[1] for c in calls]
+    kw = dict(n_groups=cfg.n_groups, top_k=cfg.top_k, activation=cfg.activation, codec_slices=cfg.codec_slices)
+    args = (up(inp.x, dt), inp.mask, up(inp.w_global, dt), up_f32(inp.b_global), up(inp.w_local, dt),
+            up_f32(inp.b_local), up(inp.w_gate_up, dt), up(inp.w_down, dt), up(inp.u, dt), up(inp.v, dt))
+    seq = Ec2moeLayer(*args, overlap=False, **kw)
+    ovl = Ec2moeLayer(*args, overlap=True, **kw)
+    for step in range(6):
+        x, m = xs[step % 3], masks[step % 3]
+        for lay in (seq, ovl):
+            lay.set_input(x, m)
+            lay.step()
+        torch.cuda.synchronize()
+        for a, b in ((seq.y, ovl.y), (seq.topk_idx, ovl.topk_idx), (seq.topk_w, ovl.topk_w), (seq.z, ovl.z)):
+            assert torch.equal(a, b), f"step {step}"
