@@ -75,10 +75,14 @@ __global__ __launch_bounds__(256) void utp_kernel(UtpArgs g) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
     const int rbase = wave * 64;
-    // U columns r_h .. 255 stay zero: a wave's blocks past r_h (and P columns past r_w) multiply
-    // zeros, which keeps the matrix-core sequence free of branches; their outputs are not stored
-    for (int i = threadIdx.x; i < kUtpT * (256 - g.rh); i += 256) {
-        const int r = i / (256 - g.rh), c = g.rh + i % (256 - g.rh);
+    // Waves whose 64 rows all lie past r_h have nothing to compute. In the last active wave
+    // the U columns r_h .. (its end) stay zero: its blocks past r_h (and P columns past r_w)
+    // multiply zeros, which keeps its matrix-core sequence free of branches; their outputs
+    // are not stored.
+    const bool active = rbase < g.rh;
+    const int zc = ((g.rh + 63) & ~63) - g.rh;
+    for (int i = threadIdx.x; i < kUtpT * zc; i += 256) {
+        const int r = i / zc, c = g.rh + i % zc;
         Us[r * kUtpUP + c] = 0.f;
     }
     f32x4 acc[4][4];
@@ -142,10 +146,10 @@ __global__ __launch_bounds__(256) void utp_kernel(UtpArgs g) {
                 for (int cb = 0; cb < 4; ++cb)
                     acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[rb], b[cb], acc[rb][cb], 0, 0, 0);
         };
-        if (nt == kUtpT) {
+        if (active && nt == kUtpT) {
 #pragma unroll
             for (int k = 0; k < kUtpT; k += 4) kstep(k);
-        } else {
+        } else if (active) {
             const int nk = (nt + 3) & ~3;
             for (int k = 0; k < nk; k += 4) kstep(k);
         }

@@ -45,6 +45,8 @@ def test_full_rank_codec_round_trips_on_gpu():
     (5, 64, 256, 16, 32, W.F32),
     (17, 40, 128, 16, 16, W.BF16),   # more slices than one batch of launches (16)
     (4, 256, 768, 64, 64, W.BF16),   # the paper-shaped layers: 4 sequences of 256 tokens
+    (1, 300, 256, 80, 64, W.BF16),   # r_h ending inside the second 64-row block of U^T P
+    (2, 260, 128, 208, 112, W.F32),  # ... inside the fourth
 ])
 def test_codec_slices_and_separate_decoder_projections(c, h, w, rh, rw, dt):
     """Several slices coded with one U, V; decoder projections different from the encoder's."""
