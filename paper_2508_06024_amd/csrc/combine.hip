@@ -1,7 +1,9 @@
 // Weighted combine of the expert outputs, Eq. 1, for gfx950:
 //   y[t] = sum_{j<k} w[t][j] * y_perm[inv_perm[t*k + j]]
 // One wave per token; each lane owns 16-byte chunks of the row, accumulates the k slots in
-// float32 in slot order and rounds once. Memory-bound: reads k rows, writes one.
+// float32 in slot order and rounds once. Memory-bound: reads k rows, writes one. Few
+// tokens (decode-sized batches) also split the row over blockIdx.y, so that enough waves
+// have loads in flight.
 #include "device_common.h"
 #include "internal.h"
 
@@ -35,21 +37,23 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y_pe
         wt[j] = __shfl(my_w, j);
     }
     const int chunks = d / EPC;
-    for (int c0 = lane; c0 < chunks; c0 += 64 * B) {
+    const int per = chunks / gridDim.y;  // chunks of this row range (gridDim.y divides chunks)
+    const int cbeg = blockIdx.y * per, cend = cbeg + per;
+    for (int c0 = cbeg + lane; c0 < cend; c0 += 64 * B) {
         uint4 v[B][KMAX];
 #pragma unroll
         for (int b = 0; b < B; ++b)
 #pragma unroll
             for (int j = 0; j < KMAX; ++j) {
                 const int c = c0 + 64 * b;
-                v[b][j] = (j < top_k && pos[j] >= 0 && c < chunks)
+                v[b][j] = (j < top_k && pos[j] >= 0 && c < cend)
                               ? ldg16(y_perm + static_cast<int64_t>(pos[j]) * d + c * EPC)
                               : make_uint4(0, 0, 0, 0);
             }
 #pragma unroll
         for (int b = 0; b < B; ++b) {
             const int c = c0 + 64 * b;
-            if (c >= chunks) break;
+            if (c >= cend) break;
             float acc[EPC];
 #pragma unroll
             for (int i = 0; i < EPC; ++i) acc[i] = 0.f;
@@ -74,7 +78,11 @@ template <typename T, int KMAX, int B>
 void launch_k(const void* y_perm, const int32_t* inv_perm, const float* w, int n_tokens, int top_k, int d, void* y,
               hipStream_t s) {
     const int grid = (n_tokens + kTokPerBlock - 1) / kTokPerBlock;
-    hipLaunchKernelGGL((combine_kernel<T, KMAX, B>), dim3(grid), dim3(64 * kTokPerBlock), 0, s,
+    // row ranges of at least 64 chunks while the token waves number fewer than 1024
+    const int chunks = d / Elem<T>::kPerChunk;
+    int ysplit = 1;
+    while (n_tokens * ysplit * 2 <= 1024 && chunks % (ysplit * 2) == 0 && chunks / (ysplit * 2) >= 64) ysplit *= 2;
+    hipLaunchKernelGGL((combine_kernel<T, KMAX, B>), dim3(grid, ysplit), dim3(64 * kTokPerBlock), 0, s,
                        static_cast<const T*>(y_perm), inv_perm, w, n_tokens, top_k, d, static_cast<T*>(y));
 }
 
