@@ -36,7 +36,7 @@ constexpr int kSplitWaves = 4;      // waves of the split-d workgroups (small ba
 constexpr int kSplitMaxTiles = 64;  // 16-token tiles below which d is split (given a workspace)
 constexpr int kMaxSplit = 32;       // d-splits per tile at most
 constexpr int kSplitMinD = 2048;    // narrower gates run unsplit (the second launch costs more)
-constexpr int kRouteWaves = 8;      // waves of the routing workgroups after a split
+constexpr int kRouteWaves = 8;      // waves of the routing workgroups after a split (16 up to 96 rows)
 
 // Keeps a kernel-argument value in a scalar register: left alone, the compiler may reload
 // it from the argument segment at every use, and each reload waits on that memory.
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(64 * WAVES) void gate_kernel(GateArgs p) {
     constexpr int EPC = Elem<T>::kPerChunk;
     constexpr int SLICE = 4 * EPC;  // k covered by one matrix-core step
     // k-slices whose loads are issued together: U * (NB + NRB) 16-byte registers per lane
-    constexpr int UB = WAVES <= 8 ? 40 : 16;
+    constexpr int UB = WAVES <= 8 ? (NB * NRB >= 16 ? 30 : 40) : 16;  // 16 accumulator blocks: fewer in flight
     constexpr int U = UB / (NB + NRB) < 1 ? 1 : (UB / (NB + NRB) > 16 ? 16 : UB / (NB + NRB));
     constexpr int THREADS = 64 * WAVES;
     const int lane = threadIdx.x & 63;
@@ -633,6 +633,7 @@ hipError_t launch_nrb(const GateArgs& a, hipStream_t s) {
         // small batch with a workspace: d split over nsplit workgroups per tile, then routing
         hipError_t e = launch_cfg<T, NRB, 1, kSplitWaves, 2, 1>(a, s);
         if (e != hipSuccess) return e;
+        if constexpr (NRB <= 6) return launch_kp<T, NRB, 1, 16, 2>(a, s);  // more loads of partials in flight
         return launch_kp<T, NRB, 1, kRouteWaves, 2>(a, s);
     }
     if constexpr (NRB <= 6)

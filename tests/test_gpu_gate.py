@@ -225,6 +225,7 @@ def _group_cut_near_ties(x, wg, bg, members, M, K, k, sizes, top_groups):
     (257, 512, 40, 6, 4, 30, (1, 9, 10, 5, 12, 3), 2),  # both, ragged token count
     (64, 128, 8, 2, 2, None, None, 1),
     (100, 256, 256, 64, 16, 200, None, 5),              # the maximum gate, top-16
+    (8200, 256, 120, 8, 4, 100, None, 0),               # 128 gate rows in 32-token tiles (>= 512 tiles)
 ])
 def test_gate_options_match_oracle(T, d, M, K, k, keep, sizes, top_groups):
     say(f"gate options T={T} M={M} K={K} k={k} sizes={sizes} top_groups={top_groups}")
