@@ -175,7 +175,7 @@ struct SplitPlan {
     int full, tail, S, chunk_slabs;
 };
 
-__device__ __forceinline__ SplitPlan split_plan(int total, int slots, int max_split, int nk) {
+__host__ __device__ __forceinline__ SplitPlan split_plan(int total, int slots, int max_split, int nk) {
     SplitPlan sp;
     sp.full = slots > 0 ? total / slots * slots : total;
     sp.tail = total - sp.full;
@@ -967,7 +967,7 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
 // Sums the float32 partial tiles of the split tail in chunk order and applies the
 // epilogue (store, ReLU store, or silu(gate) * up) of the large-tile kernel. One workgroup per
 // (tail tile, 16 rows); every thread owns a run of 4 output columns per pass and issues
-// the loads of all chunks before adding them in order.
+// the loads of up to 16 chunks (8 of each half with SwiGLU) before adding them in order.
 template <int TM, int TN, bool SWIGLU, typename TO>
 __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs a) {
     constexpr int NOUT = SWIGLU ? TN / 2 : TN;
@@ -976,6 +976,7 @@ __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs a) {
     if (sp.S <= 1) return;
     constexpr int ROWS = 16;
     constexpr int QUADS = NOUT / 4;                  // float4 column runs per row
+    constexpr int KB = SWIGLU ? 8 : 16;              // chunks loaded together
     const int t = blockIdx.x / (TM / ROWS);
     if (t >= sp.tail) return;
     TileInfo ti;
@@ -986,12 +987,12 @@ __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs a) {
         const int r = r0 + i / QUADS;
         const int c = (i % QUADS) * 4;
         if (r >= ti.valid) continue;
-        // chunks in order, 8 loads in flight at a time
+        // chunks in order, KB (SwiGLU: twice KB / 2) loads in flight at a time
         f32x4 sg = f32x4{0.f, 0.f, 0.f, 0.f}, su = sg;
-        for (int k0 = 0; k0 < sp.S; k0 += 8) {
-            f32x4 g[8], u[8];
+        for (int k0 = 0; k0 < sp.S; k0 += KB) {
+            f32x4 g[KB], u[KB];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
+            for (int k = 0; k < KB; ++k) {
                 if (k0 + k < sp.S) {
                     const float* src = tile_part + static_cast<int64_t>(k0 + k) * TM * TN + r * TN + c;
                     g[k] = *reinterpret_cast<const f32x4*>(src);
@@ -999,7 +1000,7 @@ __global__ __launch_bounds__(256) void gemm_split_reduce_kernel(GemmArgs a) {
                 }
             }
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
+            for (int k = 0; k < KB; ++k) {
                 if (k0 + k < sp.S) {
                     sg = k0 + k == 0 ? g[k] : sg + g[k];
                     if (SWIGLU) su = k0 + k == 0 ? u[k] : su + u[k];
@@ -1055,15 +1056,20 @@ hipError_t run_lds(const GemmArgs& a, hipStream_t s) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !can_split) return e;
-    // the tile count of a dense launch is known here: no tail, no reduction
+    // The tile count of a dense launch is known here: the reduction gets one workgroup per
+    // (tail tile, 16 rows), or no launch without a split tail. Grouped launches count their
+    // tiles on the device: a workgroup for every possible tail tile, the surplus leaving at once.
+    int64_t rgrid = static_cast<int64_t>(gemm_slots<TM, TN>()) * (TM / 16);
     if (a.seg == nullptr) {
         constexpr int NOUT = SWIGLU ? TN / 2 : TN;
         const int64_t tiles = (a.rows + TM - 1) / TM * ((a.N + NOUT - 1) / NOUT);
-        if (tiles % gemm_slots<TM, TN>() == 0) return hipSuccess;
+        const SplitPlan sp = split_plan(static_cast<int>(tiles), gemm_slots<TM, TN>(), a.max_split, a.K / 64);
+        if (sp.S <= 1) return hipSuccess;
+        rgrid = static_cast<int64_t>(sp.tail) * (TM / 16);
     }
     std::string rname = std::string(a.name ? a.name : "gemm") + "_tail";
     ProfileScope prof(rname.c_str(), s);
-    hipLaunchKernelGGL((gemm_split_reduce_kernel<TM, TN, SWIGLU, TO>), dim3(gemm_slots<TM, TN>() * (TM / 16)), dim3(256),
+    hipLaunchKernelGGL((gemm_split_reduce_kernel<TM, TN, SWIGLU, TO>), dim3(static_cast<unsigned>(rgrid)), dim3(256),
                        0, s, a);
     return hipGetLastError();
 }
