@@ -109,7 +109,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         log("bench.py measures one GPU: this implementation has no multi-GPU path "
-            "(the token-sharded design is described in DESIGN.md); run with --gpus 1")
+            "(it would shard over tokens, with one all-reduce of the encoder's Z); run with --gpus 1")
         sys.exit(2)
 
     import torch
