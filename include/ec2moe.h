@@ -60,12 +60,12 @@ typedef enum {
  * groups (group k = experts [k*M/K, (k+1)*M/K)), expert hidden width H, top-k routing. */
 typedef struct {
     int32_t n_tokens;   /* T */
+    int32_t d_model;    /* d */
     int32_t n_experts;  /* M */
     int32_t n_groups;   /* K */
-    int32_t d_model;    /* d */
-    int32_t ffn_hidden; /* H */
     int32_t top_k;      /* k */
-    int32_t dtype;      /* ec2moe_dtype of x, gate weights, expert weights and y */
+    int32_t ffn_hidden; /* H */
+    ec2moe_dtype dtype; /* of x, gate weights, expert weights and y (an int-sized enum) */
     uint32_t flags;     /* OR of EC2MOE_GATE_RENORMALIZE, EC2MOE_EXPERT_RELU, or 0 */
 } ec2moe_moe_desc;
 
@@ -77,7 +77,7 @@ typedef struct {
     int32_t w;
     int32_t r_h;
     int32_t r_w;
-    int32_t dtype;    /* ec2moe_dtype of x, x_hat and the projections */
+    ec2moe_dtype dtype; /* of x, x_hat and the projections (an int-sized enum) */
 } ec2moe_codec_desc;
 
 /*

@@ -3,7 +3,9 @@
     python -m paper_2508_06024_amd.build
 
 Every source under csrc/ is compiled to an object (in parallel) and linked into
-paper_2508_06024_amd/libec2moe.so next to this file.
+paper_2508_06024_amd/libec2moe.so next to this file. With --incremental, sources whose
+object is newer than the source and every header under csrc/ and include/ are not
+recompiled (a development shortcut; the default rebuilds everything).
 """
 from __future__ import annotations
 
@@ -32,6 +34,20 @@ def sources():
     return sorted(f for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
 
 
+def _headers_mtime() -> float:
+    hs = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".h")]
+    hs += [os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h")]
+    return max(os.path.getmtime(h) for h in hs)
+
+
+def _up_to_date(src: str) -> bool:
+    obj = os.path.join(BUILD_DIR, src + ".o")
+    if not os.path.exists(obj):
+        return False
+    t = os.path.getmtime(obj)
+    return t > os.path.getmtime(os.path.join(CSRC, src)) and t > _headers_mtime()
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, src + ".o")
     cmd = [HIPCC, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
@@ -47,13 +63,16 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = True) -> str:
+def build(verbose: bool = True, incremental: bool = False) -> str:
     if not shutil.which(HIPCC) and not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
     os.makedirs(BUILD_DIR, exist_ok=True)
     srcs = sources()
-    with ThreadPoolExecutor(min(8, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
+    todo = [s for s in srcs if not (incremental and _up_to_date(s))]
+    if todo:
+        with ThreadPoolExecutor(min(8, len(todo))) as ex:
+            list(ex.map(_compile, todo))
+    objs = [os.path.join(BUILD_DIR, s + ".o") for s in srcs]
     tmp = LIB + ".tmp"
     r = subprocess.run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,--no-undefined",
                         "-o", tmp, *objs],
@@ -62,9 +81,9 @@ def build(verbose: bool = True) -> str:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, LIB)
     if verbose:
-        print(f"built {LIB} from {len(srcs)} sources")
+        print(f"built {LIB} from {len(srcs)} sources ({len(todo)} compiled)")
     return LIB
 
 
 if __name__ == "__main__":
-    build()
+    build(incremental="--incremental" in sys.argv[1:])

@@ -71,7 +71,7 @@ constexpr int kMaxTopK = 16;
 ec2moe_status check_moe_desc(const ec2moe_moe_desc* d, bool equal_groups = true) {
     REQUIRE(d != nullptr, EC2MOE_ERR_INVALID_ARGUMENT, "desc is NULL");
     REQUIRE(d->dtype == EC2MOE_F32 || d->dtype == EC2MOE_BF16, EC2MOE_ERR_INVALID_ARGUMENT, "unknown dtype %d",
-            d->dtype);
+            static_cast<int>(d->dtype));
     REQUIRE(d->n_tokens >= 0, EC2MOE_ERR_INVALID_ARGUMENT, "n_tokens %d < 0", d->n_tokens);
     REQUIRE(d->n_experts > 0 && d->n_groups > 0 && d->d_model > 0 && d->ffn_hidden > 0 && d->top_k > 0,
             EC2MOE_ERR_INVALID_ARGUMENT, "n_experts, n_groups, d_model, ffn_hidden and top_k must be positive");
@@ -142,7 +142,7 @@ ec2moe_status check_ws(void* ws, size_t have, size_t need) {
 ec2moe_status check_codec_desc(const ec2moe_codec_desc* d) {
     REQUIRE(d != nullptr, EC2MOE_ERR_INVALID_ARGUMENT, "desc is NULL");
     REQUIRE(d->dtype == EC2MOE_F32 || d->dtype == EC2MOE_BF16, EC2MOE_ERR_INVALID_ARGUMENT, "unknown dtype %d",
-            d->dtype);
+            static_cast<int>(d->dtype));
     REQUIRE(d->n_slices >= 0 && d->h >= 0, EC2MOE_ERR_INVALID_ARGUMENT, "n_slices and h must be >= 0");
     REQUIRE(d->w > 0 && d->r_h > 0 && d->r_w > 0, EC2MOE_ERR_INVALID_ARGUMENT, "w, r_h and r_w must be positive");
     REQUIRE(d->r_h <= d->h || d->h == 0, EC2MOE_ERR_INVALID_ARGUMENT, "r_h %d > h %d", d->r_h, d->h);

@@ -34,14 +34,15 @@ class Ec2moeError(RuntimeError):
 
 
 class MoeDesc(ctypes.Structure):
-    _fields_ = [("n_tokens", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("n_groups", ctypes.c_int32),
-                ("d_model", ctypes.c_int32), ("ffn_hidden", ctypes.c_int32), ("top_k", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+    # field order of ec2moe_moe_desc: T, d, M, K, k, H, dtype (an int-sized enum), flags
+    _fields_ = [("n_tokens", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_experts", ctypes.c_int32),
+                ("n_groups", ctypes.c_int32), ("top_k", ctypes.c_int32), ("ffn_hidden", ctypes.c_int32),
+                ("dtype", ctypes.c_int), ("flags", ctypes.c_uint32)]
 
 
 class CodecDesc(ctypes.Structure):
     _fields_ = [("n_slices", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32),
-                ("r_h", ctypes.c_int32), ("r_w", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+                ("r_h", ctypes.c_int32), ("r_w", ctypes.c_int32), ("dtype", ctypes.c_int)]
 
 
 class GateOpts(ctypes.Structure):
@@ -148,8 +149,8 @@ def moe_desc(n_tokens, n_experts, n_groups, d_model, ffn_hidden, top_k, dtype, r
     if activation not in ACTIVATIONS:
         raise ValueError(f"activation must be one of {ACTIVATIONS}, got {activation!r}")
     flags = (GATE_RENORMALIZE if renormalize else 0) | (EXPERT_RELU if activation == "relu" else 0)
-    return MoeDesc(n_tokens, n_experts, n_groups, d_model, ffn_hidden, top_k,
-                   dtype if isinstance(dtype, int) else dtype_code(dtype), flags)
+    return MoeDesc(n_tokens=n_tokens, d_model=d_model, n_experts=n_experts, n_groups=n_groups, top_k=top_k,
+                   ffn_hidden=ffn_hidden, dtype=dtype if isinstance(dtype, int) else dtype_code(dtype), flags=flags)
 
 
 def w_in_rows(ffn_hidden: int, activation: str) -> int:

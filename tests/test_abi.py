@@ -217,3 +217,52 @@ def test_codec_validation():
 
 def test_profile_collect_without_records():
     assert E.profile_collect() == {}
+
+
+# ----------------------------------------------------------------------------- descriptor layout
+
+# The descriptors' field order is the interface contract: T, d, M, K, k, H, dtype, flags for
+# the MoE layer and c, h, w, r_h, r_w, dtype for the codec, every field 4 bytes.
+MOE_FIELDS = ["n_tokens", "d_model", "n_experts", "n_groups", "top_k", "ffn_hidden", "dtype", "flags"]
+CODEC_FIELDS = ["n_slices", "h", "w", "r_h", "r_w", "dtype"]
+
+
+def _c_offsets(tmp_path):
+    """offsetof / sizeof of every descriptor field as a C compiler lays out the header."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ec2moe.h"', 'int main(void) {']
+    for s, fields in (("ec2moe_moe_desc", MOE_FIELDS), ("ec2moe_codec_desc", CODEC_FIELDS)):
+        for f in fields:
+            lines.append(f'printf("{s} {f} %zu %zu\\n", offsetof({s}, {f}), sizeof((({s}*)0)->{f}));')
+        lines.append(f'printf("{s} sizeof %zu 0\\n", sizeof({s}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "offsets.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "offsets"
+    subprocess.run([cc, "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include", "-I", os.path.join(ROOT, "include"),
+                    str(src), "-o", str(exe)], check=True, capture_output=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
+    res = {}
+    for ln in out.splitlines():
+        s, f, off, size = ln.split()
+        res[(s, f)] = (int(off), int(size))
+    return res
+
+
+def test_descriptor_layout_matches_the_contract(tmp_path):
+    c = _c_offsets(tmp_path)
+    for s, fields, py in (("ec2moe_moe_desc", MOE_FIELDS, E.MoeDesc), ("ec2moe_codec_desc", CODEC_FIELDS, E.CodecDesc)):
+        for i, f in enumerate(fields):
+            assert c[(s, f)] == (4 * i, 4), (s, f, c[(s, f)])
+            assert getattr(py, f).offset == 4 * i and getattr(py, f).size == 4, (s, f)
+        assert c[(s, "sizeof")][0] == 4 * len(fields) == ctypes.sizeof(py)
+        assert [n for n, _ in py._fields_] == fields
+    # a descriptor built by the binding carries each shape in its own field
+    d = E.moe_desc(n_tokens=11, n_experts=12, n_groups=3, d_model=256, ffn_hidden=384, top_k=2, dtype=E.BF16)
+    raw = bytes(d)
+    vals = [int.from_bytes(raw[4 * i:4 * i + 4], "little") for i in range(8)]
+    assert vals == [11, 256, 12, 3, 2, 384, E.BF16, E.GATE_RENORMALIZE]

@@ -568,6 +568,19 @@ def test_layer_routes_on_x_and_runs_experts_on_reconstruction():
     np.testing.assert_allclose(out["x_hat"], xh, atol=1e-14)
     assert out["y"].shape == (cfg.n_tokens, cfg.d_model)
     assert not set(out["idx"].ravel().tolist()) & set(cfg.masked_out)
+    # Eq. 1 token by token on the reconstruction X_hat = U U^T X V V^T, with the routing the
+    # gate took on X: y[t] = sum_j w[t, j] E_{idx[t, j]}(x_hat[t]), each expert a dense SwiGLU
+    # FFN evaluated by torch (not the oracle's permuted expert path)
+    gu, dn = f("w_gate_up"), f("w_down")
+    for t in range(cfg.n_tokens):
+        ref = sum(float(w[t, j]) * _torch_dense_swiglu(xh[t:t + 1], gu[idx[t, j]], dn[idx[t, j]])[0]
+                  for j in range(cfg.top_k))
+        np.testing.assert_allclose(out["y"][t], ref, rtol=1e-12, atol=1e-15)
+    # the experts see X_hat, not X: below full rank (16 of 64 tokens, 16 of 128 features) the
+    # two outputs differ by far more than rounding
+    y_on_x = np.stack([sum(float(w[t, j]) * _torch_dense_swiglu(f("x")[t:t + 1], gu[idx[t, j]], dn[idx[t, j]])[0]
+                           for j in range(cfg.top_k)) for t in range(cfg.n_tokens)])
+    assert np.max(np.abs(out["y"] - y_on_x)) > 0.1 * np.max(np.abs(y_on_x))
 
 
 # ----------------------------------------------------------------------------- codec fitting (Eq. 8, lambda = 0)
