@@ -53,13 +53,16 @@ def parse():
     return ap.parse_args()
 
 
-def blas_threads():
+def blas_info():
+    """(threads, vendor) of the BLAS pool numpy calls."""
     try:
         from threadpoolctl import threadpool_info
-        n = [p["num_threads"] for p in threadpool_info() if p.get("user_api") == "blas"]
-        return max(n) if n else 1
+        pools = [p for p in threadpool_info() if p.get("user_api") == "blas"]
     except Exception:
-        return 1
+        pools = []
+    threads = max([p["num_threads"] for p in pools] or [1])
+    vendor = ", ".join(sorted({f"{p.get('internal_api', '?')} {p.get('version', '')}".strip() for p in pools})) or "unknown"
+    return threads, vendor
 
 
 def cpu_baseline(inp, cfg, target_s, top_groups=0):
@@ -96,7 +99,9 @@ def cpu_baseline(inp, cfg, target_s, top_groups=0):
     while S == T and t < target_s:
         t += run(S)
         reps += 1
-    return {"value": S * reps / t, "unit": "tokens/s", "cores": blas_threads(), "kind": "oracle",
+    threads, vendor = blas_info()
+    return {"value": S * reps / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "host_cores": len(os.sched_getaffinity(0)), "blas_vendor": vendor, "blas_threads": threads,
             "sample": f"oracle step (gate, encode, decode, experts, combine) on the first {S} of {T} tokens "
                       f"of the same inputs" + (", U restricted to those rows" if c == 1 else
                                                 f", {S // h} of {c} codec slices") +
@@ -163,9 +168,8 @@ def main():
     torch.cuda.synchronize()
     stats = E.profile_collect()
     E.profile_enable(False)
-    idx = layer.topk_idx.cpu().numpy()
-    work = R.kernel_work(cfg, R.expert_rows(idx, cfg.n_experts))
-    dom = max((n for n in stats if n in work), key=lambda n: stats[n][1])
+    stage_names = R.kernel_work(cfg, np.ones(cfg.n_experts, np.int64)).keys()
+    dom = max((n for n in stats if n in stage_names), key=lambda n: stats[n][1])
 
     # Timed region: events only around the dominant kernel, so the others run back to back.
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -225,6 +229,25 @@ def main():
         log(f"[bench] calibration copy of {args.calibrate_copy_mib} MiB done")
         del a, b
 
+    # Algorithmic work at the realised routing of the very calls each figure covers. With a
+    # candidate mask drawn per call the routing, and with it the set of active experts whose
+    # weights the GEMMs stream, changes from call to call: the work is then averaged over
+    # the same calls (the gate, which is deterministic, run again alone on each).
+    def mean_work(n):
+        """(work per kernel, active experts), averaged over calls 0..n-1."""
+        tot, active = None, 0
+        for i in range(n if per_call else 1):
+            layer.set_input(xs[i % len(xs)], masks[i % len(masks)])
+            rows_e = R.expert_rows(layer.route()[0].cpu().numpy(), cfg.n_experts)
+            w = R.kernel_work(cfg, rows_e)
+            active += int(np.count_nonzero(rows_e))
+            tot = w if tot is None else {k: (tot[k][0] + w[k][0], tot[k][1] + w[k][1]) for k in w}
+        m = n if per_call else 1
+        return {k: (f / m, b / m) for k, (f, b) in tot.items()}, active / m
+
+    work, _ = mean_work(prof_steps)  # the calls of the per-kernel pass
+    work_timed, active_timed = mean_work(steps) if per_call else (work, None)  # the calls of the timed region
+
     # per-kernel algorithmic work at the realised routing
     base = {"gate_split": "gate", "perm_small": "permute", "perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
             "transpose": "encode", "codec_xv": "encode", "codec_utp": "encode",
@@ -249,10 +272,11 @@ def main():
     step_roof_ms = 0.0
     for g, (ms_g, _) in rows.items():
         if g in work:
+            ft, bt = work_timed[g]
+            step_roof_ms += max(ft / (peak_f * 1e12), bt / (R.PEAK_HBM_GBS * 1e9)) * 1e3
             flop, byt = work[g]
             t_f = flop / (peak_f * 1e12) * 1e3
             t_b = byt / (R.PEAK_HBM_GBS * 1e9) * 1e3
-            step_roof_ms += max(t_f, t_b)
             bound = "mfma" if t_f >= t_b else "hbm"
             ach = flop / (ms_g * 1e-3) / 1e12 if bound == "mfma" else byt / (ms_g * 1e-3) / 1e9
             peak = peak_f if bound == "mfma" else R.PEAK_HBM_GBS
@@ -265,7 +289,7 @@ def main():
 
     n_l, tot = dom_stats  # the dominant kernel's launches inside the timed region
     avg_s = tot / n_l * 1e-3
-    flop, byt = work[dom]
+    flop, byt = work_timed[dom]
     bound = "mfma" if flop / (peak_f * 1e12) >= byt / (R.PEAK_HBM_GBS * 1e9) else "hbm"
     if bound == "mfma":
         achieved, peak, unit = flop / avg_s / 1e12, peak_f, "TFLOP/s"
@@ -275,6 +299,15 @@ def main():
     roof = {"kernel": dom, "bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": traffic,
             "algorithmic": {"flop": flop, "bytes": byt}, "avg_launch_us": round(avg_s * 1e6, 1)}
+    if per_call:
+        roof["algorithmic_note"] = (f"mean over the {steps} timed calls of each call's work at its own routing "
+                                    f"(active experts per call: {active_timed:.1f} on average)")
+    # A step whose algorithmic bytes stay below twice the 256 MB Infinity Cache re-reads the same
+    # weights every step: its "HBM" rates may be partly cache hits.
+    step_bytes = sum(b for _, b in work_timed.values())
+    cache_note = (f"the step moves {step_bytes / 1e6:.0f} MB (algorithmic), the same weights every step: below "
+                  f"512 MB the per-stage HBM rates may include Infinity Cache (256 MB) hits"
+                  if step_bytes < 512e6 and not per_call else None)
 
     # host planner (candidate mask producer and task scheduler): host time per call
     rng = np.random.default_rng(0)
@@ -321,6 +354,7 @@ def main():
                    "tokens_per_step": cfg.n_tokens},
         "roofline": roof,
         "layer_roofline_frac": round(step_roof_ms / ms_step, 4),
+        "cache_note": cache_note,
         "kernels": kernels,
         "kernels_pass": f"separate pass of {prof_steps} steps with HIP events around every kernel",
         "launch": ("HIP graph replays of the step (the dominant kernel's time from an eager pass)"

@@ -78,6 +78,11 @@ class Ec2moeLayer:
         E.group_gate_ex(self.moe_desc, self.gate_opts, self.mask, self.x, self.w_global, self.b_global,
                         self.w_local, self.b_local, self.topk_idx, self.topk_w)
 
+    def route(self):
+        """The gate alone on the current input: (topk_idx, topk_w), the routing step() uses."""
+        self._gate()
+        return self.topk_idx, self.topk_w
+
     def _codec(self):
         E.lowrank_encode_into(self.codec_desc, self.x, self.u, self.v, self.z, self.codec_ws)
         E.lowrank_decode_into(self.codec_desc, self.z, self.u_hat, self.v_hat, self.x_hat, self.codec_ws)

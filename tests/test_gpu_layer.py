@@ -30,7 +30,10 @@ def oracle_sampled(inp, toks, top_groups=0, group_sizes=None):
                              cfg.n_groups, cfg.top_k, group_sizes=group_sizes, top_groups=top_groups)
     h = cfg.codec_h
     z = np.stack([O.lowrank_encode(x[s * h:(s + 1) * h], u, v) for s in range(cfg.codec_slices)])
-    xh = np.stack([O.lowrank_decode(z[t // h], u[[t % h]], v)[0] for t in toks])
+    if len(toks) == cfg.n_tokens:
+        xh = np.concatenate([O.lowrank_decode(z[s], u, v) for s in range(cfg.codec_slices)])
+    else:
+        xh = np.stack([O.lowrank_decode(z[t // h], u[[t % h]], v)[0] for t in toks])
     y = np.zeros((len(toks), cfg.d_model))
     expert = O.EXPERTS[cfg.activation]
     for e in np.unique(idx):
@@ -41,11 +44,11 @@ def oracle_sampled(inp, toks, top_groups=0, group_sizes=None):
     return idx, w, g, z, xh, y
 
 
-@pytest.mark.parametrize("name,call,sample", [("tiny", None, 0), ("small", None, 0), ("mixtral", None, 40),
-                                              ("finegrained", None, 40), ("decode", 4, 0), ("decode", 777, 0),
-                                              ("switch8", None, 0), ("switch16", None, 64),
-                                              ("switch32", None, 64), ("switch64", None, 0)])
-def test_layer_step_matches_oracle(name, call, sample):
+@pytest.mark.parametrize("name,call", [("tiny", None), ("small", None), ("mixtral", None), ("finegrained", None),
+                                       ("decode", 4), ("decode", 777), ("switch8", None), ("switch16", None),
+                                       ("switch32", None), ("switch64", None)])
+def test_layer_step_matches_oracle(name, call):
+    """Every token of the step: routing (certified near-ties aside), Z, X_hat and y."""
     cfg = W.CONFIGS[name]
     say(f"layer {name} call {call}")
     torch.cuda.empty_cache()
@@ -53,12 +56,7 @@ def test_layer_step_matches_oracle(name, call, sample):
     lay = build(inp)
     lay.step()
     torch.cuda.synchronize()
-    T = cfg.n_tokens
-    if sample:
-        rng = np.random.default_rng(1)
-        toks = np.array(sorted(set(rng.choice(T, sample, replace=False).tolist()) | {0, T - 1}))
-    else:
-        toks = np.arange(T)
+    toks = np.arange(cfg.n_tokens)
     idx, w, g, z, xh, y = oracle_sampled(inp, toks)
     gidx, gw = down(lay.topk_idx)[toks], down(lay.topk_w)[toks]
     n_cert = check_routing(gidx, gw, idx, w, g, W.mask_members(inp.mask, cfg.n_experts), cfg.top_k)
