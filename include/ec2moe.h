@@ -158,6 +158,22 @@ ec2moe_status ec2moe_permute(const ec2moe_moe_desc* desc, const int32_t* topk_id
                              hipStream_t stream);
 
 /*
+ * ec2moe_permute without a workspace, for callers that cannot allocate (code under HIP
+ * graph capture, serving loops, harnesses that forbid allocation). The same kernels and
+ * results as ec2moe_permute; the per-chunk expert counts of inputs above 8192 assignments
+ * go to an array the library holds on each GPU (1 MiB, kept until the process ends, looked
+ * up on the first call on that device; this call allocates nothing). Every count it reads
+ * is written first in the same call, so the array needs no clearing.
+ *   Limit: ceil(T*k / 1024) * n_experts <= 262144 (e.g. 1,048,576 assignments over 256
+ *   experts); larger inputs return EC2MOE_ERR_UNSUPPORTED before any launch.
+ *   Calls that overlap on one GPU (other streams, other threads) share the array and race:
+ *   order them, or use ec2moe_permute with a workspace each.
+ */
+ec2moe_status ec2moe_permute_noalloc(const ec2moe_moe_desc* desc, const int32_t* topk_idx,
+                                     const void* x, int32_t* seg_offsets, int32_t* perm_src,
+                                     int32_t* inv_perm, void* x_perm, hipStream_t stream);
+
+/*
  * The expert networks E_i of Eq. 1 on permuted rows:
  *   y_perm[p] = E_e(x[perm_src[p]]) for every position p of segment e.
  * Default: SwiGLU feed-forward layers, E(x) = W_down (silu(W_gate x) * (W_up x)),

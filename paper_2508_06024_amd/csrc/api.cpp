@@ -385,6 +385,34 @@ ec2moe_status ec2moe_permute(const ec2moe_moe_desc* desc, const int32_t* topk_id
     return hip_status(e, "permute launch");
 }
 
+ec2moe_status ec2moe_permute_noalloc(const ec2moe_moe_desc* desc, const int32_t* topk_idx, const void* x,
+                                     int32_t* seg_offsets, int32_t* perm_src, int32_t* inv_perm, void* x_perm,
+                                     hipStream_t stream) {
+    if (ec2moe_status st = check_moe_desc(desc, false); st != EC2MOE_OK) return st;
+    REQUIRE_PTR(seg_offsets);
+    REQUIRE((x == nullptr) == (x_perm == nullptr), EC2MOE_ERR_INVALID_ARGUMENT,
+            "x and x_perm must both be given or both be NULL");
+    const int64_t A = static_cast<int64_t>(desc->n_tokens) * desc->top_k;
+    const int64_t words = static_cast<int64_t>(perm_chunks(A)) * desc->n_experts;
+    REQUIRE(words <= kPermStaticCountWords, EC2MOE_ERR_UNSUPPORTED,
+            "%lld assignments over %d experts need %lld count words; the library's own array holds %d "
+            "(ceil(T*k / %d) * n_experts <= %d): pass a workspace to ec2moe_permute instead",
+            static_cast<long long>(A), desc->n_experts, static_cast<long long>(words), kPermStaticCountWords,
+            kPermChunk, kPermStaticCountWords);
+    if (A > 0) {
+        REQUIRE_PTR(topk_idx); REQUIRE_PTR(perm_src); REQUIRE_PTR(inv_perm);
+        if (x) { REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(x_perm); }
+    }
+    int32_t* counts = nullptr;
+    hipError_t e = permute_static_counts(&counts);
+    if (e != hipSuccess) return hip_status(e, "permute_noalloc: device count array");
+    e = launch_permute(topk_idx, A, desc->top_k, desc->n_experts, counts, seg_offsets, perm_src, inv_perm, stream);
+    if (e == hipSuccess && x)
+        e = launch_gather_rows(static_cast<DType>(desc->dtype), x, desc->n_tokens, perm_src,
+                               seg_offsets + desc->n_experts, A, desc->d_model, x_perm, stream);
+    return hip_status(e, "permute_noalloc launch");
+}
+
 namespace {
 
 hipError_t run_experts(const ec2moe_moe_desc* desc, const void* x, const int32_t* seg, const int32_t* perm_src,

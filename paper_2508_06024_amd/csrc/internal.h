@@ -46,6 +46,12 @@ size_t gate_split_bytes(DType dt, int n_tokens, int d, int gate_rows);
 constexpr int kPermChunk = 1024;
 inline int perm_chunks(int64_t n_assign) { return static_cast<int>((n_assign + kPermChunk - 1) / kPermChunk); }
 
+// The library's own per-device count array (1 MiB) for callers that pass no workspace:
+// *counts receives the current device's copy (looked up once per device). Calls that
+// overlap on one device share it and race.
+constexpr int kPermStaticCountWords = 1 << 18;
+hipError_t permute_static_counts(int32_t** counts);
+
 hipError_t launch_permute(const int32_t* topk_idx, int64_t n_assign, int top_k, int n_experts,
                           int32_t* chunk_counts /*[chunks][M]*/, int32_t* seg_offsets,
                           int32_t* perm_src, int32_t* inv_perm, hipStream_t s);

@@ -14,8 +14,16 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <mutex>
 
 namespace ec2moe {
+
+// Per-chunk expert counts of the chunked path for callers that cannot allocate: one array
+// per GPU, held until the process ends. Host code never uses this name as an address (on
+// the host it only stands for the symbol): permute_static_counts() looks up each device's
+// copy with hipGetSymbolAddress and the kernels receive that pointer.
+static __device__ __align__(256) int32_t scratch[kPermStaticCountWords];
+
 namespace {
 
 constexpr int kWaveItems = kPermChunk / 4;  // assignments per wave per chunk
@@ -343,6 +351,26 @@ hipError_t launch_permute(const int32_t* topk_idx, int64_t n_assign, int top_k, 
                            n_experts, chunk_counts, perm_src, inv_perm);
     }
     return hipGetLastError();
+}
+
+hipError_t permute_static_counts(int32_t** counts) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static int32_t* addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(mu);
+    if (addr[dev] == nullptr) {
+        void* p = nullptr;
+        // once per device, with that device current: its own copy of the array
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = static_cast<int32_t*>(p);
+    }
+    *counts = addr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_gather_rows(DType dt, const void* x, int64_t n_src, const int32_t* perm_src,

@@ -86,6 +86,7 @@ _SIGS = {
     "ec2moe_gate_workspace_size": [ctypes.POINTER(MoeDesc), ctypes.POINTER(ctypes.c_size_t)],
     "ec2moe_moe_workspace_size": [ctypes.POINTER(MoeDesc), ctypes.POINTER(ctypes.c_size_t)],
     "ec2moe_permute": [ctypes.POINTER(MoeDesc), _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
+    "ec2moe_permute_noalloc": [ctypes.POINTER(MoeDesc), _P, _P, _P, _P, _P, _P, _P],
     "ec2moe_expert_ffn": [ctypes.POINTER(MoeDesc), _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
     "ec2moe_combine": [ctypes.POINTER(MoeDesc), _P, _P, _P, _P, _P],
     "ec2moe_moe_forward": [ctypes.POINTER(MoeDesc), _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
@@ -294,6 +295,13 @@ def combine(y_perm, inv_perm, topk_w):
     _check(_lib.ec2moe_combine(ctypes.byref(desc), _ptr(y_perm), _ptr(inv_perm), _ptr(topk_w), _ptr(y),
                                _stream()))
     return y
+
+
+def permute_noalloc_into(desc: MoeDesc, topk_idx, seg_offsets, perm_src, inv_perm, x=None, x_perm=None):
+    """Raw call of the workspace-free permutation (caller-owned outputs; the library allocates
+    nothing)."""
+    _check(_lib.ec2moe_permute_noalloc(ctypes.byref(desc), _ptr(topk_idx), _ptr(x), _ptr(seg_offsets),
+                                       _ptr(perm_src), _ptr(inv_perm), _ptr(x_perm), _stream()))
 
 
 def permute_into(desc: MoeDesc, topk_idx, seg_offsets, perm_src, inv_perm, ws, x=None, x_perm=None):

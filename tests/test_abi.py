@@ -266,3 +266,14 @@ def test_descriptor_layout_matches_the_contract(tmp_path):
     raw = bytes(d)
     vals = [int.from_bytes(raw[4 * i:4 * i + 4], "little") for i in range(8)]
     assert vals == [11, 256, 12, 3, 2, 384, E.BF16, E.GATE_RENORMALIZE]
+
+
+def test_permute_noalloc_rejects_inputs_beyond_its_array():
+    """ceil(T*k / 1024) * n_experts count words must fit the library's 262144-word array; the
+    error comes from the host before any launch (no device pointer is touched)."""
+    p = ctypes.c_void_p(1 << 20)
+    over = _desc(n_tokens=1048577, top_k=1, n_experts=256, n_groups=16)
+    assert E._lib.ec2moe_permute_noalloc(ctypes.byref(over), p, None, p, p, p, None, None) == UNSUPPORTED
+    assert "count words" in E.last_error()
+    assert E._lib.ec2moe_permute_noalloc(ctypes.byref(_desc()), p, p, p, p, p, None, None) == INVALID  # x without x_perm
+    assert E._lib.ec2moe_permute_noalloc(ctypes.byref(_desc()), p, None, None, p, p, None, None) == INVALID
