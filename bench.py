@@ -249,7 +249,7 @@ def main():
     work_timed, active_timed = mean_work(steps) if per_call else (work, None)  # the calls of the timed region
 
     # per-kernel algorithmic work at the realised routing
-    base = {"gate_split": "gate", "perm_small": "permute", "perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
+    base = {"gate_split": "gate", "perm_onepass": "permute", "perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
             "transpose": "encode", "codec_xv": "encode", "codec_utp": "encode",
             "codec_z_bf16": "decode", "codec_prep": "decode", "codec_vzt": "decode", "codec_uw": "decode"}
 

@@ -4,7 +4,7 @@
 
 Every source under csrc/ is compiled to an object (in parallel) and linked into
 paper_2508_06024_amd/libec2moe.so next to this file. With --incremental, sources whose
-object is newer than the source and every header under csrc/ and include/ are not
+object is newer than the source and every project header it includes are not
 recompiled (a development shortcut; the default rebuilds everything).
 """
 from __future__ import annotations
@@ -34,10 +34,22 @@ def sources():
     return sorted(f for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
 
 
-def _headers_mtime() -> float:
-    hs = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".h")]
-    hs += [os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h")]
-    return max(os.path.getmtime(h) for h in hs)
+def _deps(path: str, seen=None) -> set:
+    """The file and every project header it includes, transitively (#include "...")."""
+    seen = set() if seen is None else seen
+    if path in seen:
+        return seen
+    seen.add(path)
+    for line in open(path):
+        line = line.strip()
+        if line.startswith('#include "'):
+            name = line.split('"')[1]
+            for d in (CSRC, INCLUDE):
+                cand = os.path.join(d, name)
+                if os.path.exists(cand):
+                    _deps(cand, seen)
+                    break
+    return seen
 
 
 def _up_to_date(src: str) -> bool:
@@ -45,7 +57,7 @@ def _up_to_date(src: str) -> bool:
     if not os.path.exists(obj):
         return False
     t = os.path.getmtime(obj)
-    return t > os.path.getmtime(os.path.join(CSRC, src)) and t > _headers_mtime()
+    return all(t > os.path.getmtime(f) for f in _deps(os.path.join(CSRC, src)))
 
 
 def _compile(src: str) -> str:

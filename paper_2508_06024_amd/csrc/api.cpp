@@ -175,13 +175,16 @@ int codec_batch(const ec2moe_codec_desc* d) {
     return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({fit, kMaxCodecBatch, std::max(1, d->n_slices)})));
 }
 
-// Token chunk of the U^T P contraction: about one workgroup per CU over (slice, chunk,
-// 64-column block) triples, in multiples of 4 tokens.
-int utp_chunk(int h, int r_w, int slices) {
+// Token chunk of the U^T P contraction over (slice, chunk, 64-column block) workgroups:
+// bfloat16 layers (three bf16 products per float32 one, about 1/5 of the float32 matrix-core
+// time) aim at 128 workgroups of whole 64-token stages, halving the partial sums; float32
+// layers at one workgroup per CU, in multiples of 4 tokens.
+int utp_chunk(int h, int r_w, int slices, DType dt) {
     const int col_blocks = (r_w + 63) / 64;
-    const int target = std::max(1, 256 / (col_blocks * slices));
+    const bool bf16 = dt == DType::BF16;
+    const int target = std::max(1, (bf16 ? 128 : 256) / (col_blocks * slices));
     const int tc = (std::max(1, h) + target - 1) / target;
-    return (tc + 3) & ~3;
+    return bf16 ? (tc + 63) & ~63 : (tc + 3) & ~3;
 }
 
 CodecWs codec_ws(const ec2moe_codec_desc* d) {
@@ -189,7 +192,7 @@ CodecWs codec_ws(const ec2moe_codec_desc* d) {
     CodecWs w{};
     w.batch = codec_batch(d);
     const size_t nb = static_cast<size_t>(w.batch);
-    w.tc = utp_chunk(d->h, d->r_w, w.batch);
+    w.tc = utp_chunk(d->h, d->r_w, w.batch, static_cast<DType>(d->dtype));
     const size_t chunks = (static_cast<size_t>(std::max(1, d->h)) + w.tc - 1) / w.tc;
     size_t o = 0;
     w.gpart = o; o += up(gemm_split_scratch_bytes());

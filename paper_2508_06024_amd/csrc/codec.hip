@@ -1,6 +1,7 @@
 // Helpers of the low-rank codec (Encoder-Decoder based on Low-Rank Compression) for
-// gfx950: a tiled transpose, the float32 contraction Z = U^T P of the encoder (P = X V in
-// float32, so Z keeps float32 accuracy), its in-order reduction over token chunks, and the
+// gfx950: a tiled transpose, the contraction Z = U^T P of the encoder at float32 accuracy
+// (P = X V in float32; bfloat16 U on the bf16 matrix cores with P split in three bf16
+// planes, float32 U on the float32 matrix cores), its in-order reduction over token chunks, and the
 // float32 -> bfloat16 rounding of Z for the decoder. The large products X V, V_hat Z^T and
 // U_hat W^T run on the matrix-core GEMM.
 #include "device_common.h"
@@ -168,6 +169,156 @@ __global__ __launch_bounds__(256) void utp_kernel(UtpArgs g) {
             }
 }
 
+// Z = U^T P with bfloat16 U on the bfloat16 matrix cores at float32 accuracy. Each float32
+// value of P is split exactly into three bfloat16 values, p = hi + mid + lo up to 2^-27 |p|
+// (hi = bf16(p), mid = bf16(p - hi), lo = bf16(p - hi - mid); each difference is exact in
+// float32), and the three products with U, all exact in float32, are accumulated in
+// float32: the same order of accuracy as a float32 contraction, at 3/16 of its matrix-core
+// cost. Tokens are the contraction axis, so a stage of 64 tokens is staged transposed in
+// LDS: U^T as [r][t] rows (an 8x8 register transpose of 16-byte loads) and each plane of P
+// as [c][t] rows, 128 bytes per row with the GEMM's chunk swizzle (chunk i of row R at
+// i ^ ((R >> 1) & 7)). Wave w owns rows 64 w .. 64 w + 63 of this workgroup's 64 columns:
+// 2 x 2 blocks of v_mfma_f32_32x32x16_bf16 (lane l: column l % 32 of a block, rows
+// 8 (q / 4) + 4 (l / 32) + q % 4 in register q). Tokens past the chunk are zero in every
+// operand. Partials per token chunk as in utp_kernel.
+constexpr int kU3T = 64;  // tokens per LDS stage
+constexpr int kU3C = 64;  // columns of P per workgroup
+
+__device__ __forceinline__ uint32_t bf16_pair(uint4 a, uint4 b, int j) {
+    const uint32_t wa = (&a.x)[j >> 1] >> (16 * (j & 1));
+    const uint32_t wb = (&b.x)[j >> 1] >> (16 * (j & 1));
+    return (wa & 0xffffu) | (wb << 16);
+}
+
+__global__ __launch_bounds__(256) void utp3_kernel(UtpArgs g) {
+    __shared__ __attribute__((aligned(1024))) char lds_u[256 * 128];      // U^T [r][64 tokens]
+    __shared__ __attribute__((aligned(1024))) char lds_p[3 * kU3C * 128];  // P^T planes [3][c][64 tokens]
+    const int c0 = blockIdx.x * kU3C;
+    const int tb = blockIdx.y * g.tc;
+    const int te = min(g.T, tb + g.tc);
+    const float* ps = g.p + static_cast<int64_t>(blockIdx.z) * g.T * g.rw;
+    const bf16_t* u = static_cast<const bf16_t*>(g.u);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int l32 = lane & 31, lh = lane >> 5;
+    const int sw = (l32 >> 1) & 7;
+    const int rbase = wave * 64;
+    const bool active = rbase < g.rh;
+    const int rgroups = ((g.rh + 63) & ~63) / 8;  // 8-row groups of U^T staged (zeros past r_h)
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+
+    // Per stage each thread holds at most one U item (8 tokens x 8 rows: 8 * rgroups <= 256)
+    // and one P item (8 tokens x 2 columns). The next stage's loads are issued before this
+    // stage's matrix-core work, so they fly while it runs.
+    const bool has_u = tid < 8 * rgroups;
+    const int urg = tid % rgroups, utg = tid / rgroups;
+    const int pcg = tid % 32, ptg = tid / 32;
+    const int pc = c0 + pcg * 2;
+    uint4 rowv[8];
+    float2 pv[8];
+    auto load_stage = [&](int t0) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int t = t0 + utg * 8 + q;
+            rowv[q] = (has_u && t < te && urg * 8 < g.rh) ? ldg16(u + static_cast<int64_t>(t) * g.rh + urg * 8)
+                                                          : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int t = t0 + ptg * 8 + q;
+            pv[q] = (t < te && pc < g.rw) ? *reinterpret_cast<const float2*>(ps + static_cast<int64_t>(t) * g.rw + pc)
+                                          : make_float2(0.f, 0.f);
+        }
+    };
+    if (tb < te) load_stage(tb);
+    for (int t0 = tb; t0 < te; t0 += kU3T) {
+        // U^T rows r0 .. r0 + 7, 8 tokens of group utg: an 8 x 8 transpose in registers
+        if (has_u) {
+            const int r0 = urg * 8;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int R = r0 + j;
+                const uint4 o = make_uint4(bf16_pair(rowv[0], rowv[1], j), bf16_pair(rowv[2], rowv[3], j),
+                                           bf16_pair(rowv[4], rowv[5], j), bf16_pair(rowv[6], rowv[7], j));
+                *reinterpret_cast<uint4*>(lds_u + R * 128 + ((utg ^ ((R >> 1) & 7)) * 16)) = o;
+            }
+        }
+        // P^T planes: columns pc, pc + 1, each value split into hi, mid, lo
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+            uint32_t hw[4], mw[4], lw[4];
+#pragma unroll
+            for (int q = 0; q < 8; q += 2) {
+                uint32_t hb[2], mb[2], lb[2];
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const float v = cc ? pv[q + e].y : pv[q + e].x;
+                    const uint16_t h = f32_to_bf16(v);
+                    const float r1 = v - bf16_to_f32(h);
+                    const uint16_t m = f32_to_bf16(r1);
+                    const float r2 = r1 - bf16_to_f32(m);
+                    hb[e] = h;
+                    mb[e] = m;
+                    lb[e] = f32_to_bf16(r2);
+                }
+                hw[q / 2] = hb[0] | (hb[1] << 16);
+                mw[q / 2] = mb[0] | (mb[1] << 16);
+                lw[q / 2] = lb[0] | (lb[1] << 16);
+            }
+            const int R = pcg * 2 + cc;
+            const int off = R * 128 + ((ptg ^ ((R >> 1) & 7)) * 16);
+            *reinterpret_cast<uint4*>(lds_p + 0 * kU3C * 128 + off) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+            *reinterpret_cast<uint4*>(lds_p + 1 * kU3C * 128 + off) = make_uint4(mw[0], mw[1], mw[2], mw[3]);
+            *reinterpret_cast<uint4*>(lds_p + 2 * kU3C * 128 + off) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+        }
+        __syncthreads();
+        if (t0 + kU3T < te) load_stage(t0 + kU3T);
+        if (active) {
+#pragma unroll
+            for (int s = 0; s < kU3T / 16; ++s) {
+                const int ch = ((2 * s + lh) ^ sw) * 16;
+                uint4 a[2], b[3][2];
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb) a[rb] = *reinterpret_cast<const uint4*>(lds_u + (rbase + rb * 32 + l32) * 128 + ch);
+#pragma unroll
+                for (int j = 0; j < 3; ++j)
+#pragma unroll
+                    for (int cb = 0; cb < 2; ++cb)
+                        b[j][cb] = *reinterpret_cast<const uint4*>(lds_p + (j * kU3C + cb * 32 + l32) * 128 + ch);
+#pragma unroll
+                for (int j = 0; j < 3; ++j)
+#pragma unroll
+                    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+                        for (int cb = 0; cb < 2; ++cb)
+                            acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                __builtin_bit_cast(bf16x8, a[rb]), __builtin_bit_cast(bf16x8, b[j][cb]), acc[rb][cb], 0, 0,
+                                0);
+            }
+        }
+        __syncthreads();
+    }
+    if (!active) return;
+    float* part = g.part + (static_cast<int64_t>(blockIdx.z) * gridDim.y + blockIdx.y) * g.rh * g.rw;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int r = rbase + rb * 32 + 8 * (q / 4) + 4 * lh + (q % 4);
+                const int c = c0 + cb * 32 + l32;
+                if (r < g.rh && c < g.rw) part[static_cast<int64_t>(r) * g.rw + c] = acc[rb][cb][q];
+            }
+}
+
 // dst[i] = round-to-nearest-even bfloat16 of src[i], four elements per thread (n a multiple of 4)
 __global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ src, int64_t n,
                                                           bf16_t* __restrict__ dst) {
@@ -264,9 +415,10 @@ hipError_t launch_transpose(DType dt, const void* src, int rows, int cols, void*
 hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s) {
     const int chunks = (g.T + g.tc - 1) / g.tc;
     dim3 grid((g.rw + kUtpC - 1) / kUtpC, chunks, g.slices);
+    static_assert(kUtpC == kU3C, "both contractions tile P by the same column blocks");
     {
         ProfileScope prof("codec_utp", s);
-        if (udt == DType::BF16) hipLaunchKernelGGL(utp_kernel<bf16_t>, grid, dim3(256), 0, s, g);
+        if (udt == DType::BF16) hipLaunchKernelGGL(utp3_kernel, grid, dim3(256), 0, s, g);
         else hipLaunchKernelGGL(utp_kernel<float>, grid, dim3(256), 0, s, g);
     }
     hipError_t e = hipGetLastError();

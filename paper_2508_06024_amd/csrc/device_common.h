@@ -26,6 +26,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));  // accumulators of a 32x32 matrix-core block
 
 // Element traits: how many elements fill one 16-byte chunk and how a chunk of the
 // token operand and a chunk of the weight operand feed the 16x16 matrix core.

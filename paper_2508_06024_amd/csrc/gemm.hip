@@ -409,7 +409,6 @@ __device__ __forceinline__ i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
     return r;
 }
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 // Writes a wave's 32x32-block accumulators. After v_mfma_f32_32x32x16 with weight rows as A

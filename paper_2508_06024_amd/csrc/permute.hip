@@ -1,14 +1,15 @@
 // Dispatch of (token, slot) assignments to per-expert segments, for gfx950.
 //
 // The assignments a = t*k + j are sorted stably by expert id with integer work only:
-//   1. count:   each 4096-assignment chunk builds an LDS histogram over the experts;
+//   1. count:   each 1024-assignment chunk builds an LDS histogram over the experts;
 //   2. scan:    one workgroup turns the chunk counts into segment offsets and the
 //               first position of every (chunk, expert) pair;
-//   3. scatter: each wave walks 1024 consecutive assignments 64 at a time; lanes with
+//   3. scatter: each wave walks 256 consecutive assignments 64 at a time; lanes with
 //               the same expert find each other with one ballot per bit of the expert
 //               id, so the rank inside the 64 comes from a popcount and the order of
 //               the input is kept.
-// Up to 8192 assignments the three steps run in one workgroup (one launch instead of three).
+// Up to 65536 assignments the three steps run in one launch (perm_onepass_kernel), with
+// the counts of step 1 recomputed by every workgroup instead of exchanged through memory.
 // No floating point and no global atomics: the result is unique and deterministic.
 #include "device_common.h"
 #include "internal.h"
@@ -169,52 +170,65 @@ __global__ __launch_bounds__(256) void perm_scatter_kernel(const int32_t* __rest
     }
 }
 
-// The three steps in one workgroup of 16 waves, for up to kSmallMax assignments: wave w
-// takes the w-th of 16 consecutive ranges, so the input order is kept across waves as it is
-// across chunks above; the segment offsets come from a wave-level scan over the experts.
-constexpr int kSmallWaves = 16;
-constexpr int64_t kSmallMax = 8192;
+// Up to kOnePassMax assignments the three steps take one launch and need no workspace: a
+// workgroup per chunk of kPermChunk assignments, each counting the whole index array (a few
+// tens of KB, read from L2) split into the assignments before its chunk, in it (per wave)
+// and after it. That gives every segment's offset and the position of the chunk inside each
+// segment without any exchange between workgroups; wave w then scatters the w-th run of 64
+// assignments of the chunk with ballot ranks, which keep the input order.
+constexpr int kOneWaves = kPermChunk / 64;  // one 64-assignment run per wave
+constexpr int64_t kOnePassMax = 65536;      // the redundant counting reads n^2 / 1024 indices in all
 
-__global__ __launch_bounds__(64 * kSmallWaves) void perm_small_kernel(const int32_t* __restrict__ idx, int64_t n,
+__global__ __launch_bounds__(64 * kOneWaves) void perm_onepass_kernel(const int32_t* __restrict__ idx, int64_t n,
                                                                       int top_k, int M, int32_t* __restrict__ seg,
                                                                       int32_t* __restrict__ perm_src,
                                                                       int32_t* __restrict__ inv_perm) {
-    __shared__ int wpos[kSmallWaves][256];  // counts per (wave, expert), then first positions
-    __shared__ int total[256];
+    constexpr int NT = 64 * kOneWaves;
+    __shared__ int before[256];              // assignments to each expert before this chunk
+    __shared__ int after[256];               // ... after it
+    __shared__ int start[256];               // expert totals, then segment offsets
+    __shared__ int wpos[kOneWaves][256];     // this chunk's counts per (wave, expert), then positions
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    for (int i = threadIdx.x; i < kSmallWaves * 256; i += 64 * kSmallWaves) (&wpos[0][0])[i] = 0;
+    for (int i = threadIdx.x; i < 256; i += NT) {
+        before[i] = 0;
+        after[i] = 0;
+    }
+    for (int i = threadIdx.x; i < kOneWaves * 256; i += NT) (&wpos[0][0])[i] = 0;
     __syncthreads();
-    const int64_t per = (n + kSmallWaves - 1) / kSmallWaves;
-    const int64_t wbeg = wave * per;
-    const int64_t wend = std::min<int64_t>(n, wbeg + per);
-    // the wave's expert ids are read 8 passes of 64 at a time (loads in flight together)
-    constexpr int U = 8;
-    for (int64_t s0 = wbeg; s0 < wend; s0 += 64 * U) {
+    const int64_t cbeg = static_cast<int64_t>(blockIdx.x) * kPermChunk;
+    const int64_t cend = std::min<int64_t>(n, cbeg + kPermChunk);
+    const int64_t a_mine = cbeg + 64 * wave + lane;
+    const int e_mine = a_mine < cend ? idx[a_mine] : -1;
+    const bool valid = e_mine >= 0 && e_mine < M;
+    // everything outside the chunk, U loads in flight per thread
+    constexpr int U = 16;
+    for (int64_t s0 = 0; s0 < n; s0 += static_cast<int64_t>(NT) * U) {
         int ev[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t a = s0 + 64 * u + lane;
-            ev[u] = a < wend ? idx[a] : -1;
+            const int64_t a = s0 + static_cast<int64_t>(NT) * u + threadIdx.x;
+            ev[u] = (a < n && (a < cbeg || a >= cend)) ? idx[a] : -1;
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (ev[u] >= 0 && ev[u] < M) atomicAdd(&wpos[wave][ev[u]], 1);
+        for (int u = 0; u < U; ++u) {
+            const int64_t a = s0 + static_cast<int64_t>(NT) * u + threadIdx.x;
+            if (ev[u] >= 0 && ev[u] < M) atomicAdd(a < cbeg ? &before[ev[u]] : &after[ev[u]], 1);
+        }
     }
+    if (valid) atomicAdd(&wpos[wave][e_mine], 1);
     __syncthreads();
-    // per expert: offsets of the waves' runs inside its segment, and its total
+    // per expert: the waves' runs inside the chunk, and the expert's total
     if (threadIdx.x < M) {
         const int e = threadIdx.x;
-        int c[kSmallWaves];
-#pragma unroll
-        for (int w = 0; w < kSmallWaves; ++w) c[w] = wpos[w][e];
         int run = 0;
 #pragma unroll
-        for (int w = 0; w < kSmallWaves; ++w) {
+        for (int w = 0; w < kOneWaves; ++w) {
+            const int c = wpos[w][e];
             wpos[w][e] = run;
-            run += c[w];
+            run += c;
         }
-        total[e] = run;
+        start[e] = before[e] + run + after[e];
     }
     __syncthreads();
     // exclusive scan of the totals over experts: lane l of wave 0 owns experts 4 l .. 4 l + 3
@@ -223,7 +237,7 @@ __global__ __launch_bounds__(64 * kSmallWaves) void perm_small_kernel(const int3
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = 4 * lane + q;
-            v[q] = e < M ? total[e] : 0;
+            v[q] = e < M ? start[e] : 0;
             sum += v[q];
         }
         int inc = sum;
@@ -237,62 +251,37 @@ __global__ __launch_bounds__(64 * kSmallWaves) void perm_small_kernel(const int3
         for (int q = 0; q < 4; ++q) {
             const int e = 4 * lane + q;
             if (e < M) {
-                total[e] = run;
-                seg[e] = run;
+                start[e] = run;
+                if (blockIdx.x == 0) seg[e] = run;
             }
             run += v[q];
         }
-        if (lane == 63) seg[M] = inc;
+        if (blockIdx.x == 0 && lane == 63) seg[M] = inc;
     }
     __syncthreads();
     if (threadIdx.x < M) {
         const int e = threadIdx.x;
-        const int start = total[e];
+        const int base = start[e] + before[e];
 #pragma unroll
-        for (int w = 0; w < kSmallWaves; ++w) wpos[w][e] += start;
+        for (int w = 0; w < kOneWaves; ++w) wpos[w][e] += base;
     }
     __syncthreads();
-
+    if (a_mine >= cend) return;  // the wave's run ends inside the chunk: the ballots below skip these lanes
     int nbits = 0;
     while ((1 << nbits) < M) ++nbits;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
-    for (int64_t s1 = wbeg; s1 < wend; s1 += 64 * U) {
-    int ev[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t a = s1 + 64 * u + lane;
-        ev[u] = a < wend ? idx[a] : -1;
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < nbits; ++b) {
+        const bool bit = valid && ((e_mine >> b) & 1);
+        const uint64_t ones = __ballot(bit);
+        peers &= bit ? ones : ~ones;
     }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t s0 = s1 + 64 * u;
-        if (s0 >= wend) break;
-        const int64_t a = s0 + lane;
-        int e = -1;
-        if (a < wend) {
-            e = ev[u];
-            if (e < 0 || e >= M) {
-                inv_perm[a] = -1;
-                e = -1;
-            }
-        }
-        const bool valid = e >= 0;
-        uint64_t peers = __ballot(valid);
-        for (int b = 0; b < nbits; ++b) {
-            const bool bit = valid && ((e >> b) & 1);
-            const uint64_t ones = __ballot(bit);
-            peers &= bit ? ones : ~ones;
-        }
-        if (valid) {
-            const int rank = __popcll(peers & lt_mask);
-            const int pos = wpos[wave][e] + rank;
-            perm_src[pos] = static_cast<int32_t>(a / top_k);
-            inv_perm[a] = pos;
-        }
-        __builtin_amdgcn_wave_barrier();
-        if (valid && (peers & lt_mask) == 0) wpos[wave][e] += __popcll(peers);
-        __builtin_amdgcn_wave_barrier();
-    }
+    if (valid) {
+        const int pos = wpos[wave][e_mine] + __popcll(peers & lt_mask);
+        perm_src[pos] = static_cast<int32_t>(a_mine / top_k);
+        inv_perm[a_mine] = pos;
+    } else {
+        inv_perm[a_mine] = -1;
     }
 }
 
@@ -319,9 +308,10 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const char* __restrict
 hipError_t launch_permute(const int32_t* topk_idx, int64_t n_assign, int top_k, int n_experts,
                           int32_t* chunk_counts, int32_t* seg_offsets, int32_t* perm_src,
                           int32_t* inv_perm, hipStream_t s) {
-    if (n_assign <= kSmallMax) {
-        ProfileScope prof("perm_small", s);
-        hipLaunchKernelGGL(perm_small_kernel, dim3(1), dim3(64 * kSmallWaves), 0, s, topk_idx, n_assign, top_k,
+    if (n_assign <= kOnePassMax) {
+        ProfileScope prof("perm_onepass", s);
+        const int grid = std::max(1, perm_chunks(n_assign));
+        hipLaunchKernelGGL(perm_onepass_kernel, dim3(grid), dim3(64 * kOneWaves), 0, s, topk_idx, n_assign, top_k,
                            n_experts, seg_offsets, perm_src, inv_perm);
         return hipGetLastError();
     }

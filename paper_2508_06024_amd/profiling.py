@@ -3,6 +3,8 @@
     python -m paper_2508_06024_amd.profiling stats <run_kernel_stats.csv> --command "<cmd>" [-o out.md]
     python -m paper_2508_06024_amd.profiling traffic --fetch <fetch counter csv> --write <write counter csv>
         --kernel <substring> --copy-mib N --workload NAME --command "<cmd>" [-o out.json]
+    python -m paper_2508_06024_amd.profiling counters --mfma <csv> --fetch <csv> --write <csv>
+        --copy-mib N --command "<cmd>" [-o out.md]
 
 HBM bytes of a kernel come from FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
 scaled by the ratio of the known bytes of a plain elementwise pass over N MiB (the
@@ -94,6 +96,72 @@ def traffic(fetch_csv: str, write_csv: str, kernel: str, copy_mib: int):
             "hbm_bytes_per_launch": (f_kib * f_scale + w_kib * w_scale) * 1024.0}
 
 
+def _per_dispatch(path: str):
+    """{dispatch id: (kernel name, duration ns, {counter: value summed over instances})}."""
+    out = {}
+    for r in csv.DictReader(open(path)):
+        did = r.get("Dispatch_Id") or r.get("Correlation_Id")
+        if did not in out:
+            out[did] = [r["Kernel_Name"], int(r["End_Timestamp"]) - int(r["Start_Timestamp"]), defaultdict(float)]
+        out[did][2][r["Counter_Name"]] += float(r["Counter_Value"])
+    return out
+
+
+def counters_summary(mfma_csv: str, fetch_csv: str, write_csv: str, copy_mib: int, command: str,
+                     xcds: int = 8, simds: int = 1024) -> str:
+    """Per kernel: matrix-core busy fraction and clock (SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE)
+    and HBM bytes (FETCH_SIZE, WRITE_SIZE scaled by the copy calibration), averaged over its
+    dispatches. GRBM_GUI_ACTIVE sums the active cycles of every XCD, so the kernel's clock is
+    GUI / xcds / duration and its SIMD-cycles GUI / xcds * simds; a 32x32x16 bf16 MFMA keeps a
+    SIMD's matrix core busy for 32 of them."""
+    m = _per_dispatch(mfma_csv)
+    f = _per_dispatch(fetch_csv)
+    w = _per_dispatch(write_csv)
+
+    def calib(d, counter):
+        vals = [c[counter] for n, _, c in d.values() if "elementwise" in n and counter in c]
+        if not vals:
+            raise KeyError("no elementwise calibration dispatch")
+        return copy_mib * 1024.0 / max(vals)
+
+    fs, ws = calib(f, "FETCH_SIZE"), calib(w, "WRITE_SIZE")
+    rows = defaultdict(lambda: defaultdict(list))
+    for d, key in ((m, "m"), (f, "f"), (w, "w")):
+        for name, dur, c in d.values():
+            if "elementwise" in name or "rocclr" in name:
+                continue
+            r = rows[short_name(name)]
+            r["dur_" + key].append(dur)
+            for cn, v in c.items():
+                r[cn].append(v)
+    avg = lambda v: sum(v) / len(v) if v else float("nan")
+    lines = ["# rocprofv3 counters per kernel", "", f"command: `{command}`", "",
+             f"date: {datetime.date.today().isoformat()}", "",
+             f"FETCH_SIZE scaled by {fs:.3f} and WRITE_SIZE by {ws:.3f} (a plain elementwise pass over "
+             f"{copy_mib} MiB reads and writes {copy_mib} MiB); durations are those of the counter runs "
+             "(dispatches serialised by the profiler). GRBM_GUI_ACTIVE counts the GPU's busy cycles over "
+             "the counter window, which for a dispatch of a few microseconds includes its launch and "
+             "drain: MFMA busy and clock are shown for dispatches above 100 us only.", "",
+             "| kernel | dispatches | avg us | MFMA busy | clock GHz | HBM read MB | HBM write MB | GB/s |",
+             "|---|---|---|---|---|---|---|---|"]
+    for name, r in rows.items():
+        dur_m = avg(r["dur_m"])
+        gui = avg(r["GRBM_GUI_ACTIVE"])
+        busy = avg(r["SQ_VALU_MFMA_BUSY_CYCLES"])
+        long = r["GRBM_GUI_ACTIVE"] and dur_m > 100e3
+        util = busy / (gui / xcds * simds) if long else float("nan")
+        clk = gui / xcds / dur_m if long else float("nan")
+        rd = avg(r["FETCH_SIZE"]) * fs * 1024 / 1e6
+        wr = avg(r["WRITE_SIZE"]) * ws * 1024 / 1e6
+        dur_fw = avg(r["dur_f"] + r["dur_w"])
+        gbs = (rd + wr) * 1e6 / (dur_fw * 1e-9) / 1e9 if dur_fw > 0 else float("nan")
+        ut = f"{util:.1%}" if util == util else "-"
+        ck = f"{clk:.2f}" if clk == clk else "-"
+        lines.append(f"| {name} | {len(r['dur_m']) or len(r['dur_f'])} | {dur_m / 1e3:.2f} | {ut} | {ck} | "
+                     f"{rd:.1f} | {wr:.1f} | {gbs:.0f} |")
+    return "\n".join(lines) + "\n"
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -103,6 +171,13 @@ def main(argv=None):
     s.add_argument("--bench-json", help="the bench.py JSON line of the same run: its HIP-event "
                                         "averages are listed beside the profiler's")
     s.add_argument("-o", "--out")
+    c = sub.add_parser("counters")
+    c.add_argument("--mfma", required=True, help="csv of a run with GRBM_GUI_ACTIVE and SQ_VALU_MFMA_BUSY_CYCLES")
+    c.add_argument("--fetch", required=True)
+    c.add_argument("--write", required=True)
+    c.add_argument("--copy-mib", type=int, required=True)
+    c.add_argument("--command", required=True)
+    c.add_argument("-o", "--out")
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
@@ -114,7 +189,9 @@ def main(argv=None):
     t.add_argument("--command", required=True)
     t.add_argument("-o", "--out")
     a = ap.parse_args(argv)
-    if a.cmd == "stats":
+    if a.cmd == "counters":
+        text = counters_summary(a.mfma, a.fetch, a.write, a.copy_mib, a.command)
+    elif a.cmd == "stats":
         text = stats_summary(a.csv, a.command)
         if a.bench_json:
             rec = json.loads(open(a.bench_json).read().strip().splitlines()[-1])
