@@ -125,15 +125,34 @@ def counters_summary(mfma_csv: str, fetch_csv: str, write_csv: str, copy_mib: in
         return copy_mib * 1024.0 / max(vals)
 
     fs, ws = calib(f, "FETCH_SIZE"), calib(w, "WRITE_SIZE")
+    # one kernel serving launches of very different sizes (the same GEMM for a codec product
+    # and an expert layer): its dispatches are split at the geometric mean of the extremes when
+    # they differ by more than 5x
+    # the passes run the same launch sequence: the i-th dispatch of a kernel is the same launch
+    # in every pass, classified by the median of its durations
+    def ordered(d):
+        out = defaultdict(list)
+        for did in sorted(d, key=lambda x: int(x)):
+            name, dur, c = d[did]
+            out[short_name(name)].append((dur, c))
+        return out
+    om, of_, ow = ordered(m), ordered(f), ordered(w)
     rows = defaultdict(lambda: defaultdict(list))
-    for d, key in ((m, "m"), (f, "f"), (w, "w")):
-        for name, dur, c in d.values():
-            if "elementwise" in name or "rocclr" in name:
-                continue
-            r = rows[short_name(name)]
-            r["dur_" + key].append(dur)
-            for cn, v in c.items():
-                r[cn].append(v)
+    for n in om:
+        if "elementwise" in n or "rocclr" in n:
+            continue
+        per = [om[n], of_.get(n, []), ow.get(n, [])]
+        k = min(len(x) for x in per)
+        med = [sorted(x[i][0] for x in per)[1] for i in range(k)]
+        lo, hi = (min(med), max(med)) if med else (0, 0)
+        cut = (lo * hi) ** 0.5 if lo > 0 and hi > 5 * lo else None
+        for i in range(k):
+            name = n if cut is None else n + (" (long launches)" if med[i] > cut else " (short launches)")
+            r = rows[name]
+            for (dur, c), key in zip((per[0][i], per[1][i], per[2][i]), ("m", "f", "w")):
+                r["dur_" + key].append(dur)
+                for cn, v in c.items():
+                    r[cn].append(v)
     avg = lambda v: sum(v) / len(v) if v else float("nan")
     lines = ["# rocprofv3 counters per kernel", "", f"command: `{command}`", "",
              f"date: {datetime.date.today().isoformat()}", "",
