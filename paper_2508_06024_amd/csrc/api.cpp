@@ -617,7 +617,7 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
 namespace {
 
 struct FitWs {
-    size_t gpart, gram, xt, q, y, q1, qt, g64, g64part, rinv64, rinv_t, total;
+    size_t gpart, gram, xt, q, y, q1, qt, g64, g64part, rinv_t, total;
 };
 
 FitWs fit_ws(const ec2moe_codec_desc* d) {
@@ -637,7 +637,6 @@ FitWs fit_ws(const ec2moe_codec_desc* d) {
     w.g64 = o; o += up(r * r * 8);
     const int chunks = std::max(gram64_chunks(d->h, static_cast<int>(d->r_h)), gram64_chunks(d->w, static_cast<int>(d->r_w)));
     w.g64part = o; o += up(static_cast<size_t>(chunks) * r * r * 8);
-    w.rinv64 = o; o += up(r * r * 8);
     w.rinv_t = o; o += up(r * r * 4);
     w.total = o;
     return w;
@@ -662,7 +661,7 @@ hipError_t orthonormalise(float* y, int n, int r, float* q1, float* q, const Fit
     for (int pass = 0; pass < 2; ++pass) {
         float* dst = pass == 0 ? q1 : q;
         hipError_t e = launch_gram64(src, n, r, at<double>(ws, w.g64part), g64, s);
-        if (e == hipSuccess) e = launch_chol_inv(g64, r, rinv_t, at<double>(ws, w.rinv64), status, reset, s);
+        if (e == hipSuccess) e = launch_chol_inv(g64, r, rinv_t, status, reset, s);
         reset = false;
         if (e == hipSuccess) e = dense_gemm(DType::F32, OutType::Same, src, rinv_t, n, r, r, dst, "fit_qr", part, s);
         if (e != hipSuccess) return e;

@@ -72,165 +72,228 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const double* __restri
     }
 }
 
-constexpr int kPanel = 32;  // columns per panel of the blocked Cholesky factor and inverse
+// Cholesky factor and triangular inverse of one r x r float64 Gram matrix (r <= 256, a
+// multiple of 16) in one workgroup of 512 threads, with the matrix held in registers:
+// thread (ti, tj) = (tid / 32, tid % 32) owns the entries (16 a + ti, 32 b + tj) of the
+// blocks (a, b) that meet the upper triangle (a <= 2 b + 1: 72 of the 128 blocks, 144
+// registers). Each of the 2 r steps publishes one row (and column) through LDS, double
+// buffered by the parity of the step, so one barrier per step suffices; every thread then
+// applies the step to its entries with multipliers that are zero where the step changes
+// nothing, so the update is branch-free. The steps run in four phases of 64; a phase
+// leaves out, at compile time, the blocks that none of its steps can change.
+//   factor (right-looking, a rank-1 update per column): with d = A[k][k],
+//     A[i][j] -= A[k][i] A[k][j] / d for i, j > k, and row k becomes R[k][j] = A[k][j] / sqrt(d)
+//     for j >= k (zero left of the diagonal); a pivot that is not positive sets the status
+//     and is replaced by 1;
+//   inverse (Gauss-Jordan elimination on R, in place; the triangle is preserved): with
+//     q = 1 / R[k][k], A[i][j] -= A[i][k] q A[k][j] for i < k < j, column k above the
+//     diagonal becomes -A[i][k] q, and row k becomes q A[k][j] (q on the diagonal).
+// Outputs rinv_t[n][k] = R^-1[k][n] in float32 (the weight layout of the GEMM for Y R^-1).
+constexpr int kCholThreads = 512;
+constexpr int kCholRB = 16;  // row blocks: row 16 a + ti
+constexpr int kCholCB = 8;   // column blocks: column 32 b + tj
 
-// Cholesky factor of g (r x r, float64, symmetric positive definite, r <= 256): g = R^T R
-// with R upper triangular, overwriting g's upper triangle, then R^-1 (rinv, float64) and
-// rinv_t[n][k] = R^-1[k][n] in float32 (the weight layout of the GEMM for Y R^-1). A pivot
-// that is not positive sets *status to 1 and is replaced by 1, so the outputs stay finite;
-// reset: *status = 0 first. One workgroup; blocked by panels of 32 columns:
-//   factor: per panel, the diagonal block in LDS (column steps), the panel rows by
-//   forward substitution (a thread per column), then the rank-32 update of the trailing
-//   upper triangle from the panel kept in LDS;
-//   inverse: the diagonal blocks' inverses in LDS, then X_ij = -X_ii (sum_k R_ik X_kj) for
-//   the blocks above the diagonal, block column by block column, rows upward.
-__global__ __launch_bounds__(256) void chol_inv_kernel(double* __restrict__ g, int r, float* __restrict__ rinv_t,
-                                                        double* __restrict__ rinv, int32_t* __restrict__ status,
-                                                        int reset) {
-    __shared__ double dl[kPanel][kPanel + 1];
-    __shared__ double pl[kPanel][256];  // the panel rows of R right of the diagonal block
-    __shared__ double piv;
-    __shared__ int bad;
+__host__ __device__ constexpr bool chol_kept(int a, int b) { return a <= 2 * b + 1; }
+
+// 1 / sqrt(d) and 1 / p for d, p > 0 (the pivots): the hardware estimates refined by two
+// Newton steps each, to within a few units in the last place of float64
+__device__ __forceinline__ double rsqrt64(double d) {
+    double y = __builtin_amdgcn_rsq(d);
+    const double h = 0.5 * d;
+#pragma unroll
+    for (int n = 0; n < 2; ++n) y = y * fma(-h * y, y, 1.5);
+    return y;
+}
+__device__ __forceinline__ double rcp64(double p) {
+    double q = __builtin_amdgcn_rcp(p);
+#pragma unroll
+    for (int n = 0; n < 2; ++n) q = fma(q, fma(-p, q, 1.0), q);
+    return q;
+}
+
+// Reads the published values of a step: cols[b] = crow[32 b + tj] and rows[a] = rrow[16 a + ti],
+// every read issued before any is used.
+__device__ __forceinline__ void lds_step(const double* crow, const double* rrow, int tj, int ti,
+                                         double (&cols)[kCholCB], double (&rows)[kCholRB]) {
+#pragma unroll
+    for (int b = 0; b < kCholCB; ++b) cols[b] = crow[32 * b + tj];
+#pragma unroll
+    for (int a = 0; a < kCholRB; ++a) rows[a] = rrow[16 * a + ti];
+#pragma unroll
+    for (int b = 0; b < kCholCB; ++b) asm volatile("" : "+v"(cols[b]));
+#pragma unroll
+    for (int a = 0; a < kCholRB; ++a) asm volatile("" : "+v"(rows[a]));
+}
+
+struct CholLds {
+    double row[2][256];
+    double col[2][256];
+    int bad;
+};
+
+// Steps k in [64 P, 64 P + 64) of the factor. Row blocks a < 4 P hold finished rows and
+// column blocks b < 2 P only entries left of every pivot of the phase: neither changes.
+template <int P>
+__device__ __forceinline__ void chol_factor_phase(double (&m)[kCholRB][kCholCB], CholLds& sh, int r, int ti, int tj,
+                                                  int tid) {
+    constexpr int A0 = 4 * P, B0 = 2 * P;
+    const int kend = min(r, 64 * P + 64);
+    for (int k = 64 * P; k < kend; ++k) {
+        const int ak = k >> 4, buf = k & 1;
+        if (ti == (k & 15)) {
+#pragma unroll
+            for (int a = A0; a < kCholRB; ++a)
+                if (a == ak) {
+#pragma unroll
+                    for (int b = B0; b < kCholCB; ++b)
+                        if (chol_kept(a, b)) sh.row[buf][32 * b + tj] = m[a][b];
+                }
+        }
+        __syncthreads();
+        double d = sh.row[buf][k];
+        double v[kCholCB], ur[kCholRB];
+        lds_step(sh.row[buf], sh.row[buf], tj, ti, v, ur);
+        if (!(d > 0.0)) {
+            d = 1.0;
+            if (tid == 0) sh.bad = 1;
+        }
+        const double inv_s = rsqrt64(d), inv_d = inv_s * inv_s, sd = d * inv_s;
+        double vm[kCholCB];
+#pragma unroll
+        for (int b = B0; b < kCholCB; ++b) vm[b] = 32 * b + tj > k ? v[b] : 0.0;
+#pragma unroll
+        for (int a = A0; a < kCholRB; ++a) {
+            const double u = 16 * a + ti > k ? ur[a] * inv_d : 0.0;
+#pragma unroll
+            for (int b = B0; b < kCholCB; ++b)
+                if (chol_kept(a, b)) m[a][b] = fma(-u, vm[b], m[a][b]);
+        }
+        if (ti == (k & 15)) {
+#pragma unroll
+            for (int a = A0; a < kCholRB; ++a)
+                if (a == ak) {
+#pragma unroll
+                    for (int b = 0; b < kCholCB; ++b)
+                        if (chol_kept(a, b)) {
+                            const int j = 32 * b + tj;
+                            m[a][b] = j == k ? sd : (j > k ? v[b] * inv_s : 0.0);
+                        }
+                }
+        }
+    }
+}
+
+// Steps k in [64 P, 64 P + 64) of the inverse. Row blocks a > 4 P + 3 lie below every pivot
+// of the phase and column blocks b < 2 P left of it: neither changes.
+template <int P>
+__device__ __forceinline__ void chol_inverse_phase(double (&m)[kCholRB][kCholCB], CholLds& sh, int r, int ti, int tj) {
+    constexpr int A1 = 4 * P + 4, B0 = 2 * P;
+    const int kend = min(r, 64 * P + 64);
+    for (int k = 64 * P; k < kend; ++k) {
+        const int ak = k >> 4, bk = k >> 5, buf = k & 1;
+        if (ti == (k & 15)) {
+#pragma unroll
+            for (int a = 0; a < A1; ++a)
+                if (a == ak) {
+#pragma unroll
+                    for (int b = B0; b < kCholCB; ++b)
+                        if (chol_kept(a, b)) sh.row[buf][32 * b + tj] = m[a][b];
+                }
+        }
+        if (tj == (k & 31)) {
+#pragma unroll
+            for (int b = B0; b < kCholCB; ++b)
+                if (b == bk) {
+#pragma unroll
+                    for (int a = 0; a < A1; ++a)
+                        if (chol_kept(a, b)) sh.col[buf][16 * a + ti] = m[a][b];
+                }
+        }
+        __syncthreads();
+        const double p = sh.row[buf][k];
+        double rq[kCholCB], cr[kCholRB];
+        lds_step(sh.row[buf], sh.col[buf], tj, ti, rq, cr);
+        const double q = rcp64(p);
+        double rqm[kCholCB];
+#pragma unroll
+        for (int b = B0; b < kCholCB; ++b) rqm[b] = 32 * b + tj > k ? rq[b] * q : 0.0;
+#pragma unroll
+        for (int a = 0; a < A1; ++a) {
+            const double c = 16 * a + ti < k ? cr[a] : 0.0;
+#pragma unroll
+            for (int b = B0; b < kCholCB; ++b)
+                if (chol_kept(a, b)) m[a][b] = fma(-c, rqm[b], m[a][b]);
+        }
+        if (tj == (k & 31)) {
+#pragma unroll
+            for (int b = B0; b < kCholCB; ++b)
+                if (b == bk) {
+#pragma unroll
+                    for (int a = 0; a < A1; ++a)
+                        if (chol_kept(a, b)) m[a][b] = 16 * a + ti < k ? -cr[a] * q : m[a][b];
+                }
+        }
+        if (ti == (k & 15)) {
+#pragma unroll
+            for (int a = 0; a < A1; ++a)
+                if (a == ak) {
+#pragma unroll
+                    for (int b = B0; b < kCholCB; ++b)
+                        if (chol_kept(a, b)) {
+                            const int j = 32 * b + tj;
+                            m[a][b] = j == k ? q : (j > k ? rq[b] * q : m[a][b]);
+                        }
+                }
+        }
+    }
+}
+
+__global__ __launch_bounds__(kCholThreads, 1) void chol_inv_kernel(const double* __restrict__ g, int r,
+                                                                   float* __restrict__ rinv_t,
+                                                                   int32_t* __restrict__ status, int reset) {
+    __shared__ CholLds sh;
     const int tid = threadIdx.x;
-    auto G = [&](int i, int j) -> double& { return g[static_cast<int64_t>(i) * r + j]; };
-    auto X = [&](int i, int j) -> double& { return rinv[static_cast<int64_t>(i) * r + j]; };
-    if (tid == 0) bad = 0;
-    for (int p0 = 0; p0 < r; p0 += kPanel) {
-        const int pb = min(kPanel, r - p0), pe = p0 + pb, m = r - pe;
-        for (int e = tid; e < pb * pb; e += blockDim.x) dl[e / pb][e % pb] = G(p0 + e / pb, p0 + e % pb);
-        __syncthreads();
-        for (int k = 0; k < pb; ++k) {
-            if (tid == 0) {
-                double d = dl[k][k];
-                if (!(d > 0.0)) {
-                    bad = 1;
-                    d = 1.0;
-                }
-                piv = sqrt(d);
-                dl[k][k] = piv;
-            }
-            __syncthreads();
-            for (int j = k + 1 + tid; j < pb; j += blockDim.x) dl[k][j] /= piv;
-            __syncthreads();
-            for (int e = tid; e < pb * pb; e += blockDim.x) {
-                const int i = e / pb, j = e % pb;
-                if (i > k && j >= i) dl[i][j] -= dl[k][i] * dl[k][j];
-            }
-            __syncthreads();
-        }
-        for (int e = tid; e < pb * pb; e += blockDim.x) {
-            const int i = e / pb, j = e % pb;
-            if (j >= i) G(p0 + i, p0 + j) = dl[i][j];
-        }
-        // panel rows: R_d^T x = g[p0:pe][j] for each column j right of the block
-        for (int c = tid; c < m; c += blockDim.x) {
-            const int j = pe + c;
-            double x[kPanel];
+    const int ti = tid >> 5, tj = tid & 31;
+    double m[kCholRB][kCholCB];
+
+    // the upper triangle of g; zeros below it and outside r (also in the published rows)
 #pragma unroll
-            for (int i = 0; i < kPanel; ++i) {
-                if (i < pb) {
-                    double v = G(p0 + i, j);
+    for (int a = 0; a < kCholRB; ++a)
 #pragma unroll
-                    for (int l = 0; l < i; ++l) v -= dl[l][i] * x[l];
-                    x[i] = v / dl[i][i];
-                    G(p0 + i, j) = x[i];
-                    pl[i][c] = x[i];
-                }
+        for (int b = 0; b < kCholCB; ++b)
+            if (chol_kept(a, b)) {
+                const int i = 16 * a + ti, j = 32 * b + tj;
+                m[a][b] = i <= j && i < r && j < r ? g[static_cast<int64_t>(i) * r + j] : 0.0;
             }
-        }
-        __syncthreads();
-        // trailing update of the upper triangle: g[i][j] -= sum_l R[l][i] R[l][j], pe <= i <= j
-        for (int64_t e = tid; e < static_cast<int64_t>(m) * m; e += blockDim.x) {
-            const int i = static_cast<int>(e / m), j = static_cast<int>(e % m);
-            if (j < i) continue;
-            double v = G(pe + i, pe + j);
-            for (int l = 0; l < pb; ++l) v -= pl[l][i] * pl[l][j];
-            G(pe + i, pe + j) = v;
-        }
-        __syncthreads();
+    for (int e = tid; e < 2 * 256; e += kCholThreads) {
+        (&sh.row[0][0])[e] = 0.0;
+        (&sh.col[0][0])[e] = 0.0;
     }
-    // R^-1: zero below the diagonal, then the diagonal blocks (back substitution in LDS)
-    for (int64_t e = tid; e < static_cast<int64_t>(r) * r; e += blockDim.x) {
-        const int i = static_cast<int>(e / r), j = static_cast<int>(e % r);
-        if (i > j) X(i, j) = 0.0;
-    }
-    for (int p0 = 0; p0 < r; p0 += kPanel) {
-        const int pb = min(kPanel, r - p0);
-        __syncthreads();
-        for (int e = tid; e < pb * pb; e += blockDim.x) dl[e / pb][e % pb] = G(p0 + e / pb, p0 + e % pb);
-        __syncthreads();
-        for (int c = tid; c < pb; c += blockDim.x) {  // column c of the block's inverse
-            double x[kPanel];
-#pragma unroll
-            for (int i = kPanel - 1; i >= 0; --i) {
-                if (i < pb) {
-                    double v = i == c ? 1.0 : 0.0;
-#pragma unroll
-                    for (int l = i + 1; l < kPanel; ++l)
-                        if (l <= c) v -= dl[i][l] * x[l];
-                    x[i] = i <= c ? v / dl[i][i] : 0.0;
-                    X(p0 + i, p0 + c) = x[i];
-                }
-            }
-        }
-    }
+    if (tid == 0) sh.bad = 0;
     __syncthreads();
-    // off-diagonal blocks: X_ij = -X_ii * sum_{k = i+1 .. j} R_ik X_kj; the blocks of R and X
-    // of each term staged in LDS, every thread accumulating 4 entries of the 32x32 block
-    constexpr int EPT = kPanel * kPanel / 256;  // entries per thread (blockDim 256)
-    const int nb = (r + kPanel - 1) / kPanel;
-    for (int bj = 1; bj < nb; ++bj) {
-        const int j0 = bj * kPanel, jb = min(kPanel, r - j0);
-        for (int bi = bj - 1; bi >= 0; --bi) {
-            const int i0 = bi * kPanel;  // full panel (only the last block can be short)
-            double acc[EPT] = {};
-            for (int kb = bi + 1; kb <= bj; ++kb) {
-                const int k0 = kb * kPanel, kw = min(kPanel, r - k0);
-                __syncthreads();
-                for (int e = tid; e < kPanel * kPanel; e += blockDim.x) {
-                    const int a = e / kPanel, l = e % kPanel;
-                    dl[a][l] = l < kw ? G(i0 + a, k0 + l) : 0.0;           // R_{i, kb}
-                    pl[a][l] = a < kw && l < jb ? X(k0 + a, j0 + l) : 0.0;  // X_{kb, j} (row a, column l)
-                }
-                __syncthreads();
+
+    chol_factor_phase<0>(m, sh, r, ti, tj, tid);
+    chol_factor_phase<1>(m, sh, r, ti, tj, tid);
+    chol_factor_phase<2>(m, sh, r, ti, tj, tid);
+    chol_factor_phase<3>(m, sh, r, ti, tj, tid);
+    chol_inverse_phase<0>(m, sh, r, ti, tj);
+    chol_inverse_phase<1>(m, sh, r, ti, tj);
+    chol_inverse_phase<2>(m, sh, r, ti, tj);
+    chol_inverse_phase<3>(m, sh, r, ti, tj);
+
+    // entries below the diagonal of a kept block hold leftovers of the factor's updates
 #pragma unroll
-                for (int q = 0; q < EPT; ++q) {
-                    const int e = tid + q * 256, a = e / kPanel, b = e % kPanel;
-                    double v = acc[q];
-                    for (int l = 0; l < kPanel; ++l) v += dl[a][l] * pl[l][b];
-                    acc[q] = v;
-                }
-            }
-            __syncthreads();
-            for (int e = tid; e < kPanel * kPanel; e += blockDim.x) {
-                const int a = e / kPanel, l = e % kPanel;
-                dl[a][l] = X(i0 + a, i0 + l);  // X_{i, i}
-            }
+    for (int a = 0; a < kCholRB; ++a)
 #pragma unroll
-            for (int q = 0; q < EPT; ++q) {
-                const int e = tid + q * 256;
-                pl[e / kPanel][e % kPanel] = acc[q];  // the sum S, row a, column b
-            }
-            __syncthreads();
-#pragma unroll
-            for (int q = 0; q < EPT; ++q) {
-                const int e = tid + q * 256, a = e / kPanel, b = e % kPanel;
-                if (b < jb) {
-                    double v = 0.0;
-                    for (int l = a; l < kPanel; ++l) v -= dl[a][l] * pl[l][b];
-                    X(i0 + a, j0 + b) = v;
-                }
-            }
+        for (int b = 0; b < kCholCB; ++b) {
+            const int i = 16 * a + ti, j = 32 * b + tj;
+            if (i < r && j < r)
+                rinv_t[static_cast<int64_t>(j) * r + i] = chol_kept(a, b) && i <= j ? static_cast<float>(m[a][b]) : 0.f;
         }
-    }
     __syncthreads();
-    for (int64_t e = tid; e < static_cast<int64_t>(r) * r; e += blockDim.x) {
-        const int n = static_cast<int>(e / r), k = static_cast<int>(e % r);
-        rinv_t[e] = static_cast<float>(X(k, n));
-    }
     if (tid == 0 && status) {
-        if (reset) *status = bad;
-        else if (bad) *status = 1;
+        if (reset) *status = sh.bad;
+        else if (sh.bad) *status = 1;
     }
 }
 
@@ -275,9 +338,9 @@ hipError_t launch_gram64(const float* y, int n, int r, double* part, double* g, 
     return hipGetLastError();
 }
 
-hipError_t launch_chol_inv(double* g, int r, float* rinv_t, double* rinv, int32_t* status, bool reset, hipStream_t s) {
+hipError_t launch_chol_inv(const double* g, int r, float* rinv_t, int32_t* status, bool reset, hipStream_t s) {
     ProfileScope prof("fit_chol", s);
-    hipLaunchKernelGGL(chol_inv_kernel, dim3(1), dim3(256), 0, s, g, r, rinv_t, rinv, status, reset ? 1 : 0);
+    hipLaunchKernelGGL(chol_inv_kernel, dim3(1), dim3(kCholThreads), 0, s, g, r, rinv_t, status, reset ? 1 : 0);
     return hipGetLastError();
 }
 

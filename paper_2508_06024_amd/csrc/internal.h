@@ -89,9 +89,10 @@ hipError_t launch_codec_prep(const float* z, int64_t nz, void* zb, int n, int w,
 // ([gram64_chunks(n, r)][r][r] float64) added in chunk order
 int gram64_chunks(int n, int r);
 hipError_t launch_gram64(const float* y, int n, int r, double* part, double* g, hipStream_t s);
-// g = R^T R (Cholesky, in place, float64) and rinv_t[n][k] = (R^-1)[k][n] in float32; rinv is a
-// float64 [r][r] scratch. *status: 1 if a pivot was not positive (set to 0 first when reset).
-hipError_t launch_chol_inv(double* g, int r, float* rinv_t, double* rinv, int32_t* status, bool reset, hipStream_t s);
+// g = R^T R (Cholesky, float64, r <= 256 a multiple of 16; g is read only) and
+// rinv_t[n][k] = (R^-1)[k][n] in float32. *status: 1 if a pivot was not positive (set to 0
+// first when reset).
+hipError_t launch_chol_inv(const double* g, int r, float* rinv_t, int32_t* status, bool reset, hipStream_t s);
 // xu [h][c*w] = the slices [c][h][w] side by side (w a multiple of 16 bytes)
 hipError_t launch_unfold(DType dt, const void* x, int c, int h, int w, void* xu, hipStream_t s);
 

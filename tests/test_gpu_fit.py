@@ -40,6 +40,8 @@ def _proj(a):
     (1, 128, 256, 16, 32, W.F32, 3, 1e-5),
     (3, 96, 128, 16, 16, W.F32, 5, 1e-5),
     (4, 256, 768, 64, 64, W.BF16, 4, 2e-2),   # the paper-shaped layers' calibration block
+    (2, 64, 128, 48, 48, W.F32, 3, 1e-5),     # rank not a multiple of 32
+    (1, 320, 384, 256, 256, W.F32, 2, 1e-5),  # the largest rank: every block of the factorisation
 ])
 def test_fit_matches_oracle_iteration(c, h, w, rh, rw, dt, iters, tol):
     say(f"fit c={c} h={h} w={w} r={rh}x{rw} {dt} iters={iters}")
