@@ -160,7 +160,8 @@ struct CodecWs {
     int batch;     // slices handled by one set of launches
     // encode: V^T, P = X V (float32), per-chunk partial sums of U^T P
     size_t vt, p, epart, enc_total;
-    int tc;  // tokens per chunk of the U^T P contraction
+    int tc;      // tokens per chunk of the U^T P contraction
+    bool fused;  // bf16 layers of whole 64-token and 64-column tiles: P and U^T P in one kernel
     // decode: Z rounded to the layer dtype (bf16 only), W = V_hat Z^T per slice, and the segment
     // offsets and row maps of the grouped products over a batch of slices
     size_t zb, wt, seg_w, rows_w, seg_h, rows_h, dec_total;
@@ -193,12 +194,15 @@ CodecWs codec_ws(const ec2moe_codec_desc* d) {
     w.batch = codec_batch(d);
     const size_t nb = static_cast<size_t>(w.batch);
     w.tc = utp_chunk(d->h, d->r_w, w.batch, static_cast<DType>(d->dtype));
-    const size_t chunks = (static_cast<size_t>(std::max(1, d->h)) + w.tc - 1) / w.tc;
+    w.fused = encode_fused_ok(static_cast<DType>(d->dtype), d->h, d->w, d->r_h, d->r_w);
+    // partial sums of U^T P: per token chunk, or per 64-token tile of the fused encoder
+    const size_t chunks = w.fused ? static_cast<size_t>(d->h) / 64
+                                  : (static_cast<size_t>(std::max(1, d->h)) + w.tc - 1) / w.tc;
     size_t o = 0;
     w.gpart = o; o += up(gemm_split_scratch_bytes());
     const size_t shared = o;
     w.vt = o; o += up(static_cast<size_t>(d->r_w) * d->w * eb);
-    w.p = o; o += up(nb * d->h * d->r_w * 4);
+    w.p = o; o += w.fused ? 0 : up(nb * d->h * d->r_w * 4);
     w.epart = o; o += up(nb * chunks * d->r_h * d->r_w * 4);
     w.enc_total = o;
     o = shared;
@@ -523,6 +527,13 @@ ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x
     const size_t slice_bytes = static_cast<size_t>(desc->h) * desc->w * eb;
     for (int c0 = 0; c0 < desc->n_slices && e == hipSuccess; c0 += w.batch) {
         const int nc = std::min(w.batch, desc->n_slices - c0);
+        if (w.fused) {
+            EncArgs a{};
+            a.x = static_cast<const char*>(x) + c0 * slice_bytes; a.vt = vt; a.u = u; a.part = at<float>(ws, w.epart);
+            a.h = desc->h; a.w = desc->w; a.rh = desc->r_h; a.rw = desc->r_w; a.slices = nc;
+            e = launch_encode_fused(a, z + static_cast<size_t>(c0) * desc->r_h * desc->r_w, stream);
+            continue;
+        }
         // P = X V  [nc * h][r_w], float32: V is shared, so the slices stack into one product
         GemmArgs g{};
         g.tok = static_cast<const char*>(x) + c0 * slice_bytes; g.row_index = nullptr; g.w = vt;

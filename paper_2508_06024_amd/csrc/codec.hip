@@ -319,6 +319,237 @@ __global__ __launch_bounds__(256) void utp3_kernel(UtpArgs g) {
             }
 }
 
+// ------------------------------------------------------------------ fused encoder (bf16 layers)
+//
+// One workgroup per (64-token tile, 64-column tile) of P = X V: the tile's products over the
+// whole model width (no split along it), then at once its share of Z = U^T P,
+//   part[s][tt][r][c] = sum over the tile's 64 tokens t of U[t][r] P[t][c],
+// which split_reduce_kernel adds over the token tiles in order. X and V^T ([r_w][w], K-contiguous)
+// stream through a ring of four LDS stages of 128 model columns (32 KB: 64 token rows and 64
+// V^T rows of 256 bytes) filled by buffer_load ... lds, so three stages are in flight while
+// one is consumed. Eight waves: wave w computes the 32x32 block (w & 1, (w >> 1) & 1) of the
+// P tile over the even (w < 4) or odd (w >= 4) 16-column steps of each stage; the two halves
+// are added once at the end. The P tile is then split exactly into three bf16 planes
+// (hi + mid + lo) and, with U^T, staged in LDS for the bf16 matrix cores, as in utp3_kernel.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+}  // namespace
+
+// buffer_load_dwordx4 ... lds: each lane's 16 bytes land at M0 + 16 * lane
+__device__ void raw_buffer_load_lds(i32x4 rsrc, lds_void* lds, int size, int voffset, int soffset, int offset,
+                                    int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+
+namespace {
+
+__device__ __forceinline__ i32x4 enc_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t p = reinterpret_cast<uint64_t>(base);
+    i32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(p)));
+    r[1] = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(p >> 32)));
+    r[2] = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes));
+    r[3] = 0x00020000;  // raw (untyped, unswizzled) buffer of the gfx9 family
+    return r;
+}
+
+constexpr int kEncT = 64;                            // tokens per tile
+constexpr int kEncC = 64;                            // columns of P per tile
+constexpr int kEncK = 128;                           // model columns per LDS stage
+constexpr int kEncRing = 4;                          // LDS stages
+constexpr int kEncRow = kEncK * 2;                   // bytes per staged row
+constexpr int kEncStage = (kEncT + kEncC) * kEncRow;  // 32 KB
+constexpr int kEncLoads = 4;                         // DMA instructions per wave per stage
+
+__global__ __launch_bounds__(512, 1) void encode_fused_kernel(EncArgs a) {
+    // one LDS object per ring slot, each named at compile time where it is read, so the wait
+    // before a fragment read only covers the DMA into that slot
+    __shared__ __attribute__((aligned(1024))) char lds0[kEncStage];
+    __shared__ __attribute__((aligned(1024))) char lds1[kEncStage];
+    __shared__ __attribute__((aligned(1024))) char lds2[kEncStage];
+    __shared__ __attribute__((aligned(1024))) char lds3[kEncStage];
+    const int ct_n = a.rw / kEncC, tt_n = a.h / kEncT;
+    const int n = ct_n * tt_n * a.slices;
+    const int g = blockIdx.x;
+    int ct, tts;
+    if (n % (8 * ct_n) == 0) {
+        // the column tiles of one token tile run on one XCD (workgroups go round-robin over the
+        // eight): X rows are fetched into that XCD's L2 once for all of them
+        const int q = g / 8;
+        ct = q % ct_n;
+        tts = g % 8 + 8 * (q / ct_n);
+    } else {
+        ct = g % ct_n;
+        tts = g / ct_n;
+    }
+    const int s = tts / tt_n, tt = tts % tt_n;
+
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l32 = lane & 31, lh = lane >> 5;
+    const uint32_t row_bytes = static_cast<uint32_t>(a.w) * 2u;
+
+    // U^T staging items (8 tokens x 8 rows of U^T each), loaded first: their loads are older
+    // than every DMA load, so the counted waits of the ring also cover them
+    const int rgroups = ((a.rh + 63) & ~63) / 8;
+    const bool has_u = tid < 8 * rgroups;
+    const int urg = tid % rgroups, utg = tid / rgroups;
+    uint4 rowv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const int t = tt * kEncT + utg * 8 + q;
+        rowv[q] = has_u && urg * 8 < a.rh ? ldg16(static_cast<const bf16_t*>(a.u) + static_cast<int64_t>(t) * a.rh + urg * 8)
+                                           : make_uint4(0, 0, 0, 0);
+    }
+
+    // DMA: wave w fills staged rows 16 w .. 16 w + 15 (rows 0..63: the tile's tokens, 64..127: its
+    // V^T rows), four rows of 256 bytes per instruction; chunk c of staged row R sits at
+    // c ^ (R % 16), the swizzle applied on the global side
+    const bool tok_wave = wave < 4;
+    const i32x4 rs = tok_wave
+        ? enc_rsrc(static_cast<const bf16_t*>(a.x) + (static_cast<int64_t>(s) * a.h + static_cast<int64_t>(tt) * kEncT) * a.w,
+                   kEncT * row_bytes)
+        : enc_rsrc(static_cast<const bf16_t*>(a.vt) + static_cast<int64_t>(ct) * kEncC * a.w, kEncC * row_bytes);
+    uint32_t voff[kEncLoads];
+#pragma unroll
+    for (int j = 0; j < kEncLoads; ++j) {
+        const int row = 16 * (wave & 3) + 4 * j + (lane >> 4);  // row within its operand
+        voff[j] = static_cast<uint32_t>(row) * row_bytes + static_cast<uint32_t>(((lane & 15) ^ (row & 15)) * 16);
+    }
+    auto issue = [&](int st, char* slot) {
+        char* base = slot + 16 * wave * kEncRow;
+#pragma unroll
+        for (int j = 0; j < kEncLoads; ++j)
+            raw_buffer_load_lds(rs, reinterpret_cast<lds_void*>(reinterpret_cast<uintptr_t>(base + 4 * j * kEncRow)), 16,
+                                static_cast<int>(voff[j]), st * kEncRow, 0, 0);
+    };
+
+    // fragments: A = V^T row 64 + 32 wn + l32 (a column of P), B = token row 32 wm + l32, each
+    // lane the 16 bytes of logical chunk 2 q + lh of k-step q
+    const int wm = wave & 1, wn = (wave >> 1) & 1, kh = wave >> 2;
+    const int ra = kEncT + 32 * wn + l32, rb = 32 * wm + l32;
+    int offa[4], offb[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int ch = 2 * (2 * q + kh) + lh;
+        offa[q] = ra * kEncRow + ((ch ^ (ra & 15)) * 16);
+        offb[q] = rb * kEncRow + ((ch ^ (rb & 15)) * 16);
+    }
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+
+    const int ns = a.w / kEncK;
+    auto step = [&](int st, const char* cur, char* refill) {
+        if (st >= ns) return;
+        const int later = min(kEncRing - 2, ns - 1 - st);  // stages issued after this one
+        if (later >= 2) __builtin_amdgcn_s_waitcnt(0x0070 | (2 * kEncLoads));
+        else if (later == 1) __builtin_amdgcn_s_waitcnt(0x0070 | kEncLoads);
+        else __builtin_amdgcn_s_waitcnt(0x0070);
+        // every wave's loads of this stage are in LDS, and every wave is done with the previous
+        // stage, whose slot is refilled next (a bare barrier: __syncthreads would also wait for
+        // the loads still in flight)
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_barrier" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        if (st + kEncRing - 1 < ns) issue(st + kEncRing - 1, refill);
+        uint4 fa[4], fb[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            fa[q] = *reinterpret_cast<const uint4*>(cur + offa[q]);
+            fb[q] = *reinterpret_cast<const uint4*>(cur + offb[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[q]), __builtin_bit_cast(bf16x8, fb[q]),
+                                                          acc, 0, 0, 0);
+    };
+    if (ns > 0) issue(0, lds0);
+    if (ns > 1) issue(1, lds1);
+    if (ns > 2) issue(2, lds2);
+    for (int st = 0; st < ns; st += kEncRing) {
+        step(st, lds0, lds3);
+        step(st + 1, lds1, lds0);
+        step(st + 2, lds2, lds1);
+        step(st + 3, lds3, lds2);
+    }
+
+    // the odd-step half of each block is added to the even-step half
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(lds0);
+    if (kh == 1) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) red[((wave - 4) * 16 + r) * 64 + lane] = acc[r];
+    }
+    char* lds_u = lds1;  // U^T [r][64 tokens], 128-byte rows (32 KB)
+    char* lds_p = lds2;  // P^T planes [3][64 columns][64 tokens] (24 KB)
+    __syncthreads();
+    if (kh == 0) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[r] += red[(wave * 16 + r) * 64 + lane];
+        // lane holds token j = 32 wm + l32 and, in register r, column i = 32 wn + 8 (r / 4) + 4 lh + r % 4
+        const int j = 32 * wm + l32;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int i = 32 * wn + 8 * (r / 4) + 4 * lh + (r % 4);
+            const float v = acc[r];
+            const uint16_t hi = f32_to_bf16(v);
+            const float r1 = v - bf16_to_f32(hi);
+            const uint16_t mid = f32_to_bf16(r1);
+            const uint16_t lo = f32_to_bf16(r1 - bf16_to_f32(mid));
+            const int off = i * 128 + (((j >> 3) ^ ((i >> 1) & 7)) * 16) + (j & 7) * 2;
+            *reinterpret_cast<uint16_t*>(lds_p + 0 * kEncC * 128 + off) = hi;
+            *reinterpret_cast<uint16_t*>(lds_p + 1 * kEncC * 128 + off) = mid;
+            *reinterpret_cast<uint16_t*>(lds_p + 2 * kEncC * 128 + off) = lo;
+        }
+    }
+    if (has_u) {
+        const int r0 = urg * 8;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int R = r0 + j;
+            const uint4 o = make_uint4(bf16_pair(rowv[0], rowv[1], j), bf16_pair(rowv[2], rowv[3], j),
+                                       bf16_pair(rowv[4], rowv[5], j), bf16_pair(rowv[6], rowv[7], j));
+            *reinterpret_cast<uint4*>(lds_u + R * 128 + ((utg ^ ((R >> 1) & 7)) * 16)) = o;
+        }
+    }
+    __syncthreads();
+
+    // Z share: wave w owns rows 64 (w & 3) .. + 63 of U^T P and the 32 columns 32 (w >> 2) ..
+    const int rbase = 64 * (wave & 3), cb = wave >> 2;
+    if (rbase >= a.rh) return;
+    f32x16 z[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) z[i][r] = 0.f;
+    const int sw = (l32 >> 1) & 7;
+#pragma unroll
+    for (int q = 0; q < kEncT / 16; ++q) {
+        const int ch = ((2 * q + lh) ^ sw) * 16;
+        uint4 ua[2], pb[3];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) ua[i] = *reinterpret_cast<const uint4*>(lds_u + (rbase + 32 * i + l32) * 128 + ch);
+#pragma unroll
+        for (int pl = 0; pl < 3; ++pl) pb[pl] = *reinterpret_cast<const uint4*>(lds_p + (pl * kEncC + 32 * cb + l32) * 128 + ch);
+#pragma unroll
+        for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                z[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ua[i]), __builtin_bit_cast(bf16x8, pb[pl]),
+                                                               z[i], 0, 0, 0);
+    }
+    float* part = a.part + (static_cast<int64_t>(s) * tt_n + tt) * a.rh * a.rw;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int r = rbase + 32 * i + 8 * (q / 4) + 4 * lh + (q % 4);
+            const int c = ct * kEncC + 32 * cb + l32;
+            if (r < a.rh) part[static_cast<int64_t>(r) * a.rw + c] = z[i][q];
+        }
+}
+
 // dst[i] = round-to-nearest-even bfloat16 of src[i], four elements per thread (n a multiple of 4)
 __global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ src, int64_t n,
                                                           bf16_t* __restrict__ dst) {
@@ -427,6 +658,25 @@ hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s) {
     const int rgrid = static_cast<int>(std::min<int64_t>((mn + 255) / 256, 4096));
     ProfileScope prof("codec_utp_reduce", s);
     hipLaunchKernelGGL(split_reduce_kernel<float>, dim3(rgrid, g.slices), dim3(256), 0, s, g.part, mn, chunks, g.z);
+    return hipGetLastError();
+}
+
+bool encode_fused_ok(DType dt, int h, int w, int rh, int rw) {
+    return dt == DType::BF16 && h > 0 && h % kEncT == 0 && rw % kEncC == 0 && w % kEncK == 0 && rh <= 256;
+}
+
+hipError_t launch_encode_fused(const EncArgs& a, float* z, hipStream_t s) {
+    const int tt_n = a.h / kEncT;
+    {
+        ProfileScope prof("codec_encode", s);
+        hipLaunchKernelGGL(encode_fused_kernel, dim3((a.rw / kEncC) * tt_n * a.slices), dim3(512), 0, s, a);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t mn = static_cast<int64_t>(a.rh) * a.rw;
+    const int rgrid = static_cast<int>(std::min<int64_t>((mn + 255) / 256, 4096));
+    ProfileScope prof("codec_utp_reduce", s);
+    hipLaunchKernelGGL(split_reduce_kernel<float>, dim3(rgrid, a.slices), dim3(256), 0, s, a.part, mn, tt_n, z);
     return hipGetLastError();
 }
 

@@ -80,6 +80,18 @@ struct UtpArgs {
     float* z;
 };
 hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s);
+// Fused encoder of bf16 layers: part[s][tt][r][c] = U^T (X V) over 64-token tiles tt (X [slices][h][w],
+// V^T [r_w][w], U [h][r_h]), then z[s] = sum over tt in order. Applies when encode_fused_ok();
+// part holds slices * (h / 64) * r_h * r_w floats.
+struct EncArgs {
+    const void* x;   // bf16
+    const void* vt;  // bf16
+    const void* u;   // bf16
+    float* part;
+    int h, w, rh, rw, slices;
+};
+bool encode_fused_ok(DType dt, int h, int w, int rh, int rw);
+hipError_t launch_encode_fused(const EncArgs& a, float* z, hipStream_t s);
 // Decoder set-up of n slices: zb = bfloat16(z) (nz elements, a multiple of 4; skipped when zb is
 // null); seg_w[s] = s*w, rows_w[p] = p % w, seg_h[s] = s*h, rows_h[p] = p % h (s <= n).
 hipError_t launch_codec_prep(const float* z, int64_t nz, void* zb, int n, int w, int h, int32_t* seg_w,

@@ -47,6 +47,10 @@ def test_full_rank_codec_round_trips_on_gpu():
     (4, 256, 768, 64, 64, W.BF16),   # the paper-shaped layers: 4 sequences of 256 tokens
     (1, 300, 256, 80, 64, W.BF16),   # r_h ending inside the second 64-row block of U^T P
     (2, 260, 128, 208, 112, W.F32),  # ... inside the fourth
+    # bf16 layers of whole 64-token, 64-column tiles take the fused encoder:
+    (3, 128, 256, 80, 128, W.BF16),   # r_h inside the second 64-row block, two column tiles
+    (2, 256, 384, 256, 192, W.BF16),  # three column tiles of a token tile placed on one XCD
+    (17, 64, 128, 16, 64, W.BF16),    # one tile per slice, more slices than one batch
 ])
 def test_codec_slices_and_separate_decoder_projections(c, h, w, rh, rw, dt):
     """Several slices coded with one U, V; decoder projections different from the encoder's."""
