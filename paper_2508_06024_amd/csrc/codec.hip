@@ -1,9 +1,11 @@
-// Helpers of the low-rank codec (Encoder-Decoder based on Low-Rank Compression) for
-// gfx950: a tiled transpose, the contraction Z = U^T P of the encoder at float32 accuracy
-// (P = X V in float32; bfloat16 U on the bf16 matrix cores with P split in three bf16
-// planes, float32 U on the float32 matrix cores), its in-order reduction over token chunks, and the
-// float32 -> bfloat16 rounding of Z for the decoder. The large products X V, V_hat Z^T and
-// U_hat W^T run on the matrix-core GEMM.
+// Kernels of the low-rank codec (Encoder-Decoder based on Low-Rank Compression) for gfx950:
+// a tiled transpose; the fused encoder of bf16 layers (P = X V and its share of Z = U^T P in
+// one workgroup per 64 x 64 tile of P); the contraction Z = U^T P of the other shapes at
+// float32 accuracy (P = X V in float32; bfloat16 U on the bf16 matrix cores with P split in
+// three bf16 planes, float32 U on the float32 matrix cores); the in-order reduction of the
+// partial sums over token tiles or chunks; and the float32 -> bfloat16 rounding of Z for the
+// decoder. The decoder's products V_hat Z^T and U_hat W^T, and X V outside the fused
+// encoder, run on the matrix-core GEMM.
 #include "device_common.h"
 #include "internal.h"
 
