@@ -43,6 +43,13 @@ def test_selection_hand_example():
     assert PO.select_candidates(c["state"], dict(c["params"], max_fraction=1.0), c["complexity"]) == c["selected_uncapped"]
 
 
+def test_selection_hand_example_with_every_capability_term():
+    c = _hand()["selection_all_terms"]
+    assert PO.capability(c["state"], c["params"]) == c["capability"]
+    assert PO.select_candidates(c["state"], c["params"], c["complexity"]) == c["selected"]
+    assert PO.select_candidates(c["state"], dict(c["params"], max_fraction=1.0), c["complexity"]) == c["selected_uncapped"]
+
+
 def test_schedule_hand_example():
     c = _hand()["schedule"]
     loc, order, obj, le, lc = PO.schedule_tasks(c["params"], c["complexity"], c["comm"])
@@ -102,9 +109,10 @@ def test_schedule_invariants(seed):
 
 def test_library_matches_hand_examples():
     c = _hand()
-    s = c["selection"]
-    words, n = E.select_candidates(_state(s["state"]), _sel(s["params"]), s["complexity"])
-    assert W.mask_members(words, len(s["complexity"])) == s["selected"] and n == len(s["selected"])
+    for key in ("selection", "selection_all_terms"):
+        s = c[key]
+        words, n = E.select_candidates(_state(s["state"]), _sel(s["params"]), s["complexity"])
+        assert W.mask_members(words, len(s["complexity"])) == s["selected"] and n == len(s["selected"])
     t = c["schedule"]
     loc, order, (obj, le, lc) = E.schedule_tasks(_sched(t["params"]), t["complexity"], t["comm"])
     assert loc.tolist() == t["location"] and order.tolist() == t["order"]
