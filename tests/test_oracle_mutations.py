@@ -65,6 +65,16 @@ MUTATIONS = [
      "return np.asarray(x, np.float64) @ np.asarray(v, np.float64)"),
     ("decoder with V_hat where its transpose belongs",
      "@ np.asarray(z, np.float64) @ np.asarray(v_hat, np.float64).T", "@ np.asarray(z, np.float64) @ np.asarray(v_hat, np.float64)"),
+    ("fit: R's diagonal left with either sign (basis not the positive-diagonal QR)",
+     "    return q * s\n", "    return q\n"),
+    ("fit: the Gram matrices of the two sides swapped (Eq. 8)",
+     "return iterate(a, omega_u), iterate(b, omega_v)", "return iterate(b, omega_u), iterate(a, omega_v)"),
+    ("fit: V from the mode-1 unfolding",
+     "v = np.linalg.svd(_unfold_cols(xs), full_matrices=False)[0][:, :r_w]",
+     "v = np.linalg.svd(_unfold_rows(xs), full_matrices=False)[0][:, :r_w]"),
+    ("fit: one power step fewer than asked",
+     "        for _ in range(iters):\n            q = orthonormal_basis(g @ q)",
+     "        for _ in range(iters - 1):\n            q = orthonormal_basis(g @ q)"),
     ("experts run on X instead of the reconstruction X_hat",
      "y = moe_forward(x_hat, idx, w, w_gate_up, w_down, activation)", "y = moe_forward(x, idx, w, w_gate_up, w_down, activation)"),
 ]

@@ -633,6 +633,19 @@ def test_subspace_iteration_converges_to_the_hosvd_subspace():
     np.testing.assert_allclose(u.T @ u, np.eye(r), atol=1e-12)
 
 
+@pytest.mark.parametrize("iters", [0, 1, 3])
+def test_subspace_iteration_takes_the_asked_power_steps(iters):
+    """Closed form: one slice X = diag(sqrt(a)) has A = B = diag(a), and from a start block of
+    ones (rank 1) the i-th iterate is A^i 1 / ||A^i 1||: U = V = a^iters normalised."""
+    a = np.array([4.0, 3.0, 2.0, 1.5, 1.0, 0.5])
+    x = np.diag(np.sqrt(a))
+    ones = np.ones((a.size, 1))
+    u, v = O.codec_fit_subspace(x[None], ones, ones, iters)
+    want = a ** iters / np.linalg.norm(a ** iters)
+    np.testing.assert_allclose(u[:, 0], want, rtol=1e-12)
+    np.testing.assert_allclose(v[:, 0], want, rtol=1e-12)
+
+
 def test_orthonormal_basis_is_the_positive_diagonal_qr():
     rng = np.random.default_rng(53)
     y = rng.standard_normal((30, 6))
