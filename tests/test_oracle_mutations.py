@@ -56,6 +56,13 @@ MUTATIONS = [
      "w[t] = w[t] / w[t].sum()", "w[t] = w[t]"),
     ("top-G groups stop before they hold k candidates",
      "if len(kept) >= top_groups and held >= min_candidates:", "if len(kept) >= top_groups:"),
+    ("permutation sorted without keeping the input order inside a segment",
+     'order = np.argsort(flat, kind="stable")', 'order = np.argsort(flat, kind="quicksort")'),
+    ("top-G ranking ties to the higher group index",
+     "order = sorted(range(len(active)), key=lambda a: (-p_group[a], active[a]))",
+     "order = sorted(range(len(active)), key=lambda a: (-p_group[a], -active[a]))"),
+    ("unequal groups start one expert late",
+     "starts = np.concatenate([[0], np.cumsum(group_sizes)])", "starts = np.concatenate([[1], 1 + np.cumsum(group_sizes)])"),
     ("inverse permutation taken as the permutation itself",
      "inv_perm[order] = np.arange(flat.size, dtype=np.int32)", "inv_perm[:] = order"),
     ("combine without the gate weights (Eq. 1)",
