@@ -162,6 +162,7 @@ struct CodecWs {
     size_t vt, p, epart, enc_total;
     int tc;      // tokens per chunk of the U^T P contraction
     bool fused;  // bf16 layers of whole 64-token and 64-column tiles: P and U^T P in one kernel
+    bool small;  // at most 64 tokens per slice: the small-batch encoder and decoder
     // decode: Z rounded to the layer dtype (bf16 only), W = V_hat Z^T per slice, and the segment
     // offsets and row maps of the grouped products over a batch of slices
     size_t zb, wt, seg_w, rows_w, seg_h, rows_h, dec_total;
@@ -194,7 +195,8 @@ CodecWs codec_ws(const ec2moe_codec_desc* d) {
     w.batch = codec_batch(d);
     const size_t nb = static_cast<size_t>(w.batch);
     w.tc = utp_chunk(d->h, d->r_w, w.batch, static_cast<DType>(d->dtype));
-    w.fused = encode_fused_ok(static_cast<DType>(d->dtype), d->h, d->w, d->r_h, d->r_w);
+    w.small = codec_small_ok(d->h, d->w, d->r_h, d->r_w);
+    w.fused = !w.small && encode_fused_ok(static_cast<DType>(d->dtype), d->h, d->w, d->r_h, d->r_w);
     // partial sums of U^T P: per token chunk, or per 64-token tile of the fused encoder
     const size_t chunks = w.fused ? static_cast<size_t>(d->h) / 64
                                   : (static_cast<size_t>(std::max(1, d->h)) + w.tc - 1) / w.tc;
@@ -202,8 +204,10 @@ CodecWs codec_ws(const ec2moe_codec_desc* d) {
     w.gpart = o; o += up(gemm_split_scratch_bytes());
     const size_t shared = o;
     w.vt = o; o += up(static_cast<size_t>(d->r_w) * d->w * eb);
-    w.p = o; o += w.fused ? 0 : up(nb * d->h * d->r_w * 4);
-    w.epart = o; o += up(nb * chunks * d->r_h * d->r_w * 4);
+    w.p = o; o += w.fused || w.small ? 0 : up(nb * d->h * d->r_w * 4);
+    w.epart = o;
+    o += w.small ? up(codec_small_part_floats(d->h, d->w, d->r_w, static_cast<int>(nb)) * 4)
+                 : up(nb * chunks * d->r_h * d->r_w * 4);
     w.enc_total = o;
     o = shared;
     w.zb = o; o += up(nb * d->r_h * d->r_w * eb);
@@ -521,10 +525,20 @@ ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x
     REQUIRE_ALIGNED(x); REQUIRE_ALIGNED(u); REQUIRE_ALIGNED(v); REQUIRE_ALIGNED(z);
     const DType dt = static_cast<DType>(desc->dtype);
     const size_t eb = elem_bytes(dt);
+    const size_t slice_bytes = static_cast<size_t>(desc->h) * desc->w * eb;
+    if (w.small) {
+        hipError_t e = hipSuccess;
+        for (int c0 = 0; c0 < desc->n_slices && e == hipSuccess; c0 += w.batch) {
+            const int nc = std::min(w.batch, desc->n_slices - c0);
+            e = launch_encode_small(dt, static_cast<const char*>(x) + c0 * slice_bytes, u, v, desc->h, desc->w,
+                                    desc->r_h, desc->r_w, nc, at<float>(ws, w.epart),
+                                    z + static_cast<size_t>(c0) * desc->r_h * desc->r_w, stream);
+        }
+        return hip_status(e, "lowrank_encode launch");
+    }
     void* vt = at<void>(ws, w.vt);
     float* p = at<float>(ws, w.p);
     hipError_t e = launch_transpose(dt, v, desc->w, desc->r_w, vt, stream);
-    const size_t slice_bytes = static_cast<size_t>(desc->h) * desc->w * eb;
     for (int c0 = 0; c0 < desc->n_slices && e == hipSuccess; c0 += w.batch) {
         const int nc = std::min(w.batch, desc->n_slices - c0);
         if (w.fused) {
@@ -566,6 +580,15 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
     void* wt = at<void>(ws, w.wt);
     hipError_t e = hipSuccess;
     const int64_t zn = static_cast<int64_t>(desc->r_h) * desc->r_w;
+    if (w.small) {
+        const size_t slice_bytes = static_cast<size_t>(desc->h) * desc->w * eb;
+        for (int c0 = 0; c0 < desc->n_slices && e == hipSuccess; c0 += w.batch) {
+            const int nc = std::min(w.batch, desc->n_slices - c0);
+            e = launch_decode_small(dt, z + static_cast<size_t>(c0) * zn, u_hat, v_hat, desc->h, desc->w, desc->r_h,
+                                    desc->r_w, nc, static_cast<char*>(x_hat) + c0 * slice_bytes, stream);
+        }
+        return hip_status(e, "lowrank_decode launch");
+    }
     if (desc->n_slices == 1) {
         // Wt = V_hat Z^T  [w][r_h]: both operands are K-contiguous rows (V_hat [w][r_w], Z [r_h][r_w]).
         // In bf16 layers Z is rounded to bf16 first (the product runs on the bf16 matrix cores;

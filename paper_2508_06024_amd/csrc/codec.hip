@@ -552,6 +552,161 @@ __global__ __launch_bounds__(512, 1) void encode_fused_kernel(EncArgs a) {
         }
 }
 
+// ------------------------------------------------------------------ small batches (h <= 64 tokens)
+//
+// With a few dozen tokens per slice the codec's products are tiny, and the launches of the
+// general path cost more than their work. Three launches do the whole round trip, in float32
+// throughout (products of the layer dtype's values are exact in float32):
+//   enc_small_partial: part[s][kc][t][c] = sum over the 64 model columns k of chunk kc of
+//                      X[s][t][k] V[k][c] (one workgroup per chunk, 16 columns of P and slice);
+//   enc_small_finish:  P[t][c] = the chunk partials added in a fixed order (the even and the
+//                      odd chunks each in order, then the two sums), then
+//                      Z[s] = U^T P (one workgroup per 2 columns of Z and slice);
+//   dec_small:         Y = U_hat Z[s] (h x r_w), then X_hat[s][t][j] = sum_c Y[t][c] V_hat[j][c] for 32
+//                      model columns j per workgroup, rounded once to the layer dtype.
+constexpr int kSmallT = 64;   // tokens per slice at most
+constexpr int kSmallK = 64;   // model columns per encoder chunk
+constexpr int kSmallPC = 16;  // columns of P per partial workgroup
+constexpr int kSmallZC = 2;   // columns of Z per finishing workgroup
+constexpr int kSmallJ = 32;   // model columns per decoder workgroup
+
+template <typename T>
+__device__ __forceinline__ void load_chunk_f32(const T* src, float* dst) {
+    const uint4 v = ldg16(src);
+    const T* e = reinterpret_cast<const T*>(&v);
+#pragma unroll
+    for (int i = 0; i < Elem<T>::kPerChunk; ++i) dst[i] = Elem<T>::to_f32(e[i]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void enc_small_partial_kernel(const T* __restrict__ x, const T* __restrict__ v,
+                                                                int h, int w, int rw, float* __restrict__ part) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    __shared__ float xs[kSmallT][kSmallK + 1];
+    __shared__ float vs[kSmallK][kSmallPC];
+    const int kc = blockIdx.x, c0 = blockIdx.y * kSmallPC, s = blockIdx.z, nkc = gridDim.x;
+    const int k0 = kc * kSmallK;
+    const T* xsl = x + static_cast<int64_t>(s) * h * w;
+    for (int e = threadIdx.x; e < h * (kSmallK / EPC); e += 256) {
+        const int t = e / (kSmallK / EPC), q = (e % (kSmallK / EPC)) * EPC;
+        load_chunk_f32(xsl + static_cast<int64_t>(t) * w + k0 + q, &xs[t][q]);
+    }
+    for (int e = threadIdx.x; e < kSmallK * (kSmallPC / EPC); e += 256) {
+        const int k = e / (kSmallPC / EPC), q = (e % (kSmallPC / EPC)) * EPC;
+        load_chunk_f32(v + static_cast<int64_t>(k0 + k) * rw + c0 + q, &vs[k][q]);
+    }
+    __syncthreads();
+    float* out = part + (static_cast<int64_t>(s) * nkc + kc) * h * rw;
+    for (int o = threadIdx.x; o < h * kSmallPC; o += 256) {
+        const int t = o / kSmallPC, c = o % kSmallPC;
+        float acc = 0.f;
+#pragma unroll 16
+        for (int k = 0; k < kSmallK; ++k) acc = fmaf(xs[t][k], vs[k][c], acc);
+        out[static_cast<int64_t>(t) * rw + c0 + c] = acc;
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void enc_small_finish_kernel(const float* __restrict__ part, const T* __restrict__ u,
+                                                               int h, int rh, int rw, int nkc, float* __restrict__ z) {
+    constexpr int RUNS = 256 / (kSmallT * kSmallZC);  // interleaved runs of chunks per element (2)
+    __shared__ float red[RUNS][kSmallT * kSmallZC];
+    __shared__ float ps[kSmallT][kSmallZC];
+    __shared__ float us[kSmallT][kSmallT + 1];
+    const int c0 = blockIdx.x * kSmallZC, s = blockIdx.y;
+    const float* src = part + static_cast<int64_t>(s) * nkc * h * rw;
+    const int e = threadIdx.x % (kSmallT * kSmallZC), run = threadIdx.x / (kSmallT * kSmallZC);
+    const int t = e / kSmallZC, c = e % kSmallZC;
+    float acc = 0.f;
+    if (t < h) {
+        const float* col = src + static_cast<int64_t>(t) * rw + c0 + c;
+        // chunks run, run + RUNS, ... in order, 16 loads in flight at a time
+        for (int q0 = run; q0 < nkc; q0 += 16 * RUNS) {
+            float vq[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int ch = q0 + q * RUNS;
+                vq[q] = ch < nkc ? col[static_cast<int64_t>(ch) * h * rw] : 0.f;
+            }
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                if (q0 + q * RUNS < nkc) acc += vq[q];
+        }
+    }
+    red[run][e] = acc;
+    for (int i = threadIdx.x; i < h * rh; i += 256) us[i / rh][i % rh] = Elem<T>::to_f32(u[i]);
+    __syncthreads();
+    if (threadIdx.x < kSmallT * kSmallZC && t < h) {
+        float sum = red[0][e];
+#pragma unroll
+        for (int r = 1; r < RUNS; ++r) sum += red[r][e];
+        ps[t][c] = sum;
+    }
+    __syncthreads();
+    float* zs = z + static_cast<int64_t>(s) * rh * rw;
+    for (int o = threadIdx.x; o < rh * kSmallZC; o += 256) {
+        const int i = o / kSmallZC, cc = o % kSmallZC;
+        float zacc = 0.f;
+        for (int tt = 0; tt < h; ++tt) zacc = fmaf(us[tt][i], ps[tt][cc], zacc);
+        zs[static_cast<int64_t>(i) * rw + c0 + cc] = zacc;
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void dec_small_kernel(const float* __restrict__ z, const T* __restrict__ u_hat,
+                                                        const T* __restrict__ v_hat, int h, int w, int rh, int rw,
+                                                        T* __restrict__ x_hat) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    constexpr int TG = 256 / kSmallJ;      // token groups (8)
+    constexpr int TPT = kSmallT / TG;      // tokens per thread at most (8)
+    constexpr int PRE = 32 / EPC;          // V_hat chunks loaded before the first barrier (32 columns)
+    __shared__ float zs[kSmallT][256];          // Z [r_h][r_w]
+    __shared__ float uh[kSmallT][kSmallT + 1];  // U_hat [h][r_h]
+    __shared__ float ys[kSmallT][256];          // Y = U_hat Z [h][r_w]
+    const int j0 = blockIdx.x * kSmallJ, s = blockIdx.y;
+    const int j = j0 + (threadIdx.x % kSmallJ), tg = threadIdx.x / kSmallJ;
+    const T* vrow = v_hat + static_cast<int64_t>(j) * rw;
+    // the first columns of this thread's V_hat row, loaded while Y is formed
+    uint4 vpre[PRE];
+#pragma unroll
+    for (int q = 0; q < PRE; ++q) vpre[q] = q * EPC < rw ? ldg16(vrow + q * EPC) : make_uint4(0, 0, 0, 0);
+    const float* zsl = z + static_cast<int64_t>(s) * rh * rw;
+    for (int e = threadIdx.x; e < rh * rw; e += 256) zs[e / rw][e % rw] = zsl[e];
+    for (int e = threadIdx.x; e < h * rh; e += 256) uh[e / rh][e % rh] = Elem<T>::to_f32(u_hat[e]);
+    __syncthreads();
+    for (int o = threadIdx.x; o < h * rw; o += 256) {
+        const int t = o / rw, c = o % rw;
+        float acc = 0.f;
+        for (int i = 0; i < rh; ++i) acc = fmaf(uh[t][i], zs[i][c], acc);
+        ys[t][c] = acc;
+    }
+    __syncthreads();
+    float acc[TPT];
+#pragma unroll
+    for (int q = 0; q < TPT; ++q) acc[q] = 0.f;
+    auto columns = [&](int c, const uint4& raw) {
+        const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+        for (int q = 0; q < TPT; ++q) {
+            const int t = tg + TG * q;
+            if (t < h) {
+#pragma unroll
+                for (int i = 0; i < EPC; ++i) acc[q] = fmaf(ys[t][c + i], Elem<T>::to_f32(e[i]), acc[q]);
+            }
+        }
+    };
+#pragma unroll
+    for (int q = 0; q < PRE; ++q)
+        if (q * EPC < rw) columns(q * EPC, vpre[q]);
+    for (int c = PRE * EPC; c < rw; c += EPC) columns(c, ldg16(vrow + c));
+    T* out = x_hat + static_cast<int64_t>(s) * h * w;
+#pragma unroll
+    for (int q = 0; q < TPT; ++q) {
+        const int t = tg + TG * q;
+        if (t < h) out[static_cast<int64_t>(t) * w + j] = Elem<T>::from_f32(acc[q]);
+    }
+}
+
 // dst[i] = round-to-nearest-even bfloat16 of src[i], four elements per thread (n a multiple of 4)
 __global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ src, int64_t n,
                                                           bf16_t* __restrict__ dst) {
@@ -679,6 +834,54 @@ hipError_t launch_encode_fused(const EncArgs& a, float* z, hipStream_t s) {
     const int rgrid = static_cast<int>(std::min<int64_t>((mn + 255) / 256, 4096));
     ProfileScope prof("codec_utp_reduce", s);
     hipLaunchKernelGGL(split_reduce_kernel<float>, dim3(rgrid, a.slices), dim3(256), 0, s, a.part, mn, tt_n, z);
+    return hipGetLastError();
+}
+
+bool codec_small_ok(int h, int w, int rh, int rw) {
+    return h > 0 && h <= kSmallT && rh <= kSmallT && rw <= 256 && rw % kSmallPC == 0 && w % kSmallK == 0 &&
+           w % kSmallJ == 0;
+}
+
+size_t codec_small_part_floats(int h, int w, int rw, int slices) {
+    return static_cast<size_t>(slices) * (w / kSmallK) * h * rw;
+}
+
+hipError_t launch_encode_small(DType dt, const void* x, const void* u, const void* v, int h, int w, int rh, int rw,
+                               int slices, float* part, float* z, hipStream_t s) {
+    const int nkc = w / kSmallK;
+    {
+        ProfileScope prof("codec_encode_part", s);
+        const dim3 grid(nkc, rw / kSmallPC, slices);
+        if (dt == DType::BF16)
+            hipLaunchKernelGGL(enc_small_partial_kernel<bf16_t>, grid, dim3(256), 0, s,
+                               static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(v), h, w, rw, part);
+        else
+            hipLaunchKernelGGL(enc_small_partial_kernel<float>, grid, dim3(256), 0, s,
+                               static_cast<const float*>(x), static_cast<const float*>(v), h, w, rw, part);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    ProfileScope prof("codec_encode_finish", s);
+    if (dt == DType::BF16)
+        hipLaunchKernelGGL(enc_small_finish_kernel<bf16_t>, dim3(rw / kSmallZC, slices), dim3(256), 0, s, part,
+                           static_cast<const bf16_t*>(u), h, rh, rw, nkc, z);
+    else
+        hipLaunchKernelGGL(enc_small_finish_kernel<float>, dim3(rw / kSmallZC, slices), dim3(256), 0, s, part,
+                           static_cast<const float*>(u), h, rh, rw, nkc, z);
+    return hipGetLastError();
+}
+
+hipError_t launch_decode_small(DType dt, const float* z, const void* u_hat, const void* v_hat, int h, int w, int rh,
+                               int rw, int slices, void* x_hat, hipStream_t s) {
+    ProfileScope prof("codec_decode", s);
+    if (dt == DType::BF16)
+        hipLaunchKernelGGL(dec_small_kernel<bf16_t>, dim3(w / kSmallJ, slices), dim3(256), 0, s, z,
+                           static_cast<const bf16_t*>(u_hat), static_cast<const bf16_t*>(v_hat), h, w, rh, rw,
+                           static_cast<bf16_t*>(x_hat));
+    else
+        hipLaunchKernelGGL(dec_small_kernel<float>, dim3(w / kSmallJ, slices), dim3(256), 0, s, z,
+                           static_cast<const float*>(u_hat), static_cast<const float*>(v_hat), h, w, rh, rw,
+                           static_cast<float*>(x_hat));
     return hipGetLastError();
 }
 

@@ -91,6 +91,14 @@ struct EncArgs {
     int h, w, rh, rw, slices;
 };
 bool encode_fused_ok(DType dt, int h, int w, int rh, int rw);
+// Small batches (h <= 64 tokens per slice, r_h <= 64): the encoder in two launches through
+// part (codec_small_part_floats floats) and the decoder in one, in float32 throughout.
+bool codec_small_ok(int h, int w, int rh, int rw);
+size_t codec_small_part_floats(int h, int w, int rw, int slices);
+hipError_t launch_encode_small(DType dt, const void* x, const void* u, const void* v, int h, int w, int rh, int rw,
+                               int slices, float* part, float* z, hipStream_t s);
+hipError_t launch_decode_small(DType dt, const float* z, const void* u_hat, const void* v_hat, int h, int w, int rh,
+                               int rw, int slices, void* x_hat, hipStream_t s);
 hipError_t launch_encode_fused(const EncArgs& a, float* z, hipStream_t s);
 // Decoder set-up of n slices: zb = bfloat16(z) (nz elements, a multiple of 4; skipped when zb is
 // null); seg_w[s] = s*w, rows_w[p] = p % w, seg_h[s] = s*h, rows_h[p] = p % h (s <= n).

@@ -50,7 +50,10 @@ def test_full_rank_codec_round_trips_on_gpu():
     # bf16 layers of whole 64-token, 64-column tiles take the fused encoder:
     (3, 128, 256, 80, 128, W.BF16),   # r_h inside the second 64-row block, two column tiles
     (2, 256, 384, 256, 192, W.BF16),  # three column tiles of a token tile placed on one XCD
-    (17, 64, 128, 16, 64, W.BF16),    # one tile per slice, more slices than one batch
+    (17, 128, 128, 16, 64, W.BF16),   # two tiles per slice, more slices than one batch
+    # at most 64 tokens per slice take the small-batch encoder and decoder:
+    (3, 48, 256, 32, 48, W.BF16),
+    (2, 64, 256, 64, 256, W.F32),     # the largest r_h and r_w of that path
 ])
 def test_codec_slices_and_separate_decoder_projections(c, h, w, rh, rw, dt):
     """Several slices coded with one U, V; decoder projections different from the encoder's."""
