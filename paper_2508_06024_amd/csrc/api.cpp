@@ -592,19 +592,23 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
     if (desc->n_slices == 1) {
         // Wt = V_hat Z^T  [w][r_h]: both operands are K-contiguous rows (V_hat [w][r_w], Z [r_h][r_w]).
         // In bf16 layers Z is rounded to bf16 first (the product runs on the bf16 matrix cores;
-        // Wt itself is rounded to bf16 anyway).
-        const void* zop = z;
-        if (dt == DType::BF16) {
-            e = launch_f32_to_bf16(z, zn, at<void>(ws, w.zb), stream);
-            zop = at<void>(ws, w.zb);
-        }
-        if (e == hipSuccess) {
-            GemmArgs gw{};
-            gw.tok = v_hat; gw.row_index = nullptr; gw.w = zop; gw.w_group_stride = 0; gw.seg = nullptr;
-            gw.n_groups = 1; gw.rows = desc->w; gw.K = desc->r_w; gw.N = desc->r_h; gw.out = wt; gw.ldo = desc->r_h;
-            gw.name = "codec_vzt";
-            gw.src_rows = desc->w; gw.w_rows = desc->r_h; gw.part = at<float>(ws, w.gpart); gw.max_split = kMaxSplit;
-            e = launch_gemm(dt, Epilogue::Store, OutType::Same, gw, stream);
+        // Wt itself is rounded to bf16 anyway), inside the one-launch product where the shape allows.
+        if (vzt_ok(dt, desc->w, desc->r_h, desc->r_w)) {
+            e = launch_vzt(z, v_hat, desc->w, desc->r_h, desc->r_w, 1, wt, stream);
+        } else {
+            const void* zop = z;
+            if (dt == DType::BF16) {
+                e = launch_f32_to_bf16(z, zn, at<void>(ws, w.zb), stream);
+                zop = at<void>(ws, w.zb);
+            }
+            if (e == hipSuccess) {
+                GemmArgs gw{};
+                gw.tok = v_hat; gw.row_index = nullptr; gw.w = zop; gw.w_group_stride = 0; gw.seg = nullptr;
+                gw.n_groups = 1; gw.rows = desc->w; gw.K = desc->r_w; gw.N = desc->r_h; gw.out = wt; gw.ldo = desc->r_h;
+                gw.name = "codec_vzt";
+                gw.src_rows = desc->w; gw.w_rows = desc->r_h; gw.part = at<float>(ws, w.gpart); gw.max_split = kMaxSplit;
+                e = launch_gemm(dt, Epilogue::Store, OutType::Same, gw, stream);
+            }
         }
         if (e == hipSuccess) {
             // X_hat = U_hat Wt^T  [h][w]
@@ -625,16 +629,21 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
     for (int c0 = 0; c0 < desc->n_slices && e == hipSuccess; c0 += w.batch) {
         const int nc = std::min(w.batch, desc->n_slices - c0);
         const float* zc = z + static_cast<size_t>(c0) * zn;
-        void* zb = dt == DType::BF16 ? at<void>(ws, w.zb) : nullptr;
+        const bool vzt = vzt_ok(dt, desc->w, desc->r_h, desc->r_w);
+        void* zb = dt == DType::BF16 && !vzt ? at<void>(ws, w.zb) : nullptr;
         e = launch_codec_prep(zc, nc * zn, zb, nc, desc->w, desc->h, seg_w, rows_w, seg_h, rows_h, stream);
         if (e != hipSuccess) break;
         // Wt[s] = V_hat Z[s]^T  [w][r_h]
-        GemmArgs gw{};
-        gw.tok = v_hat; gw.row_index = rows_w; gw.w = zb ? zb : static_cast<const void*>(zc); gw.w_group_stride = zn;
-        gw.seg = seg_w; gw.n_groups = nc; gw.rows = int64_t(nc) * desc->w; gw.K = desc->r_w; gw.N = desc->r_h;
-        gw.out = wt; gw.ldo = desc->r_h; gw.name = "codec_vzt";
-        gw.src_rows = desc->w; gw.w_rows = desc->r_h; gw.part = at<float>(ws, w.gpart); gw.max_split = kMaxSplit;
-        e = launch_gemm(dt, Epilogue::Store, OutType::Same, gw, stream);
+        if (vzt) {
+            e = launch_vzt(zc, v_hat, desc->w, desc->r_h, desc->r_w, nc, wt, stream);
+        } else {
+            GemmArgs gw{};
+            gw.tok = v_hat; gw.row_index = rows_w; gw.w = zb ? zb : static_cast<const void*>(zc);
+            gw.w_group_stride = zn; gw.seg = seg_w; gw.n_groups = nc; gw.rows = int64_t(nc) * desc->w;
+            gw.K = desc->r_w; gw.N = desc->r_h; gw.out = wt; gw.ldo = desc->r_h; gw.name = "codec_vzt";
+            gw.src_rows = desc->w; gw.w_rows = desc->r_h; gw.part = at<float>(ws, w.gpart); gw.max_split = kMaxSplit;
+            e = launch_gemm(dt, Epilogue::Store, OutType::Same, gw, stream);
+        }
         if (e != hipSuccess) break;
         // X_hat[s] = U_hat Wt[s]^T  [h][w]
         GemmArgs g{};

@@ -707,6 +707,94 @@ __global__ __launch_bounds__(256) void dec_small_kernel(const float* __restrict_
     }
 }
 
+// ------------------------------------------------------------------ decoder, W = V_hat Z^T (bf16)
+//
+// Wt[s][j][i] = sum_c V_hat[j][c] * bf16(Z[s][i][c]), rounded to bfloat16: the first product of
+// the decoder with the rounding of Z folded into the staging (one launch instead of a rounding
+// pass and a GEMM). A workgroup owns 64 rows j of V_hat and 64 rows i of Z: it loads both
+// blocks whole with coalesced 16-byte loads (all of a thread's loads in flight at once), Z
+// rounded to bf16 on the way into LDS, and each of its four waves computes one 32 x 32 block
+// on v_mfma_f32_32x32x16_bf16 over K = r_w <= 256, Z as the A operand (lane l: row l % 32,
+// k-run 8 (l / 32) of each 16-wide step) and V_hat as the B operand, so that a lane's results
+// are four runs of four consecutive i of one row j: 8-byte stores.
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+constexpr int kVztT = 64;                // rows j and rows i per workgroup
+constexpr int kVztPitch = 256 * 2 + 16;  // LDS bytes per staged row (r_w <= 256, 16 bytes of skew)
+
+__global__ __launch_bounds__(256) void vzt_kernel(const float* __restrict__ z, const bf16_t* __restrict__ v_hat,
+                                                  int w, int rh, int rw, bf16_t* __restrict__ wt) {
+    __shared__ __attribute__((aligned(16))) char zs[kVztT * kVztPitch];
+    __shared__ __attribute__((aligned(16))) char vs[kVztT * kVztPitch];
+    const int j0 = blockIdx.x * kVztT, i0 = blockIdx.y * kVztT, s = blockIdx.z;
+    const int pitch = rw * 2 + 16;
+    // Z: 64 rows of r_w / 4 four-float chunks, thread t loading chunk t % 64 of rows t / 64 + 4 q;
+    // V_hat: 64 rows of r_w / 8 eight-bf16 chunks, chunk t % 32 of rows t / 32 + 8 q
+    // (no integer division in the address arithmetic; lanes past r_w idle)
+    constexpr int ZQ = kVztT / 4, VQ = kVztT / 8;
+    const int zc = threadIdx.x & 63, zr0 = threadIdx.x >> 6;
+    const int vc = threadIdx.x & 31, vr0 = threadIdx.x >> 5;
+    const bool zon = zc < rw / 4, von = vc < rw / 8;
+    f32x4 zr[ZQ];
+    uint4 vr[VQ];
+#pragma unroll
+    for (int q = 0; q < ZQ; ++q) {
+        const int i = std::min(i0 + zr0 + 4 * q, rh - 1);  // rows past r_h repeat the last (not stored)
+        if (zon) zr[q] = *reinterpret_cast<const f32x4*>(z + (static_cast<int64_t>(s) * rh + i) * rw + 4 * zc);
+    }
+#pragma unroll
+    for (int q = 0; q < VQ; ++q)
+        if (von) vr[q] = ldg16(v_hat + static_cast<int64_t>(j0 + vr0 + 8 * q) * rw + 8 * vc);
+    if (zon) {
+#pragma unroll
+        for (int q = 0; q < ZQ; ++q) {
+            bf16x4 o;  // hardware round-to-nearest-even (v_cvt_pk_bf16_f32)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(zr[q][e]);
+            *reinterpret_cast<bf16x4*>(zs + (zr0 + 4 * q) * pitch + 8 * zc) = o;
+        }
+    }
+    if (von) {
+#pragma unroll
+        for (int q = 0; q < VQ; ++q) *reinterpret_cast<uint4*>(vs + (vr0 + 8 * q) * pitch + 16 * vc) = vr[q];
+    }
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int l32 = lane & 31, lh = lane >> 5;
+    const int wi = wave >> 1, wj = wave & 1;
+    const char* arow = zs + (32 * wi + l32) * pitch + 16 * lh;
+    const char* brow = vs + (32 * wj + l32) * pitch + 16 * lh;
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    // all fragments read before the products (16 k-steps at most)
+    const int nk = rw / 16;
+    uint4 fa[16], fb[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+        if (k < nk) {
+            fa[k] = *reinterpret_cast<const uint4*>(arow + 32 * k);
+            fb[k] = *reinterpret_cast<const uint4*>(brow + 32 * k);
+        }
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+        if (k < nk)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[k]), __builtin_bit_cast(bf16x8, fb[k]),
+                                                         acc, 0, 0, 0);
+    // lane: row j of Wt, columns i0 + 32 wi + 8 q + 4 lh + e of acc[4 q + e]
+    const int j = j0 + 32 * wj + l32;
+    bf16_t* out = wt + (static_cast<int64_t>(s) * w + j) * rh;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int i = i0 + 32 * wi + 8 * q + 4 * lh;
+        if (i < rh) {  // r_h is a multiple of 4: the run of four is whole
+            bf16x4 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(acc[4 * q + e]);
+            *reinterpret_cast<bf16x4*>(out + i) = o;
+        }
+    }
+}
+
 // dst[i] = round-to-nearest-even bfloat16 of src[i], four elements per thread (n a multiple of 4)
 __global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ src, int64_t n,
                                                           bf16_t* __restrict__ dst) {
@@ -892,6 +980,17 @@ hipError_t launch_codec_prep(const float* z, int64_t nz, void* zb, int n, int w,
     ProfileScope prof("codec_prep", s);
     hipLaunchKernelGGL(codec_prep_kernel, dim3(grid), dim3(256), 0, s, z, nz, static_cast<bf16_t*>(zb), n, w, h,
                        seg_w, rows_w, seg_h, rows_h);
+    return hipGetLastError();
+}
+
+bool vzt_ok(DType dt, int w, int rh, int rw) {
+    return dt == DType::BF16 && w % kVztT == 0 && rh > 0 && rh % 4 == 0 && rw > 0 && rw % 16 == 0 && rw <= 256;
+}
+
+hipError_t launch_vzt(const float* z, const void* v_hat, int w, int rh, int rw, int slices, void* wt, hipStream_t s) {
+    ProfileScope prof("codec_vzt", s);
+    hipLaunchKernelGGL(vzt_kernel, dim3(w / kVztT, (rh + kVztT - 1) / kVztT, slices), dim3(256), 0, s, z,
+                       static_cast<const bf16_t*>(v_hat), w, rh, rw, static_cast<bf16_t*>(wt));
     return hipGetLastError();
 }
 

@@ -13,9 +13,10 @@ namespace {
 constexpr int kMaxK = 16;
 constexpr int kTokPerBlock = 4;  // one wave per token
 
-// B chunks of 16 bytes per lane per batch, with all B*k row loads issued before the sums
-template <typename T, int KMAX, int B>
-__global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y_perm, const int32_t* __restrict__ inv_perm,
+// B chunks of 16 bytes per lane per batch, with all B*k row loads issued before the sums;
+// NT: loads and stores with the streaming cache policy
+template <typename T, int KMAX, int B, bool NT>
+__global__ __launch_bounds__(64 * kTokPerBlock) void combine_kernel(const T* __restrict__ y_perm, const int32_t* __restrict__ inv_perm,
                                                       const float* __restrict__ w, int n_tokens, int top_k, int d,
                                                       T* __restrict__ y) {
     constexpr int EPC = Elem<T>::kPerChunk;
@@ -47,7 +48,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y_pe
             for (int j = 0; j < KMAX; ++j) {
                 const int c = c0 + 64 * b;
                 v[b][j] = (j < top_k && pos[j] >= 0 && c < cend)
-                              ? ldg16(y_perm + static_cast<int64_t>(pos[j]) * d + c * EPC)
+                              ? (NT ? ldg16_nt(y_perm + static_cast<int64_t>(pos[j]) * d + c * EPC)
+                                    : ldg16(y_perm + static_cast<int64_t>(pos[j]) * d + c * EPC))
                               : make_uint4(0, 0, 0, 0);
             }
 #pragma unroll
@@ -69,12 +71,13 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y_pe
             T* oe = reinterpret_cast<T*>(&o);
 #pragma unroll
             for (int i = 0; i < EPC; ++i) oe[i] = Elem<T>::from_f32(acc[i]);
-            stg16(y + static_cast<int64_t>(t) * d + c * EPC, o);
+            if (NT) stg16_nt(y + static_cast<int64_t>(t) * d + c * EPC, o);
+            else stg16(y + static_cast<int64_t>(t) * d + c * EPC, o);
         }
     }
 }
 
-template <typename T, int KMAX, int B>
+template <typename T, int KMAX, int B, bool NT>
 void launch_k(const void* y_perm, const int32_t* inv_perm, const float* w, int n_tokens, int top_k, int d, void* y,
               hipStream_t s) {
     const int grid = (n_tokens + kTokPerBlock - 1) / kTokPerBlock;
@@ -82,7 +85,7 @@ void launch_k(const void* y_perm, const int32_t* inv_perm, const float* w, int n
     const int chunks = d / Elem<T>::kPerChunk;
     int ysplit = 1;
     while (n_tokens * ysplit * 2 <= 1024 && chunks % (ysplit * 2) == 0 && chunks / (ysplit * 2) >= 64) ysplit *= 2;
-    hipLaunchKernelGGL((combine_kernel<T, KMAX, B>), dim3(grid, ysplit), dim3(64 * kTokPerBlock), 0, s,
+    hipLaunchKernelGGL((combine_kernel<T, KMAX, B, NT>), dim3(grid, ysplit), dim3(64 * kTokPerBlock), 0, s,
                        static_cast<const T*>(y_perm), inv_perm, w, n_tokens, top_k, d, static_cast<T*>(y));
 }
 
@@ -90,11 +93,13 @@ template <typename T>
 void launch_t(const void* y_perm, const int32_t* inv_perm, const float* w, int n_tokens, int top_k, int d, void* y,
               hipStream_t s) {
     // four to eight row loads in flight per lane: more (longer batches) measured slower, e.g.
-    // 18.7 against 15.9 us for 8 against 2 chunks per slot at k = 2, 4096 tokens of 4096
-    if (top_k <= 2) launch_k<T, 2, 2>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
-    else if (top_k <= 4) launch_k<T, 4, 1>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
-    else if (top_k <= 8) launch_k<T, 8, 1>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
-    else launch_k<T, kMaxK, 1>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
+    // 18.7 against 15.9 us for 8 against 2 chunks per slot at k = 2, 4096 tokens of 4096.
+    // From k = 5 on, the streaming cache policy: in the layer (expert outputs just written by
+    // the down GEMM) 40.7 against 43.7 us at k = 6, 8192 tokens of 2048; no difference at k = 2.
+    if (top_k <= 2) launch_k<T, 2, 2, false>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
+    else if (top_k <= 4) launch_k<T, 4, 1, false>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
+    else if (top_k <= 8) launch_k<T, 8, 1, true>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
+    else launch_k<T, kMaxK, 1, true>(y_perm, inv_perm, w, n_tokens, top_k, d, y, s);
 }
 
 }  // namespace

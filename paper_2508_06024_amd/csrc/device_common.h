@@ -85,4 +85,17 @@ __device__ __forceinline__ void stg16(void* p, uint4 v) {
     *reinterpret_cast<uint4*>(p) = v;
 }
 
+// 16-byte load and store with the non-temporal (streaming) cache policy: for data read or
+// written once, so that it does not displace lines that are reused.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ldg16_nt(const void* p) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+__device__ __forceinline__ void stg16_nt(void* p, uint4 v) {
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t*>(p));
+}
+
 }  // namespace ec2moe

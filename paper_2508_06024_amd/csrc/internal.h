@@ -118,5 +118,10 @@ hipError_t launch_unfold(DType dt, const void* x, int c, int h, int w, void* xu,
 
 // dst = bfloat16(src) with round-to-nearest-even, n a multiple of 4
 hipError_t launch_f32_to_bf16(const float* src, int64_t n, void* dst, hipStream_t s);
+// Decoder product Wt[s] = V_hat bf16(Z[s])^T [w][r_h] in one launch for bf16 layers
+// (w a multiple of 64, r_h of 4, r_w of 16 and at most 256); vzt_ok tells whether the shape qualifies.
+bool vzt_ok(DType dt, int w, int rh, int rw);
+hipError_t launch_vzt(const float* z, const void* v_hat, int w, int rh, int rw, int slices, void* wt, hipStream_t s);
+
 
 }  // namespace ec2moe
