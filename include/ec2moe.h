@@ -245,7 +245,8 @@ const char* ec2moe_last_error(void);
 
 /*
  * Kernel timing. While enabled, every kernel the library launches is bracketed by two
- * HIP events recorded on its launch stream. ec2moe_profile_collect waits for the
+ * HIP events recorded on its launch stream (timing-only events, created without the
+ * system-scope memory fence on record). ec2moe_profile_collect waits for the
  * recorded events, writes up to max_entries per-kernel totals (name, launches, total
  * milliseconds) in first-launch order, sets *n_out, and clears the record.
  */

@@ -246,8 +246,11 @@ struct Profiler {
             pool.pop_back();
             return e;
         }
+        // Timing-only events, without the system-scope fence of a default event record (a
+        // writeback of every XCD's L2). An event record still leaves ~5 us of idle time on
+        // each side of a timed kernel (layer step: 2.544 against 2.538 ms per step untimed).
         hipEvent_t e = nullptr;
-        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
         return e;
     }
 };
