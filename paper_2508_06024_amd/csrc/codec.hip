@@ -3,9 +3,10 @@
 // one workgroup per 64 x 64 tile of P); the contraction Z = U^T P of the other shapes at
 // float32 accuracy (P = X V in float32; bfloat16 U on the bf16 matrix cores with P split in
 // three bf16 planes, float32 U on the float32 matrix cores); the in-order reduction of the
-// partial sums over token tiles or chunks; and the float32 -> bfloat16 rounding of Z for the
-// decoder. The decoder's products V_hat Z^T and U_hat W^T, and X V outside the fused
-// encoder, run on the matrix-core GEMM.
+// partial sums over token tiles or chunks; the small-batch encoder and decoder (at most 64
+// tokens per slice, float32 throughout); the decoder's first product W = V_hat bf16(Z)^T of
+// bf16 layers in one launch; and the float32 -> bfloat16 rounding of Z for the decoder's
+// other shapes. U_hat W^T, and X V outside the fused encoder, run on the matrix-core GEMM.
 #include "device_common.h"
 #include "internal.h"
 
