@@ -167,7 +167,9 @@ def test_moe_forward_full_size_every_row(name):
 @pytest.mark.parametrize("T,k,d,dt", [(777, 6, 2048, W.BF16),
                                       (5, 8, 4096, W.BF16),    # few tokens: rows split over workgroups
                                       (1, 2, 1024, W.BF16),
-                                      (37, 3, 512, W.F32)])
+                                      (37, 3, 512, W.F32),
+                                      (64, 16, 1024, W.F32),   # the widest slot count
+                                      (50, 12, 768, W.BF16)])
 def test_combine_matches_oracle(T, k, d, dt):
     rng = np.random.default_rng(21)
     idx, w = W.gen_routing(T, 64, k, range(64), seed=5)
