@@ -67,6 +67,9 @@ struct TileInfo {
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// s_waitcnt immediate for vmcnt(n), lgkmcnt(0) and no expcnt wait: n <= 63 (vmcnt bits 3:0 and 15:14)
+constexpr int vmcnt_imm(int n) { return 0x0070 | (n & 15) | ((n >> 4) << 14); }
+
 // Number of real tiles (uniform): sum over groups of ceil(rows_e / TM) * ntn.
 template <int TM>
 __device__ __forceinline__ int count_tiles(const GemmArgs& a, int ntn) {
@@ -712,7 +715,11 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_lds_kernel(GemmArgs a) {
 //   group 0, slab s: issue token rows of slab s+1 | read slab s | barrier | MFMA slab s |
 //                    wait own loads | barrier
 //   group 1, slab s: MFMA slab s-1 | barrier | read slab s, then issue weight rows of slab
-//                    s+2 into the same stage | wait loads of slab s+1 | barrier
+//                    s+3 into the same slot | wait loads of slab s+1 | barrier
+// Token rows (served by the L2 and the last-level cache: each expert's rows are re-read once
+// per window of n-tiles) sit in two 32 KB slots; weight rows (streamed from HBM, shared by the
+// m-tiles of a window) in three, so their loads have about two and a half slabs to land
+// instead of one and a half (Mixtral-shaped gate-up launch 1570 against 1581 us).
 template <bool SWIGLU, typename TO>
 __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
     constexpr int TM = 256, TN = 256, WM = 4, WN = 2, NW = 8;
@@ -721,13 +728,19 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
     constexpr int NOUT = SWIGLU ? TN / 2 : TN;
     constexpr int ROWS = TM + TN;
     constexpr int RB = 128;
-    constexpr int STAGE = ROWS * RB;
+    constexpr int SLOT = TM * RB;              // 32 KB: the token rows, or the weight rows, of one slab
+    static_assert(TM == TN, "token and weight slots of one size");
     constexpr int WROWS = ROWS / NW;           // 64
     constexpr int LOADS = WROWS / 8;           // 8
-    static_assert(LOADS < 16, "vmcnt immediate");
+    static_assert(2 * LOADS < 64, "vmcnt immediate");
 
-    __shared__ __attribute__((aligned(1024))) char lds0[STAGE];
-    __shared__ __attribute__((aligned(1024))) char lds1[STAGE];
+    // one LDS object per slot (each named at compile time where it is read, so a wait before
+    // a fragment read covers only the loads into that slot): 160 KB in all
+    __shared__ __attribute__((aligned(1024))) char t0[SLOT];
+    __shared__ __attribute__((aligned(1024))) char t1[SLOT];
+    __shared__ __attribute__((aligned(1024))) char w0[SLOT];
+    __shared__ __attribute__((aligned(1024))) char w1[SLOT];
+    __shared__ __attribute__((aligned(1024))) char w2[SLOT];
 
     const int ntn = (a.N + NOUT - 1) / NOUT;
     const int K = a.K;
@@ -779,12 +792,13 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
             voff[i] = static_cast<uint32_t>(weight_row<TN, SWIGLU>(a, ti.nt, row - TM)) * row_bytes + chunk_off;
         }
     }
-    auto issue_slab = [&](int ks, char* stage) {
+    // this wave's rows of a slab into a token or weight slot (rows 64 (wave & 3) .. + 63 of it)
+    auto issue_slab = [&](int ks, char* slot) {
         const int soff = (kb + ks) * RB;
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
             lds_void* dst = reinterpret_cast<lds_void*>(
-                reinterpret_cast<uintptr_t>(stage + (wave * WROWS + i * 8) * RB));
+                reinterpret_cast<uintptr_t>(slot + ((wave & 3) * WROWS + i * 8) * RB));
             raw_buffer_load_lds(rs, dst, 16, static_cast<int>(voff[i]), soff, 0, 0);
         }
     };
@@ -798,8 +812,8 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
         const int ch = ((2 * s + lh) ^ sw) * 16;
-        off_t[s] = (wm * WTOK + l32) * RB + ch;
-        off_w[s] = (TM + wn * WW + l32) * RB + ch;
+        off_t[s] = (wm * WTOK + l32) * RB + ch;  // in a token slot
+        off_w[s] = (wn * WW + l32) * RB + ch;    // in a weight slot (same swizzle: row offsets of 32)
     }
     auto wblk = [](int ni) constexpr {
         if (SWIGLU) {
@@ -818,13 +832,13 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
             for (int r = 0; r < 16; ++r) acc[ni][mi][r] = 0.f;
 
     uint4 fa[4][NI], fb[4][MI];  // one slab of fragments
-    auto read_slab = [&](const char* base) {
+    auto read_slab = [&](const char* tslot, const char* wslot) {
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) fa[s][ni] = *reinterpret_cast<const uint4*>(base + off_w[s] + wblk(ni) * RB);
+            for (int ni = 0; ni < NI; ++ni) fa[s][ni] = *reinterpret_cast<const uint4*>(wslot + off_w[s] + wblk(ni) * RB);
 #pragma unroll
-            for (int mi = 0; mi < MI; ++mi) fb[s][mi] = *reinterpret_cast<const uint4*>(base + off_t[s] + mi * 32 * RB);
+            for (int mi = 0; mi < MI; ++mi) fb[s][mi] = *reinterpret_cast<const uint4*>(tslot + off_t[s] + mi * 32 * RB);
         }
     };
     auto mma_slab = [&]() {
@@ -847,14 +861,27 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
     };
 
     if (nk > 0) {  // nk is even and the same for every wave
-        issue_slab(0, lds0);
-        issue_slab(1, lds1);
-        __builtin_amdgcn_s_waitcnt(0x0070 | LOADS);  // own rows of slab 0 landed
-        barrier();
         if (tok_wave) {
-            auto slab0 = [&](const char* cur, char* nxt, int s) {
-                if (s >= 1 && s + 1 < nk) issue_slab(s + 1, nxt);
-                read_slab(cur);
+            issue_slab(0, t0);
+            issue_slab(1, t1);
+            __builtin_amdgcn_s_waitcnt(0x0070 | LOADS);  // own rows of slab 0 landed
+        } else {
+            issue_slab(0, w0);
+            issue_slab(1, w1);
+            if (nk > 2) {
+                issue_slab(2, w2);
+                __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));
+            } else {
+                __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
+            }
+        }
+        barrier();
+        // slab s: tokens in slot s % 2, weights in slot s % 3 (the loops run six slabs a turn)
+        if (tok_wave) {
+            auto slab0 = [&](const char* tcur, char* tnxt, const char* wcur, int s) {
+                if (s >= nk) return;
+                if (s >= 1 && s + 1 < nk) issue_slab(s + 1, tnxt);
+                read_slab(tcur, wcur);
                 __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
                 barrier();
                 mma_slab();
@@ -862,27 +889,38 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
                 __builtin_amdgcn_s_waitcnt(0x0070);  // token rows of slab s+1 landed
                 barrier();
             };
-            for (int s = 0; s < nk; s += 2) {
-                slab0(lds0, lds1, s);
-                slab0(lds1, lds0, s + 1);
+            for (int s = 0; s < nk; s += 6) {
+                slab0(t0, t1, w0, s);
+                slab0(t1, t0, w1, s + 1);
+                slab0(t0, t1, w2, s + 2);
+                slab0(t1, t0, w0, s + 3);
+                slab0(t0, t1, w1, s + 4);
+                slab0(t1, t0, w2, s + 5);
             }
         } else {
-            auto slab1 = [&](char* cur, int s) {
+            auto slab1 = [&](const char* tcur, char* wcur, int s) {
+                if (s >= nk) return;
                 if (s > 0) mma_slab();
                 barrier();
-                read_slab(cur);
-                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this stage's reads done
-                if (s + 2 < nk) {
-                    issue_slab(s + 2, cur);
-                    __builtin_amdgcn_s_waitcnt(0x0070 | LOADS);  // weight rows of slab s+1 landed
+                read_slab(tcur, wcur);
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this slot's reads done
+                if (s + 3 < nk) {
+                    issue_slab(s + 3, wcur);
+                    __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));  // weight rows of slab s+1 landed
+                } else if (s + 2 < nk) {
+                    __builtin_amdgcn_s_waitcnt(0x0070 | LOADS);
                 } else {
                     __builtin_amdgcn_s_waitcnt(0x0070);
                 }
                 barrier();
             };
-            for (int s = 0; s < nk; s += 2) {
-                slab1(lds0, s);
-                slab1(lds1, s + 1);
+            for (int s = 0; s < nk; s += 6) {
+                slab1(t0, w0, s);
+                slab1(t1, w1, s + 1);
+                slab1(t0, w2, s + 2);
+                slab1(t1, w0, s + 3);
+                slab1(t0, w1, s + 4);
+                slab1(t1, w2, s + 5);
             }
             mma_slab();
         }
@@ -910,15 +948,16 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
     if constexpr (sizeof(TO) == 4) {
         write_tile32<TO, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
     } else {
-        // The finished tile is staged in LDS as bf16 rows (both stages are free after the last
+        // The finished tile is staged in LDS as bf16 rows (every slot is free after the last
         // slab) so that the global stores are whole rows: 16 bytes per lane, 128-byte lines.
         // Staged row r holds its 16-byte chunk c at c ^ (r % OCH).
         constexpr int OROW = NOUT * 2;   // bytes per staged row
         constexpr int OCH = OROW / 16;   // 16-byte chunks per row
-        constexpr int RPS = STAGE / OROW;  // rows per LDS stage (all 256 for SwiGLU, 128 otherwise)
-        static_assert(TM <= 2 * RPS && WTOK <= RPS && RPS % WTOK == 0, "staged tile fits the two stages");
-        // this wave's rows wm * 64 .. wm * 64 + 63 lie in one stage
-        char* wst = (wm * WTOK < RPS ? lds0 : lds1) + (wm * WTOK % RPS) * OROW;
+        constexpr int RPS = SLOT / OROW;  // rows per 32 KB slot (128 for SwiGLU, 64 otherwise)
+        static_assert(TM <= 4 * RPS && WTOK <= RPS && RPS % WTOK == 0, "staged tile fits four slots");
+        auto ost = [&](int i) -> char* { return i == 0 ? t0 : i == 1 ? t1 : i == 2 ? w0 : w1; };
+        // this wave's rows wm * 64 .. wm * 64 + 63 lie in one slot
+        char* wst = ost(wm * WTOK / RPS) + (wm * WTOK % RPS) * OROW;
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
             const int r = mi * 32 + l32;  // row within this wave's 64
@@ -952,12 +991,12 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
         for (int j = 0; j < NINSTR; ++j) {
             const int r = wave * (TM / NW) + j * RPI + lane / OCH;  // tile row
             const int c = lane % OCH;
-            const char* src = (r < RPS ? lds0 : lds1) + (r % RPS) * OROW + ((c ^ (r % OCH)) * 16);
+            const char* src = ost(r / RPS) + (r % RPS) * OROW + ((c ^ (r % OCH)) * 16);
             const uint4 v = *reinterpret_cast<const uint4*>(src);
             const int col = ti.nt * NOUT + c * 8;
             if (r < ti.valid && col < a.N) *reinterpret_cast<uint4*>(out + (ti.row0 + r) * a.ldo + col) = v;
         }
-        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): staged rows read before the stages refill
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): staged rows read before the slots refill
         barrier();
     }
     }
