@@ -14,14 +14,15 @@
 // weight and token slabs. Each XCD walks one contiguous stretch of the logical order.
 //
 // Workgroup tile: TM token rows x TN weight rows, waves in a WM x WN grid. Each K-step
-// moves one 128-byte slab of every tile row (64 bf16 or 32 fp32 values) into LDS, double
-// buffered. Weight rows feed the MFMA A operand and token rows the B operand, so every
+// moves one 128-byte slab of every tile row (64 bf16 or 32 fp32 values) into LDS, at least
+// double buffered. Weight rows feed the MFMA A operand and token rows the B operand, so every
 // lane ends with 4 consecutive output columns of one token row (one 8- or 16-byte store).
 //
 // Three mainloops:
 //   * gemm_pp_kernel (bf16 256x256 tiles, K a multiple of 128, 32x32x16 MFMA): persistent
 //     (one workgroup per CU, each XCD's workgroups stepping through consecutive tiles
-//     together); buffer loads write the slabs straight into LDS (no register staging);
+//     together); buffer loads write the slabs straight into LDS (no register staging; two
+//     slots for token rows, three for weight rows);
 //     8 waves in two groups of one wave per SIMD that alternate between a phase of
 //     matrix-core work and a phase of memory work, so every SIMD always has a wave
 //     issuing MFMAs; the last partial round of tiles is split along K (float32 partials,
