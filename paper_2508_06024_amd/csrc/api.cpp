@@ -210,7 +210,9 @@ CodecWs codec_ws(const ec2moe_codec_desc* d) {
                  : up(nb * chunks * d->r_h * d->r_w * 4);
     w.enc_total = o;
     o = shared;
-    w.zb = o; o += up(nb * d->r_h * d->r_w * eb);
+    // Z rounded to bf16 ahead of the decoder's GEMM, where the one-launch product does not apply
+    const bool vzt = vzt_ok(static_cast<DType>(d->dtype), d->w, d->r_h, d->r_w);
+    w.zb = o; o += vzt ? 0 : up(nb * d->r_h * d->r_w * eb);
     w.wt = o; o += up(nb * d->w * d->r_h * eb);
     w.seg_w = o; o += up((nb + 1) * 4);
     w.rows_w = o; o += up(nb * d->w * 4);
