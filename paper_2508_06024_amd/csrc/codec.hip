@@ -556,8 +556,8 @@ __global__ __launch_bounds__(512, 1) void encode_fused_kernel(EncArgs a) {
 // ------------------------------------------------------------------ small batches (h <= 64 tokens)
 //
 // With a few dozen tokens per slice the codec's products are tiny, and the launches of the
-// general path cost more than their work. Three launches do the whole round trip, in float32
-// throughout (products of the layer dtype's values are exact in float32):
+// general path cost more than their work. Three launches do the whole round trip with float32
+// arithmetic throughout (exact products for bf16 layers), Z and U_hat Z kept in float32:
 //   enc_small_partial: part[s][kc][t][c] = sum over the 64 model columns k of chunk kc of
 //                      X[s][t][k] V[k][c] (one workgroup per chunk, 16 columns of P and slice);
 //   enc_small_finish:  P[t][c] = the chunk partials added in a fixed order (the even and the
