@@ -716,11 +716,11 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_lds_kernel(GemmArgs a) {
 //   group 0, slab s: issue token rows of slab s+1 | read slab s | barrier | MFMA slab s |
 //                    wait own loads | barrier
 //   group 1, slab s: MFMA slab s-1 | barrier | read slab s, then issue weight rows of slab
-//                    s+3 into the same slot | wait loads of slab s+1 | barrier
-// Token rows (served by the L2 and the last-level cache: each expert's rows are re-read once
-// per window of n-tiles) sit in two 32 KB slots; weight rows (streamed from HBM, shared by the
-// m-tiles of a window) in three, so their loads have about two and a half slabs to land
-// instead of one and a half (Mixtral-shaped gate-up launch 1570 against 1581 us).
+//                    s+2 into the slot of slab s-1 | wait loads of slab s+1 | barrier
+// Token rows sit in two 32 KB slots and weight rows in three, so that every slot is refilled
+// only after a barrier that follows the last read of it by any wave (with two combined
+// stages the weight rows of slab s+2 had to go into the stage of slab s, which the other
+// group could still be reading).
 template <bool SWIGLU, typename TO>
 __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
     constexpr int TM = 256, TN = 256, WM = 4, WN = 2, NW = 8;
@@ -869,12 +869,7 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
         } else {
             issue_slab(0, w0);
             issue_slab(1, w1);
-            if (nk > 2) {
-                issue_slab(2, w2);
-                __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));
-            } else {
-                __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
-            }
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));  // own rows of slab 0 landed
         }
         barrier();
         // slab s: tokens in slot s % 2, weights in slot s % 3 (the loops run six slabs a turn)
@@ -899,29 +894,29 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
                 slab0(t1, t0, w2, s + 5);
             }
         } else {
-            auto slab1 = [&](const char* tcur, char* wcur, int s) {
+            // The slot refilled in step s holds slab s - 1, whose last reads (this group's) were
+            // done before the previous barrier: no wave can still be reading it.
+            auto slab1 = [&](const char* tcur, const char* wcur, char* wfree, int s) {
                 if (s >= nk) return;
                 if (s > 0) mma_slab();
                 barrier();
                 read_slab(tcur, wcur);
-                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this slot's reads done
-                if (s + 3 < nk) {
-                    issue_slab(s + 3, wcur);
-                    __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));  // weight rows of slab s+1 landed
-                } else if (s + 2 < nk) {
-                    __builtin_amdgcn_s_waitcnt(0x0070 | LOADS);
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+                if (s + 2 < nk) {
+                    issue_slab(s + 2, wfree);
+                    __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));  // weight rows of slab s+1 landed
                 } else {
-                    __builtin_amdgcn_s_waitcnt(0x0070);
+                    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
                 }
                 barrier();
             };
             for (int s = 0; s < nk; s += 6) {
-                slab1(t0, w0, s);
-                slab1(t1, w1, s + 1);
-                slab1(t0, w2, s + 2);
-                slab1(t1, w0, s + 3);
-                slab1(t0, w1, s + 4);
-                slab1(t1, w2, s + 5);
+                slab1(t0, w0, w2, s);
+                slab1(t1, w1, w0, s + 1);
+                slab1(t0, w2, w1, s + 2);
+                slab1(t1, w0, w2, s + 3);
+                slab1(t0, w1, w0, s + 4);
+                slab1(t1, w2, w1, s + 5);
             }
             mma_slab();
         }
