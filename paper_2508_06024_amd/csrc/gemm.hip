@@ -281,21 +281,25 @@ __device__ __forceinline__ int weight_row(const GemmArgs& a, int nt, int n) {
 
 // ------------------------------------------------------------------ register-staged mainloop
 
-template <typename T, typename TO, int TM, int TN, int WM, int WN, bool SWIGLU>
+// CPR: 16-byte chunks of each tile row per slab (8: 128-byte rows; 16: 256-byte rows, half as
+// many slabs, for long K)
+template <typename T, typename TO, int TM, int TN, int WM, int WN, bool SWIGLU, int CPR>
 __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
     static_assert(WM * WN == 4, "4 waves per workgroup");
-    static_assert(TM % 32 == 0 && TN % 32 == 0, "tiles load 32 rows per pass");
+    constexpr int RPP = 256 / CPR;        // rows per load pass
+    static_assert(CPR == 8 || CPR == 16, "128- or 256-byte slab rows");
+    static_assert(TM % RPP == 0 && TN % RPP == 0, "tiles load whole passes");
     constexpr int EPC = Elem<T>::kPerChunk;
-    constexpr int BK = 8 * EPC;           // elements per 128-byte slab row
+    constexpr int BK = CPR * EPC;         // elements per slab row
     constexpr int MI = TM / WM / 16;      // token blocks per wave
     constexpr int NI = TN / WN / 16;      // weight blocks per wave
-    constexpr int TOK_PASSES = TM / 32;
-    constexpr int W_PASSES = TN / 32;
+    constexpr int TOK_PASSES = TM / RPP;
+    constexpr int W_PASSES = TN / RPP;
     constexpr int NOUT = SWIGLU ? TN / 2 : TN;
     constexpr int ROWS = TM + TN;
     static_assert(!SWIGLU || NI % 2 == 0, "SwiGLU waves hold matching gate/up blocks");
 
-    __shared__ uint4 lds[2][ROWS * 8];
+    __shared__ uint4 lds[2][ROWS * CPR];
 
     const int ntn = (a.N + NOUT - 1) / NOUT;
     TileInfo ti;
@@ -308,23 +312,23 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
     const int wn = wave / WM;
     const int K = a.K;
 
-    // ---- global load addressing: thread -> (chunk c, rows rr + 32 i)
-    const int c = tid & 7;
-    const int rr = tid >> 3;
+    // ---- global load addressing: thread -> (chunk c, rows rr + RPP i)
+    const int c = tid % CPR;
+    const int rr = tid / CPR;
     const T* tok = static_cast<const T*>(a.tok);
     const T* wbase = static_cast<const T*>(a.w) + static_cast<int64_t>(ti.group) * a.w_group_stride;
     uint32_t tok_off[TOK_PASSES];
     uint32_t w_off[W_PASSES];
 #pragma unroll
     for (int i = 0; i < TOK_PASSES; ++i) {
-        const int r = std::min(rr + 32 * i, ti.valid - 1);
+        const int r = std::min(rr + RPP * i, ti.valid - 1);
         const int64_t p = ti.row0 + r;
         const int64_t src = a.row_index ? a.row_index[p] : p;
         tok_off[i] = static_cast<uint32_t>(src * K + c * EPC);
     }
 #pragma unroll
     for (int i = 0; i < W_PASSES; ++i) {
-        const int wrow = weight_row<TN, SWIGLU>(a, ti.nt, rr + 32 * i);
+        const int wrow = weight_row<TN, SWIGLU>(a, ti.nt, rr + RPP * i);
         w_off[i] = static_cast<uint32_t>(static_cast<int64_t>(wrow) * K + c * EPC);
     }
 
@@ -342,13 +346,13 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
     auto store_lds = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < TOK_PASSES; ++i) {
-            const int row = rr + 32 * i;
-            lds[buf][row * 8 + (c ^ (row & 7))] = stage_t[i];
+            const int row = rr + RPP * i;
+            lds[buf][row * CPR + (c ^ (row & (CPR - 1)))] = stage_t[i];
         }
 #pragma unroll
         for (int i = 0; i < W_PASSES; ++i) {
-            const int row = TM + rr + 32 * i;
-            lds[buf][row * 8 + (c ^ (row & 7))] = stage_w[i];
+            const int row = TM + rr + RPP * i;
+            lds[buf][row * CPR + (c ^ (row & (CPR - 1)))] = stage_w[i];
         }
     };
 
@@ -375,19 +379,19 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
         const int cur = ks & 1;
         if (ks + 1 < nk) load_global(ks + 1);
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
+        for (int s = 0; s < CPR / 4; ++s) {
             const int ch = 4 * s + lg;
             uint4 bt[MI];
             uint4 aw[NI];
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi) {
                 const int row = frag_t[mi];
-                bt[mi] = lds[cur][row * 8 + (ch ^ (row & 7))];
+                bt[mi] = lds[cur][row * CPR + (ch ^ (row & (CPR - 1)))];
             }
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) {
                 const int row = frag_w[ni];
-                aw[ni] = lds[cur][row * 8 + (ch ^ (row & 7))];
+                aw[ni] = lds[cur][row * CPR + (ch ^ (row & (CPR - 1)))];
             }
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni)
@@ -1064,13 +1068,13 @@ int64_t grid_size(const GemmArgs& a) {
     return (mtiles * ntn + kXcds - 1) / kXcds * kXcds;
 }
 
-template <typename T, typename TO, int TM, int TN, int WM, int WN, bool SWIGLU>
+template <typename T, typename TO, int TM, int TN, int WM, int WN, bool SWIGLU, int CPR = 8>
 hipError_t run(const GemmArgs& a, hipStream_t s) {
     const int64_t grid = grid_size<TM, TN, SWIGLU>(a);
     if (grid == 0) return hipSuccess;
     ProfileScope prof(a.name ? a.name : "gemm", s);
-    hipLaunchKernelGGL((gemm_kernel<T, TO, TM, TN, WM, WN, SWIGLU>), dim3(static_cast<unsigned>(grid)), dim3(256),
-                       0, s, a);
+    hipLaunchKernelGGL((gemm_kernel<T, TO, TM, TN, WM, WN, SWIGLU, CPR>), dim3(static_cast<unsigned>(grid)),
+                       dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -1159,7 +1163,12 @@ hipError_t dispatch(const GemmArgs& a, hipStream_t s) {
             if constexpr (kLdsPath)
                 if (lds_ok) return run_lds<128, 128, 2, 2, SWIGLU, TO>(a, s);
             return run<T, TO, 128, 128, 2, 2, SWIGLU>(a, s);
-        default: return run<T, TO, 32, 128, 1, 4, SWIGLU>(a, s);
+        // the small tile streams its whole K a slab at a time: 256-byte slab rows (half the
+        // slabs) for long K, e.g. the 64-expert ReLU layer's output layer (K = 3072): 38.2
+        // against 48.9 us; short K keeps 128-byte rows (K = 768 there: 19.9 against 22.9 us)
+        default:
+            if (a.K >= 2048) return run<T, TO, 32, 128, 1, 4, SWIGLU, 16>(a, s);
+            return run<T, TO, 32, 128, 1, 4, SWIGLU, 8>(a, s);
     }
 }
 

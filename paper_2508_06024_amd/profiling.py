@@ -23,11 +23,12 @@ from collections import defaultdict
 
 from . import roofline as R
 
+# register-staged GEMM instances; a trailing template argument of 16 marks 256-byte slab rows
 _SHORT = [
-    (r"gemm_kernel<ec2moe::bf16_t, ec2moe::bf16_t, (\d+), (\d+), \d, \d, true>", r"gemm swiglu bf16 \1x\2"),
-    (r"gemm_kernel<ec2moe::bf16_t, ec2moe::bf16_t, (\d+), (\d+), \d, \d, false>", r"gemm store bf16 \1x\2"),
-    (r"gemm_kernel<ec2moe::bf16_t, float, (\d+), (\d+), \d, \d, false>", r"gemm store bf16->f32 \1x\2"),
-    (r"gemm_kernel<float, float, (\d+), (\d+), \d, \d, (true|false)>", r"gemm f32 \1x\2 \3"),
+    (r"gemm_kernel<ec2moe::bf16_t, ec2moe::bf16_t, (\d+), (\d+), \d, \d, true(?:, (\d+))?>", "gemm swiglu bf16 {0}x{1}"),
+    (r"gemm_kernel<ec2moe::bf16_t, ec2moe::bf16_t, (\d+), (\d+), \d, \d, false(?:, (\d+))?>", "gemm store bf16 {0}x{1}"),
+    (r"gemm_kernel<ec2moe::bf16_t, float, (\d+), (\d+), \d, \d, false(?:, (\d+))?>", "gemm store bf16->f32 {0}x{1}"),
+    (r"gemm_kernel<float, float, (\d+), (\d+), \d, \d, (?:true|false)(?:, (\d+))?>", "gemm f32 {0}x{1}"),
 ]
 
 
@@ -36,7 +37,12 @@ def short_name(n: str) -> str:
     for pat, rep in _SHORT:
         m = re.search(pat, n)
         if m:
-            return m.expand(rep)
+            name = rep.format(m.group(1), m.group(2))
+            if "float, float" in m.group(0):
+                name += " swiglu" if ", true" in m.group(0) else " store"
+            if m.group(3) == "16":
+                name += " (256-byte slabs)"
+            return name
     n = re.sub(r"\(.*\)$", "", n)
     return n.replace("ec2moe::", "").replace("void ", "")
 
