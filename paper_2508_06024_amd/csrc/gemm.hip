@@ -281,13 +281,13 @@ __device__ __forceinline__ int weight_row(const GemmArgs& a, int nt, int n) {
 
 // ------------------------------------------------------------------ register-staged mainloop
 
-// CPR: 16-byte chunks of each tile row per slab (8: 128-byte rows; 16: 256-byte rows, half as
-// many slabs, for long K)
+// CPR: 16-byte chunks of each tile row per slab (8: 128-byte rows; 16 and 32: 256- and
+// 512-byte rows, a half and a quarter as many slabs, for long K)
 template <typename T, typename TO, int TM, int TN, int WM, int WN, bool SWIGLU, int CPR>
 __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs a) {
     static_assert(WM * WN == 4, "4 waves per workgroup");
     constexpr int RPP = 256 / CPR;        // rows per load pass
-    static_assert(CPR == 8 || CPR == 16, "128- or 256-byte slab rows");
+    static_assert(CPR == 8 || CPR == 16 || CPR == 32, "128-, 256- or 512-byte slab rows");
     static_assert(TM % RPP == 0 && TN % RPP == 0, "tiles load whole passes");
     constexpr int EPC = Elem<T>::kPerChunk;
     constexpr int BK = CPR * EPC;         // elements per slab row
@@ -1163,10 +1163,12 @@ hipError_t dispatch(const GemmArgs& a, hipStream_t s) {
             if constexpr (kLdsPath)
                 if (lds_ok) return run_lds<128, 128, 2, 2, SWIGLU, TO>(a, s);
             return run<T, TO, 128, 128, 2, 2, SWIGLU>(a, s);
-        // the small tile streams its whole K a slab at a time: 256-byte slab rows (half the
-        // slabs) for long K, e.g. the 64-expert ReLU layer's output layer (K = 3072): 38.2
-        // against 48.9 us; short K keeps 128-byte rows (K = 768 there: 19.9 against 22.9 us)
+        // the small tile streams its whole K a slab at a time: wider slab rows (fewer slabs) for
+        // long K, e.g. the 64-expert ReLU layer's output layer (K = 3072): 38.2 against 48.9 us
+        // with 256-byte rows, the decode workload's gate-up (K = 4096): 181 against 187 us with
+        // 512-byte rows; short K keeps 128-byte rows (K = 768: 19.9 against 22.9 us)
         default:
+            if (a.K >= 4096) return run<T, TO, 32, 128, 1, 4, SWIGLU, 32>(a, s);
             if (a.K >= 2048) return run<T, TO, 32, 128, 1, 4, SWIGLU, 16>(a, s);
             return run<T, TO, 32, 128, 1, 4, SWIGLU, 8>(a, s);
     }

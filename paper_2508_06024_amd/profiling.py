@@ -23,7 +23,7 @@ from collections import defaultdict
 
 from . import roofline as R
 
-# register-staged GEMM instances; a trailing template argument of 16 marks 256-byte slab rows
+# register-staged GEMM instances; a trailing template argument of 16 or 32 marks 256- or 512-byte slab rows
 _SHORT = [
     (r"gemm_kernel<ec2moe::bf16_t, ec2moe::bf16_t, (\d+), (\d+), \d, \d, true(?:, (\d+))?>", "gemm swiglu bf16 {0}x{1}"),
     (r"gemm_kernel<ec2moe::bf16_t, ec2moe::bf16_t, (\d+), (\d+), \d, \d, false(?:, (\d+))?>", "gemm store bf16 {0}x{1}"),
@@ -40,8 +40,8 @@ def short_name(n: str) -> str:
             name = rep.format(m.group(1), m.group(2))
             if "float, float" in m.group(0):
                 name += " swiglu" if ", true" in m.group(0) else " store"
-            if m.group(3) == "16":
-                name += " (256-byte slabs)"
+            if m.group(3) in ("16", "32"):
+                name += f" ({int(m.group(3)) * 16}-byte slabs)"
             return name
     n = re.sub(r"\(.*\)$", "", n)
     return n.replace("ec2moe::", "").replace("void ", "")
