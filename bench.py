@@ -249,16 +249,8 @@ def main():
     work_timed, active_timed = mean_work(steps) if per_call else (work, None)  # the calls of the timed region
 
     # per-kernel algorithmic work at the realised routing
-    base = {"gate_split": "gate", "perm_onepass": "permute", "perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
-            "transpose": "encode", "codec_xv": "encode", "codec_utp": "encode",
-            "codec_z_bf16": "decode", "codec_prep": "decode", "codec_vzt": "decode", "codec_uw": "decode"}
-
     def stage_of(name):
-        # a split-K "<kernel>_tail" / "<kernel>_reduce" launch belongs to its kernel's stage
-        for suf in ("_tail", "_reduce"):
-            if name.endswith(suf):
-                name = name[: -len(suf)]
-        return base.get(name, name)
+        return R.stage_of(name) or name
     peak_f = R.PEAK_TFLOPS[cfg.dtype]
     kernels = {}
     for name, (n, tot) in stats.items():

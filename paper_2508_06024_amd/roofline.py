@@ -50,6 +50,30 @@ def kernel_work(cfg, rows_per_expert: np.ndarray) -> dict:
     return work
 
 
+# Profile name of each library launch on the layer path -> the stage whose algorithmic work
+# (kernel_work) it shares. A split-K "<name>_tail" or "<name>_reduce" launch belongs to the
+# stage of <name>.
+STAGE_OF_KERNEL = {
+    "gate": "gate", "gate_split": "gate",
+    "perm_onepass": "permute", "perm_count": "permute", "perm_scan": "permute", "perm_scatter": "permute",
+    "gather_rows": "permute",
+    "transpose": "encode", "codec_xv": "encode", "codec_utp": "encode", "codec_encode": "encode",
+    "codec_encode_part": "encode", "codec_encode_finish": "encode",
+    "codec_z_bf16": "decode", "codec_prep": "decode", "codec_vzt": "decode", "codec_uw": "decode",
+    "codec_decode": "decode",
+    "expert_gate_up": "expert_gate_up", "expert_in_relu": "expert_in_relu", "expert_down": "expert_down",
+    "combine": "combine",
+}
+
+
+def stage_of(name: str):
+    """Stage of a launch's profile name, or None for launches outside the layer step."""
+    for suf in ("_tail", "_reduce"):
+        if name.endswith(suf):
+            name = name[: -len(suf)]
+    return STAGE_OF_KERNEL.get(name)
+
+
 def source_digest(*names: str) -> str:
     h = hashlib.sha256()
     for n in names:

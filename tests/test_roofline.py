@@ -36,3 +36,26 @@ def test_codec_work():
                            4096 * 4096 * 2 + (4096 * 256 + 4096 * 256) * 2 + 4 * 256 * 256)
     # gate: the logits of M + K rows; X and the gate weights read once, the routing written
     assert w["gate"] == (2 * 4096 * 4096 * 10, 4096 * 4096 * 2 + 10 * 4096 * 2 + 8 * 4096 * 2)
+
+
+def test_every_layer_launch_has_a_stage():
+    """Each profile name the library gives a launch (the ProfileScope literals and the GEMM
+    names set in the sources) maps to a stage with algorithmic work, so the per-stage
+    figures of bench.py cover every kernel of the step. Fitting and the generic GEMM name
+    are outside the layer step."""
+    import os
+    import re
+    csrc = os.path.join(os.path.dirname(R.__file__), "csrc")
+    names = set()
+    for f in os.listdir(csrc):
+        text = open(os.path.join(csrc, f)).read()
+        for line in text.splitlines():
+            if "ProfileScope prof(" in line or re.search(r"\.name = ", line):
+                names.update(re.findall(r'"([a-z_0-9]+)"', line))
+    names -= {"gemm"}
+    names = {n for n in names if not n.startswith("fit_")}
+    assert {"codec_encode", "codec_vzt", "expert_gate_up", "gate"} <= names
+    stages = set(R.kernel_work(W.CONFIGS["mixtral"], np.ones(8, np.int64))) | {"expert_in_relu"}
+    for n in sorted(names):
+        assert R.stage_of(n) in stages, n
+        assert R.stage_of(n + "_tail") == R.stage_of(n)
