@@ -719,8 +719,8 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_lds_kernel(GemmArgs a) {
 // phases, so on every SIMD one wave issues MFMAs while the other waits on memory.
 //   group 0, slab s: issue token rows of slab s+1 | read slab s | barrier | MFMA slab s |
 //                    wait own loads | barrier
-//   group 1, slab s: MFMA slab s-1 | barrier | read slab s, then issue weight rows of slab
-//                    s+2 into the slot of slab s-1 | wait loads of slab s+1 | barrier
+//   group 1, slab s: MFMA slab s-1 | barrier | issue weight rows of slab s+2 into the slot of
+//                    slab s-1, read slab s | wait loads of slab s+1 | barrier
 // Token rows sit in two 32 KB slots and weight rows in three, so that every slot is refilled
 // only after a barrier that follows the last read of it by any wave (with two combined
 // stages the weight rows of slab s+2 had to go into the stage of slab s, which the other
@@ -904,14 +904,15 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
                 if (s >= nk) return;
                 if (s > 0) mma_slab();
                 barrier();
+                // the refill goes out before this group's fragment reads: a longer lead for the
+                // weight rows, which come from HBM (gate-up 1589 -> 1567 us, down 773 -> 760 us
+                // on the Mixtral-shaped layer; issuing it before the barrier instead, at the end of
+                // the products, delays the barrier: 1658 and 822 us)
+                if (s + 2 < nk) issue_slab(s + 2, wfree);
                 read_slab(tcur, wcur);
                 __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-                if (s + 2 < nk) {
-                    issue_slab(s + 2, wfree);
-                    __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));  // weight rows of slab s+1 landed
-                } else {
-                    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-                }
+                if (s + 2 < nk) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));  // weight rows of slab s+1 landed
+                else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
                 barrier();
             };
             for (int s = 0; s < nk; s += 6) {
