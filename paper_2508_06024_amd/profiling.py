@@ -5,6 +5,8 @@
         --kernel <substring> --copy-mib N --workload NAME --command "<cmd>" [-o out.json]
     python -m paper_2508_06024_amd.profiling counters --mfma <csv> --fetch <csv> --write <csv>
         --copy-mib N --command "<cmd>" [-o out.md]
+    python -m paper_2508_06024_amd.profiling dense [--tokens T --d-model d --hidden H --reps R]
+        (GPU: the expert GEMMs on one dense expert beside torch.matmul on the same products)
 
 HBM bytes of a kernel come from FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
 scaled by the ratio of the known bytes of a plain elementwise pass over N MiB (the
@@ -187,6 +189,78 @@ def counters_summary(mfma_csv: str, fetch_csv: str, write_csv: str, copy_mib: in
     return "\n".join(lines) + "\n"
 
 
+def dense_compare(T: int, d: int, H: int, reps: int, only: str = "", calibrate_copy_mib: int = 0) -> str:
+    """The library's expert GEMMs on a single expert that takes every token (a dense SwiGLU
+    FFN: gate-up T x 2H x d, down T x d x H) beside torch.matmul (the ROCm BLAS library) on
+    the same two products, inputs N(0, 1) tokens and N(0, 0.02) weights in bfloat16, each
+    timed with HIP events over `reps` calls after a warm-up. torch's gate-up writes all 2H
+    columns; the library's writes the H SwiGLU outputs. `only` restricts the torch products to
+    one of them (for counter runs, where both use the same library kernel); a calibration
+    copy of N MiB, if asked for, ends the run (the counter scale, as in bench.py)."""
+    import torch
+
+    from . import ec2moe as E
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev).manual_seed(0)
+    bf = torch.bfloat16
+    x = torch.randn(T, d, device=dev, generator=g).to(bf)
+    w_gu = (torch.randn(1, 2 * H, d, device=dev, generator=g) * 0.02).to(bf)
+    w_dn = (torch.randn(1, d, H, device=dev, generator=g) * 0.02).to(bf)
+    seg = torch.tensor([0, T], dtype=torch.int32, device=dev)
+    src = torch.arange(T, dtype=torch.int32, device=dev)
+    ws = E.workspace(E.moe_workspace_size(E.moe_desc(T, 1, 1, d, H, 1, bf)), dev)
+    for _ in range(2):
+        E.expert_ffn(x, seg, src, w_gu, w_dn, 1, ws=ws)
+    torch.cuda.synchronize()
+    E.profile_select(None)
+    E.profile_enable(True)
+    for _ in range(reps):
+        E.expert_ffn(x, seg, src, w_gu, w_dn, 1, ws=ws)
+    torch.cuda.synchronize()
+    st = E.profile_collect()
+    E.profile_enable(False)
+    # per call: the launch and its split-K reduction, if the tile count left a partial round
+    lib = {k: sum(st[n][1] for n in (k, k + "_tail") if n in st) / reps * 1e3 for k in ("expert_gate_up", "expert_down")}
+
+    a = torch.randn(T, H, device=dev, generator=g).to(bf)
+    wgt, wdt = w_gu[0].t(), w_dn[0].t()
+    blas = {}
+    for name, (lhs, rhs) in (("expert_gate_up", (x, wgt)), ("expert_down", (a, wdt))):
+        if only and name != "expert_" + only:
+            blas[name] = float("nan")
+            continue
+        for _ in range(2):
+            torch.matmul(lhs, rhs)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch.matmul(lhs, rhs)
+        e1.record()
+        torch.cuda.synchronize()
+        blas[name] = e0.elapsed_time(e1) / reps * 1e3
+    if calibrate_copy_mib:
+        n = calibrate_copy_mib * (1 << 20) // 4
+        c0 = torch.ones(n, dtype=torch.float32, device=dev)
+        c1 = torch.empty_like(c0)
+        torch.cuda.synchronize()
+        torch.mul(c0, 1.0, out=c1)  # one elementwise kernel: reads and writes N MiB
+        torch.cuda.synchronize()
+        del c0, c1
+    flops = {"expert_gate_up": 4.0 * T * d * H, "expert_down": 2.0 * T * d * H}
+    lib_name = str(torch.backends.cuda.preferred_blas_library()).split(".")[-1]
+    out = [f"dense SwiGLU expert, T = {T}, d = {d}, H = {H}, bf16, {reps} calls each "
+           f"(torch {torch.__version__}, BLAS backend {lib_name})", "",
+           "| product | shape (M x N x K) | library us | library PFLOP/s | torch.matmul us | torch PFLOP/s | ratio |",
+           "|---|---|---|---|---|---|---|"]
+    shapes = {"expert_gate_up": f"{T} x {2 * H} x {d}", "expert_down": f"{T} x {d} x {H}"}
+    for k in ("expert_gate_up", "expert_down"):
+        lu, bu = lib.get(k, float("nan")), blas[k]
+        out.append(f"| {k} | {shapes[k]} | {lu:.1f} | {flops[k] / lu / 1e9:.3f} | {bu:.1f} | "
+                   f"{flops[k] / bu / 1e9:.3f} | {bu / lu:.3f} |")
+    return "\n".join(out) + "\n"
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -213,8 +287,18 @@ def main(argv=None):
     t.add_argument("--workload", required=True)
     t.add_argument("--command", required=True)
     t.add_argument("-o", "--out")
+    g = sub.add_parser("dense")
+    g.add_argument("--tokens", type=int, default=8192)
+    g.add_argument("--d-model", type=int, default=4096)
+    g.add_argument("--hidden", type=int, default=14336)
+    g.add_argument("--reps", type=int, default=20)
+    g.add_argument("--only", choices=["gate_up", "down"], default="")
+    g.add_argument("--calibrate-copy-mib", type=int, default=0)
+    g.add_argument("-o", "--out")
     a = ap.parse_args(argv)
-    if a.cmd == "counters":
+    if a.cmd == "dense":
+        text = dense_compare(a.tokens, a.d_model, a.hidden, a.reps, a.only, a.calibrate_copy_mib)
+    elif a.cmd == "counters":
         text = counters_summary(a.mfma, a.fetch, a.write, a.copy_mib, a.command)
     elif a.cmd == "stats":
         text = stats_summary(a.csv, a.command)
