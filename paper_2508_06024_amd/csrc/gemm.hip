@@ -462,6 +462,43 @@ __device__ __forceinline__ void write_tile32(const GemmArgs& a, const TileInfo& 
     }
 }
 
+// Writes a wave's 16x16-block accumulators. After v_mfma_f32_16x16x32 with weight rows as A
+// and token rows as B, lane l holds token row (l % 16) of the block and, in register r,
+// weight row 4*(l/16) + r: a run of 4 consecutive output columns.
+template <typename TO, int TM, int TN, int WM, int WN, int MI, int NI, bool SWIGLU>
+__device__ __forceinline__ void write_tile16(const GemmArgs& a, const TileInfo& ti, int wm, int wn, int lane,
+                                             const f32x4 (&acc)[NI][MI]) {
+    const int l16 = lane & 15;
+    const int lg = lane >> 4;
+    TO* out = static_cast<TO*>(a.out);
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+        const int trow = wm * (TM / WM) + mi * 16 + l16;
+        if (trow >= ti.valid) continue;
+        TO* orow = out + (ti.row0 + trow) * a.ldo;
+        if (SWIGLU) {
+            constexpr int HALF = NI / 2;
+#pragma unroll
+            for (int ni = 0; ni < HALF; ++ni) {
+                const int col = ti.nt * (TN / 2) + wn * (TN / 2 / WN) + ni * 16 + 4 * lg;
+                f32x4 v;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v[i] = silu(acc[ni][mi][i]) * acc[ni + HALF][mi][i];
+                if (col < a.N) store4<TO>(orow + col, v);
+            }
+        } else {
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+                const int col = ti.nt * TN + wn * (TN / WN) + ni * 16 + 4 * lg;
+                f32x4 v;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v[i] = store_act(a, acc[ni][mi][i]);
+                if (col < a.N) store4<TO>(orow + col, v);
+            }
+        }
+    }
+}
+
 // Workgroups of the large-tile kernel resident at once on the chip: 256 CUs, and as many
 // workgroups per CU as its LDS stages allow (one 256x256 tile, two 128x128 tiles).
 constexpr int kCUs = 256;
@@ -470,7 +507,8 @@ __host__ __device__ constexpr int gemm_slots() {
     return kCUs * ((160 * 1024) / (2 * (TM + TN) * 128));
 }
 
-// bf16 mainloop on 32x32x16 matrix-core blocks (the full-rate bf16 MFMA shape on gfx950).
+// bf16 mainloop on 32x32x16 matrix-core blocks (a full-rate bf16 MFMA shape on gfx950; the
+// 256x256 ping-pong kernel below uses 16x16x32, which holds a higher clock under load).
 //
 // K advances in slabs of 64 (one 128-byte row per tile row) through two LDS stages; the
 // buffer loads of slab ks + 1 fly while slab ks is consumed. Each stage is its own LDS
@@ -714,9 +752,9 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_lds_kernel(GemmArgs a) {
 
 // 8-wave ping-pong mainloop for the 256x256 tile. Waves 0-3 (group 0, token loaders) and
 // waves 4-7 (group 1, weight loaders) sit one per SIMD each; the groups alternate between a
-// compute phase (all 32 MFMAs of one slab from registers, at raised priority) and a memory
-// phase (fragment reads of the next slab, buffer loads), with a workgroup barrier between
-// phases, so on every SIMD one wave issues MFMAs while the other waits on memory.
+// compute phase (the 64 products of one slab, at raised priority) and a memory phase
+// (fragment reads of the next slab, buffer loads), with a workgroup barrier between phases,
+// so on every SIMD one wave issues MFMAs while the other waits on memory.
 //   group 0, slab s: issue token rows of slab s+1 | read slab s | barrier | MFMA slab s |
 //                    wait own loads | barrier
 //   group 1, slab s: MFMA slab s-1 | barrier | issue weight rows of slab s+2 into the slot of
@@ -725,11 +763,20 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_lds_kernel(GemmArgs a) {
 // only after a barrier that follows the last read of it by any wave (with two combined
 // stages the weight rows of slab s+2 had to go into the stage of slab s, which the other
 // group could still be reading).
+// The products are v_mfma_f32_16x16x32_bf16: on random bf16 operands the chip sustains
+// 1.92 PFLOP/s with them against 1.72 with 32x32x16 (the same flops through a quarter of
+// the accumulator traffic per instruction), so the power-bound clock stays higher. A wave
+// holds 4 x 8 blocks of 16 x 16 (128 accumulators); the memory phase reads both k-steps'
+// token fragments and k-step 0's weight fragments, and k-step 1's weight fragments are read
+// during the products of k-step 0 (into the registers of the block just consumed). Those
+// late reads stay behind the same barriers: a group's products of slab s read the weight
+// slot of slab s before the barrier after which slab s+3 refills it, and after the last
+// slab every path waits at a barrier before any slot is written again.
 template <bool SWIGLU, typename TO>
 __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
     constexpr int TM = 256, TN = 256, WM = 4, WN = 2, NW = 8;
-    constexpr int MI = TM / WM / 32;           // 2
-    constexpr int NI = TN / WN / 32;           // 4
+    constexpr int MI = TM / WM / 16;           // 4 token blocks of 16 per wave
+    constexpr int NI = TN / WN / 16;           // 8 weight blocks of 16 per wave
     constexpr int NOUT = SWIGLU ? TN / 2 : TN;
     constexpr int ROWS = TM + TN;
     constexpr int RB = 128;
@@ -808,55 +855,74 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
         }
     };
 
-    const int l32 = lane & 31;
-    const int lh = lane >> 5;
-    const int sw = (l32 >> 1) & 7;
+    // 16x16x32 blocks: lane l feeds row l % 16 of a block with the 8 k of logical chunk
+    // 4 s + l / 16 of k-step s (two k-steps of 32 per slab); blocks start at multiples of 16
+    // rows, so the swizzle depends on the lane only
+    const int l16 = lane & 15;
+    const int lg = lane >> 4;
+    const int sw = (l16 >> 1) & 7;
     constexpr int WTOK = TM / WM;
     constexpr int WW = SWIGLU ? TN / 2 / WN : TN / WN;
-    int off_t[4], off_w[4];
+    int off_t[2], off_w[2];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        const int ch = ((2 * s + lh) ^ sw) * 16;
-        off_t[s] = (wm * WTOK + l32) * RB + ch;  // in a token slot
-        off_w[s] = (wn * WW + l32) * RB + ch;    // in a weight slot (same swizzle: row offsets of 32)
+    for (int s = 0; s < 2; ++s) {
+        const int ch = ((4 * s + lg) ^ sw) * 16;
+        off_t[s] = (wm * WTOK + l16) * RB + ch;  // in a token slot
+        off_w[s] = (wn * WW + l16) * RB + ch;    // in a weight slot
     }
     auto wblk = [](int ni) constexpr {
         if (SWIGLU) {
             constexpr int HALF = NI / 2;
-            return (ni < HALF ? 0 : TN / 2) + (ni % HALF) * 32;
+            return (ni < HALF ? 0 : TN / 2) + (ni % HALF) * 16;
         }
-        return ni * 32;
+        return ni * 16;
     };
 
-    f32x16 acc[NI][MI];
+    f32x4 acc[NI][MI];
 #pragma unroll
     for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[ni][mi][r] = 0.f;
+            for (int r = 0; r < 4; ++r) acc[ni][mi][r] = 0.f;
 
-    uint4 fa[4][NI], fb[4][MI];  // one slab of fragments
+    // one slab of fragments: both k-steps of the token rows, one k-step of the weight rows
+    // at a time (k-step 1's are read by mma_slab_w)
+    uint4 fa[NI], fb[2][MI];
     auto read_slab = [&](const char* tslot, const char* wslot) {
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
+        for (int ni = 0; ni < NI; ++ni) fa[ni] = *reinterpret_cast<const uint4*>(wslot + off_w[0] + wblk(ni) * RB);
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) fa[s][ni] = *reinterpret_cast<const uint4*>(wslot + off_w[s] + wblk(ni) * RB);
+        for (int s = 0; s < 2; ++s)
 #pragma unroll
-            for (int mi = 0; mi < MI; ++mi) fb[s][mi] = *reinterpret_cast<const uint4*>(tslot + off_t[s] + mi * 32 * RB);
-        }
+            for (int mi = 0; mi < MI; ++mi) fb[s][mi] = *reinterpret_cast<const uint4*>(tslot + off_t[s] + mi * 16 * RB);
     };
-    auto mma_slab = [&]() {
+    auto mma_slab_w = [&](const char* wslot) {
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
+        for (int ni = 0; ni < NI; ++ni) {
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni)
+            for (int mi = 0; mi < MI; ++mi)
+                acc[ni][mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fa[ni]),
+                                                                     __builtin_bit_cast(bf16x8, fb[0][mi]),
+                                                                     acc[ni][mi], 0, 0, 0);
+            fa[ni] = *reinterpret_cast<const uint4*>(wslot + off_w[1] + wblk(ni) * RB);
+        }
 #pragma unroll
-                for (int mi = 0; mi < MI; ++mi)
-                    acc[ni][mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[s][ni]),
-                                                                         __builtin_bit_cast(bf16x8, fb[s][mi]),
-                                                                         acc[ni][mi], 0, 0, 0);
+        for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+                acc[ni][mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fa[ni]),
+                                                                     __builtin_bit_cast(bf16x8, fb[1][mi]),
+                                                                     acc[ni][mi], 0, 0, 0);
+        // k-step 0 with a read after every block's products, then k-step 1: each read has the
+        // rest of k-step 0 (28 products or more) to land
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) {
+            __builtin_amdgcn_sched_group_barrier(0x008, MI, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NI * MI, 0);
         __builtin_amdgcn_s_setprio(0);
     };
     auto barrier = [&]() {
@@ -884,7 +950,7 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
                 read_slab(tcur, wcur);
                 __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
                 barrier();
-                mma_slab();
+                mma_slab_w(wcur);
                 __builtin_amdgcn_sched_barrier(0);
                 __builtin_amdgcn_s_waitcnt(0x0070);  // token rows of slab s+1 landed
                 barrier();
@@ -902,7 +968,7 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
             // done before the previous barrier: no wave can still be reading it.
             auto slab1 = [&](const char* tcur, const char* wcur, char* wfree, int s) {
                 if (s >= nk) return;
-                if (s > 0) mma_slab();
+                if (s > 0) mma_slab_w(wfree);  // slab s - 1, whose weights sit in the slot refilled next
                 barrier();
                 // the refill goes out before this group's fragment reads: a longer lead for the
                 // weight rows, which come from HBM (gate-up 1589 -> 1567 us, down 773 -> 760 us
@@ -923,31 +989,30 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
                 slab1(t0, w1, w0, s + 4);
                 slab1(t1, w2, w1, s + 5);
             }
-            mma_slab();
+            const int last = (nk - 1) % 3;
+            mma_slab_w(last == 0 ? w0 : last == 1 ? w1 : w2);
         }
     }
 
     if (split) {
+        // raw float32 partial tile [TM][TN] (weight rows in tile order) of this K chunk; lane l
+        // holds, per block, weight rows 4 (l / 16) .. + 3 of token row l % 16
         float* part = a.part + static_cast<int64_t>(p) * TM * TN;
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
-            const int trow = wm * WTOK + mi * 32 + l32;
+            const int trow = wm * WTOK + mi * 16 + l16;
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) {
-                const int wrow = wn * WW + wblk(ni);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    f32x4 v;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) v[i] = acc[ni][mi][4 * q + i];
-                    *reinterpret_cast<f32x4*>(part + trow * TN + wrow + 8 * q + 4 * lh) = v;
-                }
+                const int wrow = wn * WW + wblk(ni) + 4 * lg;
+                *reinterpret_cast<f32x4*>(part + trow * TN + wrow) = acc[ni][mi];
             }
         }
+        barrier();  // the weight loaders' last products read their slot: no refill before this
         continue;
     }
     if constexpr (sizeof(TO) == 4) {
-        write_tile32<TO, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+        write_tile16<TO, TM, TN, WM, WN, MI, NI, SWIGLU>(a, ti, wm, wn, lane, acc);
+        barrier();  // the weight loaders' last products read their slot: no refill before this
     } else {
         // The finished tile is staged in LDS as bf16 rows (every slot is free after the last
         // slab) so that the global stores are whole rows: 16 bytes per lane, 128-byte lines.
@@ -959,27 +1024,27 @@ __global__ __launch_bounds__(512, 1) void gemm_pp_kernel(GemmArgs a) {
         auto ost = [&](int i) -> char* { return i == 0 ? t0 : i == 1 ? t1 : i == 2 ? w0 : w1; };
         // this wave's rows wm * 64 .. wm * 64 + 63 lie in one slot
         char* wst = ost(wm * WTOK / RPS) + (wm * WTOK % RPS) * OROW;
+        // without SwiGLU the staged rows also fill two weight slots, one of which the weight
+        // loaders' last products may still be reading
+        if constexpr (!SWIGLU) barrier();
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
-            const int r = mi * 32 + l32;  // row within this wave's 64
+            const int r = mi * 16 + l16;  // row within this wave's 64
             const int sr = wm * WTOK + r;  // row within the tile (swizzle key)
             constexpr int NB = SWIGLU ? NI / 2 : NI;
 #pragma unroll
             for (int ni = 0; ni < NB; ++ni) {
+                float v[4];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    float v[4];
+                for (int e = 0; e < 4; ++e)
+                    v[e] = SWIGLU ? silu(acc[ni][mi][e]) * acc[ni + NB][mi][e] : store_act(a, acc[ni][mi][e]);
+                bf16x4 o;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        v[e] = SWIGLU ? silu(acc[ni][mi][4 * q + e]) * acc[ni + NB][mi][4 * q + e]
-                                       : store_act(a, acc[ni][mi][4 * q + e]);
-                    bf16x4 o;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(v[e]);
-                    const int col = wn * (NOUT / WN) + ni * 32 + 8 * q;  // first column of the 8-column chunk
-                    const int ch = (col / 8) ^ (sr % OCH);
-                    *reinterpret_cast<bf16x4*>(wst + r * OROW + ch * 16 + lh * 8) = o;
-                }
+                for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(v[e]);
+                // columns 4 lg .. + 3 of the block: half lg % 2 of 8-column chunk lg / 2
+                const int col = wn * (NOUT / WN) + ni * 16 + 8 * (lg >> 1);
+                const int ch = (col / 8) ^ (sr % OCH);
+                *reinterpret_cast<bf16x4*>(wst + r * OROW + ch * 16 + (lg & 1) * 8) = o;
             }
         }
         __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)

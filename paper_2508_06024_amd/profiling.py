@@ -121,7 +121,7 @@ def counters_summary(mfma_csv: str, fetch_csv: str, write_csv: str, copy_mib: in
     and HBM bytes (FETCH_SIZE, WRITE_SIZE scaled by the copy calibration), averaged over its
     dispatches. GRBM_GUI_ACTIVE sums the active cycles of every XCD, so the kernel's clock is
     GUI / xcds / duration and its SIMD-cycles GUI / xcds * simds; a 32x32x16 bf16 MFMA keeps a
-    SIMD's matrix core busy for 32 of them."""
+    SIMD's matrix core busy for 32 of them, a 16x16x32 one for 16."""
     m = _per_dispatch(mfma_csv)
     f = _per_dispatch(fetch_csv)
     w = _per_dispatch(write_csv)
