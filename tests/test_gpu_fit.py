@@ -60,6 +60,27 @@ def test_fit_matches_oracle_iteration(c, h, w, rh, rw, dt, iters, tol):
         say(f"  {name}: projector error {e:.2e}, orthonormality {o:.2e}")
 
 
+def test_fit_full_size_matches_oracle_iteration():
+    """A 4096 x 4096 calibration block at rank 256, one iteration: its Gram products are large
+    enough for the 256 x 256 matrix-core tile with float32 output (the only path that uses that
+    tile's float32 writer). Projectors against the oracle's iteration on the same bf16 block."""
+    h = w = 4096
+    r = 256
+    rng = np.random.default_rng(21)
+    x = (rng.standard_normal((h, w)) * np.linspace(3.0, 0.1, w)).astype(np.float32)[None]
+    stored = W.f32_to_bf16_bits(x)
+    x64 = W.to_f64(stored, W.BF16)
+    ou, ov = _omega(h, r, 8), _omega(w, r, 9)
+    u, v, status = E.lowrank_fit(up(stored, W.BF16), up_f32(ou), up_f32(ov), 1)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    ru, rv = O.codec_fit_subspace(x64, ou.astype(np.float64), ov.astype(np.float64), 1)
+    for g, ref, name in ((down(u), ru, "U"), (down(v), rv, "V")):
+        e = np.max(np.abs(_proj(g) - _proj(ref)))
+        say(f"  4096 x 4096, r = 256: {name} projector error {e:.2e}")
+        assert e <= 2e-2, f"{name} projector error {e:.2e}"
+
+
 def test_fit_one_slice_reaches_eckart_young():
     """Enough iterations for the gap: the fitted codec's error is the tail of the spectrum."""
     h, w, r = 512, 384, 32
