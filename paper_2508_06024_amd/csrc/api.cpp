@@ -203,7 +203,7 @@ CodecWs codec_ws(const ec2moe_codec_desc* d) {
     size_t o = 0;
     w.gpart = o; o += up(gemm_split_scratch_bytes());
     const size_t shared = o;
-    w.vt = o; o += up(static_cast<size_t>(d->r_w) * d->w * eb);
+    w.vt = o; o += w.fused ? 0 : up(static_cast<size_t>(d->r_w) * d->w * eb);  // the fused encoder reads V as stored
     w.p = o; o += w.fused || w.small ? 0 : up(nb * d->h * d->r_w * 4);
     w.epart = o;
     o += w.small ? up(codec_small_part_floats(d->h, d->w, d->r_w, static_cast<int>(nb)) * 4)
@@ -543,12 +543,12 @@ ec2moe_status ec2moe_lowrank_encode(const ec2moe_codec_desc* desc, const void* x
     }
     void* vt = at<void>(ws, w.vt);
     float* p = at<float>(ws, w.p);
-    hipError_t e = launch_transpose(dt, v, desc->w, desc->r_w, vt, stream);
+    hipError_t e = w.fused ? hipSuccess : launch_transpose(dt, v, desc->w, desc->r_w, vt, stream);
     for (int c0 = 0; c0 < desc->n_slices && e == hipSuccess; c0 += w.batch) {
         const int nc = std::min(w.batch, desc->n_slices - c0);
         if (w.fused) {
             EncArgs a{};
-            a.x = static_cast<const char*>(x) + c0 * slice_bytes; a.vt = vt; a.u = u; a.part = at<float>(ws, w.epart);
+            a.x = static_cast<const char*>(x) + c0 * slice_bytes; a.v = v; a.u = u; a.part = at<float>(ws, w.epart);
             a.h = desc->h; a.w = desc->w; a.rh = desc->r_h; a.rw = desc->r_w; a.slices = nc;
             e = launch_encode_fused(a, z + static_cast<size_t>(c0) * desc->r_h * desc->r_w, stream);
             continue;

@@ -327,10 +327,12 @@ __global__ __launch_bounds__(256) void utp3_kernel(UtpArgs g) {
 // One workgroup per (64-token tile, 64-column tile) of P = X V: the tile's products over the
 // whole model width (no split along it), then at once its share of Z = U^T P,
 //   part[s][tt][r][c] = sum over the tile's 64 tokens t of U[t][r] P[t][c],
-// which split_reduce_kernel adds over the token tiles in order. X and V^T ([r_w][w], K-contiguous)
-// stream through a ring of four LDS stages of 128 model columns (32 KB: 64 token rows and 64
-// V^T rows of 256 bytes) filled by buffer_load ... lds, so three stages are in flight while
-// one is consumed. Eight waves: wave w computes the 32x32 block (w & 1, (w >> 1) & 1) of the
+// which split_reduce_kernel adds over the token tiles in order. X and V (as stored, [w][r_w])
+// stream through a ring of four LDS stages of 128 model columns (32 KB: 64 token rows of 256
+// bytes, and the 128 rows of V for those model columns, 128 bytes each: the tile's 64 columns)
+// filled by buffer_load ... lds, so three stages are in flight while one is consumed. V's
+// operand fragments need 8 consecutive model columns per lane, which run down the staged
+// rows: the gfx950 transposing LDS read (ds_read_b64_tr_b16) gathers them, 4 rows at a time. Eight waves: wave w computes the 32x32 block (w & 1, (w >> 1) & 1) of the
 // P tile over the even (w < 4) or odd (w >= 4) 16-column steps of each stage; the two halves
 // are added once at the end. The P tile is then split exactly into three bf16 planes
 // (hi + mid + lo) and, with U^T, staged in LDS for the bf16 matrix cores, as in utp3_kernel.
@@ -363,6 +365,15 @@ constexpr int kEncRow = kEncK * 2;                   // bytes per staged row
 constexpr int kEncStage = (kEncT + kEncC) * kEncRow;  // 32 KB
 constexpr int kEncLoads = 4;                         // DMA instructions per wave per stage
 
+// gfx950 transposing LDS read of 16-bit data: in each group of 16 lanes, lane i reads the 8 bytes
+// at its address (elements S[i][0..3]) and receives S[4 e + i / 4][i % 4] in element e
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 lds_read_tr16(const char* p) {
+    const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) i16x4*)(const_cast<char*>(p)));
+    return __builtin_bit_cast(uint2, v);
+}
+
 __global__ __launch_bounds__(512, 1) void encode_fused_kernel(EncArgs a) {
     // one LDS object per ring slot, each named at compile time where it is read, so the wait
     // before a fragment read only covers the DMA into that slot
@@ -370,6 +381,7 @@ __global__ __launch_bounds__(512, 1) void encode_fused_kernel(EncArgs a) {
     __shared__ __attribute__((aligned(1024))) char lds1[kEncStage];
     __shared__ __attribute__((aligned(1024))) char lds2[kEncStage];
     __shared__ __attribute__((aligned(1024))) char lds3[kEncStage];
+    static_assert(kEncT * kEncRow == kEncK * kEncC * 2, "token rows and V rows fill equal halves of a stage");
     const int ct_n = a.rw / kEncC, tt_n = a.h / kEncT;
     const int n = ct_n * tt_n * a.slices;
     const int g = blockIdx.x;
@@ -405,37 +417,55 @@ __global__ __launch_bounds__(512, 1) void encode_fused_kernel(EncArgs a) {
                                            : make_uint4(0, 0, 0, 0);
     }
 
-    // DMA: wave w fills staged rows 16 w .. 16 w + 15 (rows 0..63: the tile's tokens, 64..127: its
-    // V^T rows), four rows of 256 bytes per instruction; chunk c of staged row R sits at
-    // c ^ (R % 16), the swizzle applied on the global side
+    // DMA, 1 KB per instruction: waves 0..3 fill token rows 16 w .. 16 w + 15 of the stage's first
+    // half (four rows of 256 bytes per instruction; chunk c of row R sits at c ^ (R % 16)), waves
+    // 4..7 V rows 32 (w - 4) .. + 31 of its second half (eight rows of 128 bytes per instruction;
+    // chunk c of V row k sits at c ^ 2 (k % 4)); both swizzles are applied on the global side
     const bool tok_wave = wave < 4;
+    const uint32_t vrow_bytes = static_cast<uint32_t>(a.rw) * 2u;
     const i32x4 rs = tok_wave
         ? enc_rsrc(static_cast<const bf16_t*>(a.x) + (static_cast<int64_t>(s) * a.h + static_cast<int64_t>(tt) * kEncT) * a.w,
                    kEncT * row_bytes)
-        : enc_rsrc(static_cast<const bf16_t*>(a.vt) + static_cast<int64_t>(ct) * kEncC * a.w, kEncC * row_bytes);
+        : enc_rsrc(a.v, static_cast<uint32_t>(a.w) * vrow_bytes);
+    const int sstep = tok_wave ? kEncRow : kEncK * static_cast<int>(vrow_bytes);  // bytes per stage
     uint32_t voff[kEncLoads];
 #pragma unroll
     for (int j = 0; j < kEncLoads; ++j) {
-        const int row = 16 * (wave & 3) + 4 * j + (lane >> 4);  // row within its operand
-        voff[j] = static_cast<uint32_t>(row) * row_bytes + static_cast<uint32_t>(((lane & 15) ^ (row & 15)) * 16);
+        if (tok_wave) {
+            const int row = 16 * wave + 4 * j + (lane >> 4);
+            voff[j] = static_cast<uint32_t>(row) * row_bytes + static_cast<uint32_t>(((lane & 15) ^ (row & 15)) * 16);
+        } else {
+            const int k = 32 * (wave - 4) + 8 * j + (lane >> 3);
+            voff[j] = static_cast<uint32_t>(k) * vrow_bytes + static_cast<uint32_t>(ct * kEncC * 2) +
+                      static_cast<uint32_t>(((lane & 7) ^ (2 * (k & 3))) * 16);
+        }
     }
     auto issue = [&](int st, char* slot) {
         char* base = slot + 16 * wave * kEncRow;
 #pragma unroll
         for (int j = 0; j < kEncLoads; ++j)
             raw_buffer_load_lds(rs, reinterpret_cast<lds_void*>(reinterpret_cast<uintptr_t>(base + 4 * j * kEncRow)), 16,
-                                static_cast<int>(voff[j]), st * kEncRow, 0, 0);
+                                static_cast<int>(voff[j]), st * sstep, 0, 0);
     };
 
-    // fragments: A = V^T row 64 + 32 wn + l32 (a column of P), B = token row 32 wm + l32, each
-    // lane the 16 bytes of logical chunk 2 q + lh of k-step q
+    // fragments: A = column 32 wn + l32 of P (V's column ct * 64 + 32 wn + l32), model columns
+    // 16 (2 q + kh) + 8 lh .. + 7 of the stage in k-step q; B = token row 32 wm + l32, the 16
+    // bytes of logical chunk 2 (2 q + kh) + lh. A transposing read by the 16 lanes of a group
+    // (g = lane / 16, i = lane % 16) takes 8 bytes from V row k0 + i / 4 at columns
+    // mb + 4 (i % 4) .. + 3 and hands lane i the 4 rows k0 .. k0 + 3 of column mb + i; here
+    // k0 = 16 (2 q + kh) + 8 (g / 2) + 4 h for the halves h = 0, 1 of the lane's 8 model columns
+    // and mb = 32 wn + 16 (g % 2), so lane l gets column 32 wn + l % 32 as the product needs
     const int wm = wave & 1, wn = (wave >> 1) & 1, kh = wave >> 2;
-    const int ra = kEncT + 32 * wn + l32, rb = 32 * wm + l32;
-    int offa[4], offb[4];
+    const int rb = 32 * wm + l32;
+    const int gi = lane & 15, gg = lane >> 4;
+    const int chv = 4 * wn + 2 * (gg & 1) + ((gi & 3) >> 1);  // 16-byte chunk of the V row
+    const int offv = kEncT * kEncRow + ((chv ^ (2 * (gi >> 2))) * 16) + (gi & 1) * 8;
+    int offa[4][2], offb[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int ch = 2 * (2 * q + kh) + lh;
-        offa[q] = ra * kEncRow + ((ch ^ (ra & 15)) * 16);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) offa[q][h] = offv + (16 * (2 * q + kh) + 8 * (gg >> 1) + 4 * h + (gi >> 2)) * 128;
         offb[q] = rb * kEncRow + ((ch ^ (rb & 15)) * 16);
     }
     f32x16 acc;
@@ -459,7 +489,8 @@ __global__ __launch_bounds__(512, 1) void encode_fused_kernel(EncArgs a) {
         uint4 fa[4], fb[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            fa[q] = *reinterpret_cast<const uint4*>(cur + offa[q]);
+            const uint2 lo = lds_read_tr16(cur + offa[q][0]), hi = lds_read_tr16(cur + offa[q][1]);
+            fa[q] = make_uint4(lo.x, lo.y, hi.x, hi.y);
             fb[q] = *reinterpret_cast<const uint4*>(cur + offb[q]);
         }
 #pragma unroll

@@ -81,11 +81,11 @@ struct UtpArgs {
 };
 hipError_t launch_utp(DType udt, const UtpArgs& g, hipStream_t s);
 // Fused encoder of bf16 layers: part[s][tt][r][c] = U^T (X V) over 64-token tiles tt (X [slices][h][w],
-// V^T [r_w][w], U [h][r_h]), then z[s] = sum over tt in order. Applies when encode_fused_ok();
+// V [w][r_w], U [h][r_h]), then z[s] = sum over tt in order. Applies when encode_fused_ok();
 // part holds slices * (h / 64) * r_h * r_w floats.
 struct EncArgs {
     const void* x;   // bf16
-    const void* vt;  // bf16
+    const void* v;   // bf16
     const void* u;   // bf16
     float* part;
     int h, w, rh, rw, slices;
