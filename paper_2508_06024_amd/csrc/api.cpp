@@ -615,7 +615,9 @@ ec2moe_status ec2moe_lowrank_decode(const ec2moe_codec_desc* desc, const float* 
                 e = launch_gemm(dt, Epilogue::Store, OutType::Same, gw, stream);
             }
         }
-        if (e == hipSuccess) {
+        if (e == hipSuccess && expand_ok(dt, desc->h, desc->w, desc->r_h)) {
+            e = launch_expand(u_hat, wt, desc->h, desc->w, desc->r_h, x_hat, stream);
+        } else if (e == hipSuccess) {
             // X_hat = U_hat Wt^T  [h][w]
             GemmArgs g{};
             g.tok = u_hat; g.row_index = nullptr; g.w = wt; g.w_group_stride = 0; g.seg = nullptr; g.n_groups = 1;

@@ -739,6 +739,161 @@ __global__ __launch_bounds__(256) void dec_small_kernel(const float* __restrict_
     }
 }
 
+// ------------------------------------------------------------------ decoder, X_hat = U_hat Wt^T (bf16)
+//
+// X_hat[t][j] = sum_i U_hat[t][i] Wt[j][i] over K = r_h (128 or 256), rounded to bfloat16: a
+// rank-r_h expansion whose cost is its 2-byte output. A workgroup owns a band of 128 tokens and a
+// run of 64-column chunks of X_hat. Each of its four waves holds the U_hat operand fragments of its
+// 32 tokens in registers for the whole run; the chunks' Wt rows (64 x r_h, K-contiguous) stream
+// through two LDS buffers by buffer_load ... lds. A chunk's results wait in registers (packed to
+// bf16) and are stored after the next chunk's loads have landed, so the stores drain during that
+// chunk's products instead of under the wait for its loads (the wait is vmcnt(0): loads and stores
+// are not counted in order with each other). Two workgroups per CU overlap each other's waits. Wt is the A operand
+// of v_mfma_f32_16x16x32_bf16 with its rows permuted: operand row m = 4 g + e of block b is
+// column 16 g + 4 b + e of the chunk, so a lane's 16 results of one token are 16 consecutive
+// columns. Each wave passes its 32 x 64 results through 4 KB of LDS so that every store
+// instruction writes 8 whole 128-byte row pieces (16-byte pieces spread over 16 rows per
+// instruction took 60% longer). Staged Wt row R keeps its 16-byte chunk c at c ^ ex_swz(R), which
+// spreads the 16 rows read by one group of lanes over distinct banks; the output staging keeps
+// piece p of row r at p ^ (r % 8).
+constexpr int kExT = 128;  // tokens per band: four waves of 32
+constexpr int kExC = 64;   // columns of X_hat per chunk
+
+__device__ __forceinline__ int ex_swz(int r) { return (r & 3) | (((r >> 4) & 3) << 2); }
+
+template <int RH>
+__global__ __launch_bounds__(256, 2) void expand_kernel(const bf16_t* __restrict__ u_hat, const bf16_t* __restrict__ wt,
+                                                       int w, int cpw, bf16_t* __restrict__ x_hat) {
+    constexpr int ROWB = RH * 2;         // bytes per Wt row
+    constexpr int CHB = kExC * ROWB;     // bytes per chunk
+    constexpr int CPR = ROWB / 16;       // 16-byte pieces per row
+    constexpr int RPI = 1024 / ROWB;     // rows per DMA instruction (1 KB)
+    constexpr int NLD = CHB / 1024 / 4;  // DMA instructions per wave per chunk
+    constexpr int KS = RH / 32;          // k-steps
+    __shared__ __attribute__((aligned(1024))) char buf0[CHB];
+    __shared__ __attribute__((aligned(1024))) char buf1[CHB];
+    __shared__ __attribute__((aligned(1024))) char ostage[4 * 32 * kExC * 2];
+    const int nch = w / kExC;
+    const int nranges = (nch + cpw - 1) / cpw;
+    const int band = blockIdx.x / nranges;
+    const int c0 = (blockIdx.x % nranges) * cpw, c1 = min(c0 + cpw, nch);
+
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, g = lane >> 4;
+
+    // U_hat fragments: token 32 wave + 16 n + l16 of the band, k-run 8 g of step s
+    uint4 fb[2][KS];
+    const bf16_t* urow = u_hat + (static_cast<int64_t>(band) * kExT + 32 * wave + l16) * RH + 8 * g;
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int s = 0; s < KS; ++s) fb[n][s] = ldg16(urow + 16 * n * RH + 32 * s);
+
+    // DMA: instruction j of the wave fills bytes 1024 (NLD wave + j) .. + 1023 of a buffer, i.e.
+    // row R = RPI (NLD wave + j) + lane / CPR, position lane % CPR
+    const i32x4 rs = enc_rsrc(wt, static_cast<uint32_t>(w) * ROWB);
+    uint32_t voff[NLD];
+#pragma unroll
+    for (int j = 0; j < NLD; ++j) {
+        const int R = RPI * (NLD * wave + j) + lane / CPR;
+        voff[j] = static_cast<uint32_t>(R * ROWB + (((lane % CPR) ^ ex_swz(R)) * 16));
+    }
+    auto issue = [&](int c, char* buf) {
+        char* base = buf + 1024 * NLD * wave;
+#pragma unroll
+        for (int j = 0; j < NLD; ++j)
+            raw_buffer_load_lds(rs, reinterpret_cast<lds_void*>(reinterpret_cast<uintptr_t>(base + 1024 * j)), 16,
+                                static_cast<int>(voff[j]), c * CHB, 0, 0);
+    };
+    // A fragments: operand row l16 of block b is chunk row 16 (l16 / 4) + 4 b + l16 % 4
+    int rowoff[4], rsw[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+        const int R = 16 * (l16 >> 2) + 4 * b + (l16 & 3);
+        rowoff[b] = R * ROWB;
+        rsw[b] = ex_swz(R);
+    }
+    // output staging of the wave (32 rows of 128 bytes); store q of a lane: row 8 q + lane / 8 of the
+    // wave's tokens, columns 8 (lane % 8) .. + 7 of the chunk
+    char* ost = ostage + wave * (32 * kExC * 2);
+    bf16_t* orow = x_hat + (static_cast<int64_t>(band) * kExT + 32 * wave + (lane >> 3)) * w + 8 * (lane & 7);
+
+    // the previous chunk's results, read back from the staging in store order (named values, not
+    // an array: an array read by the deferred stores was kept in scratch memory)
+    uint4 p0, p1, p2, p3;
+    const int64_t w8 = static_cast<int64_t>(8) * w;
+    auto store_pending = [&](int c) {
+        bf16_t* dst = orow + c * kExC;
+        *reinterpret_cast<uint4*>(dst) = p0;
+        *reinterpret_cast<uint4*>(dst + w8) = p1;
+        *reinterpret_cast<uint4*>(dst + 2 * w8) = p2;
+        *reinterpret_cast<uint4*>(dst + 3 * w8) = p3;
+    };
+    if (c0 < c1) issue(c0, buf0);
+    for (int c = c0; c < c1; ++c) {
+        const bool odd = (c - c0) & 1;
+        const char* cur = odd ? buf1 : buf0;
+        char* nxt = odd ? buf0 : buf1;
+        // this chunk's rows are in LDS (and the stores issued before its products are done);
+        // after the barrier every wave is done reading the other buffer, which is refilled next
+        __builtin_amdgcn_s_waitcnt(0x0070);
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_barrier" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        if (c + 1 < c1) issue(c + 1, nxt);
+        if (c > c0) store_pending(c - 1);
+        f32x4 acc[2][4];
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) acc[n][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            uint4 fa[4];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) fa[b] = *reinterpret_cast<const uint4*>(cur + rowoff[b] + (((4 * s + g) ^ rsw[b]) * 16));
+#pragma unroll
+            for (int n = 0; n < 2; ++n)
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    acc[n][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fa[b]),
+                                                                         __builtin_bit_cast(bf16x8, fb[n][s]), acc[n][b], 0, 0, 0);
+        }
+        // lane: token 16 n + l16 of the wave, columns 16 g + 4 b + e of the chunk, i.e. pieces 2 g and
+        // 2 g + 1 of staged row 16 n + l16; hardware round-to-nearest-even (v_cvt_pk_bf16_f32)
+#pragma unroll
+        for (int n = 0; n < 2; ++n) {
+            bf16x8 o0, o1;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                o0[e] = static_cast<__bf16>(acc[n][0][e]);
+                o0[4 + e] = static_cast<__bf16>(acc[n][1][e]);
+                o1[e] = static_cast<__bf16>(acc[n][2][e]);
+                o1[4 + e] = static_cast<__bf16>(acc[n][3][e]);
+            }
+            const int r = 16 * n + l16;
+            *reinterpret_cast<bf16x8*>(ost + r * 128 + (((2 * g) ^ (r & 7)) * 16)) = o0;
+            *reinterpret_cast<bf16x8*>(ost + r * 128 + (((2 * g + 1) ^ (r & 7)) * 16)) = o1;
+        }
+        // the wave's staging writes are done before its lanes read each other's pieces (the
+        // staging is the wave's own: no other wave touches it)
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+        __builtin_amdgcn_wave_barrier();
+        // row 8 q + lane / 8 has (row % 8) = lane / 8 for every q
+        const int rpos = ((lane & 7) ^ (lane >> 3)) * 16 + (lane >> 3) * 128;
+        p0 = *reinterpret_cast<const uint4*>(ost + rpos);
+        p1 = *reinterpret_cast<const uint4*>(ost + rpos + 8 * 128);
+        p2 = *reinterpret_cast<const uint4*>(ost + rpos + 16 * 128);
+        p3 = *reinterpret_cast<const uint4*>(ost + rpos + 24 * 128);
+        // the reads are done before the next chunk's staging writes
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        __builtin_amdgcn_wave_barrier();
+    }
+    if (c0 < c1) store_pending(c1 - 1);
+}
+
 // ------------------------------------------------------------------ decoder, W = V_hat Z^T (bf16)
 //
 // Wt[s][j][i] = sum_c V_hat[j][c] * bf16(Z[s][i][c]), rounded to bfloat16: the first product of
@@ -1023,6 +1178,25 @@ hipError_t launch_vzt(const float* z, const void* v_hat, int w, int rh, int rw, 
     ProfileScope prof("codec_vzt", s);
     hipLaunchKernelGGL(vzt_kernel, dim3(w / kVztT, (rh + kVztT - 1) / kVztT, slices), dim3(256), 0, s, z,
                        static_cast<const bf16_t*>(v_hat), w, rh, rw, static_cast<bf16_t*>(wt));
+    return hipGetLastError();
+}
+
+bool expand_ok(DType dt, int h, int w, int rh) {
+    return dt == DType::BF16 && h > 0 && h % kExT == 0 && w > 0 && w % kExC == 0 && (rh == 128 || rh == 256);
+}
+
+hipError_t launch_expand(const void* u_hat, const void* wt, int h, int w, int rh, void* x_hat, hipStream_t s) {
+    // about two workgroups per CU: the chunk runs are as short as that allows
+    const int64_t bands = h / kExT, nch = w / kExC;
+    const int cpw = static_cast<int>(std::max<int64_t>(1, (bands * nch + 511) / 512));
+    const int64_t grid = bands * ((nch + cpw - 1) / cpw);
+    ProfileScope prof("codec_uw", s);
+    if (rh == 256)
+        hipLaunchKernelGGL(expand_kernel<256>, dim3(static_cast<unsigned>(grid)), dim3(256), 0, s,
+                           static_cast<const bf16_t*>(u_hat), static_cast<const bf16_t*>(wt), w, cpw, static_cast<bf16_t*>(x_hat));
+    else
+        hipLaunchKernelGGL(expand_kernel<128>, dim3(static_cast<unsigned>(grid)), dim3(256), 0, s,
+                           static_cast<const bf16_t*>(u_hat), static_cast<const bf16_t*>(wt), w, cpw, static_cast<bf16_t*>(x_hat));
     return hipGetLastError();
 }
 

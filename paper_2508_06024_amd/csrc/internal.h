@@ -122,6 +122,10 @@ hipError_t launch_f32_to_bf16(const float* src, int64_t n, void* dst, hipStream_
 // (w a multiple of 64, r_h of 4, r_w of 16 and at most 256); vzt_ok tells whether the shape qualifies.
 bool vzt_ok(DType dt, int w, int rh, int rw);
 hipError_t launch_vzt(const float* z, const void* v_hat, int w, int rh, int rw, int slices, void* wt, hipStream_t s);
+// Decoder product X_hat = U_hat Wt^T [h][w] (bf16, one slice) in one launch: U_hat [h][r_h], Wt [w][r_h],
+// h a multiple of 128, w of 64, r_h 128 or 256; expand_ok tells whether the shape qualifies.
+bool expand_ok(DType dt, int h, int w, int rh);
+hipError_t launch_expand(const void* u_hat, const void* wt, int h, int w, int rh, void* x_hat, hipStream_t s);
 
 
 }  // namespace ec2moe
