@@ -51,6 +51,10 @@ def test_full_rank_codec_round_trips_on_gpu():
     (3, 128, 256, 80, 128, W.BF16),   # r_h inside the second 64-row block, two column tiles
     (2, 256, 384, 256, 192, W.BF16),  # three column tiles of a token tile placed on one XCD
     (17, 128, 128, 16, 64, W.BF16),   # two tiles per slice, more slices than one batch
+    # one slice of whole 128-token bands with r_h = 128 or 256 takes the decoder's expansion kernel:
+    (1, 128, 128, 128, 64, W.BF16),    # one band of two 64-column chunks
+    (1, 256, 512, 256, 128, W.BF16),   # with the fused encoder
+    (1, 4096, 2176, 128, 64, W.BF16),  # runs of three chunks, the last of each band one chunk (34 chunks)
     # at most 64 tokens per slice take the small-batch encoder and decoder:
     (3, 48, 256, 32, 48, W.BF16),
     (2, 64, 256, 64, 256, W.F32),     # the largest r_h and r_w of that path
