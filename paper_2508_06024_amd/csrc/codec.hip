@@ -748,12 +748,12 @@ __global__ __launch_bounds__(256) void dec_small_kernel(const float* __restrict_
 // through two LDS buffers by buffer_load ... lds. A chunk's results wait in registers (packed to
 // bf16) and are stored after the next chunk's loads have landed, so the stores drain during that
 // chunk's products instead of under the wait for its loads (the wait is vmcnt(0): loads and stores
-// are not counted in order with each other). Two workgroups per CU overlap each other's waits. Wt is the A operand
-// of v_mfma_f32_16x16x32_bf16 with its rows permuted: operand row m = 4 g + e of block b is
-// column 16 g + 4 b + e of the chunk, so a lane's 16 results of one token are 16 consecutive
-// columns. Each wave passes its 32 x 64 results through 4 KB of LDS so that every store
-// instruction writes 8 whole 128-byte row pieces (16-byte pieces spread over 16 rows per
-// instruction took 60% longer). Staged Wt row R keeps its 16-byte chunk c at c ^ ex_swz(R), which
+// are not counted in order with each other). Two workgroups per CU overlap each other's waits.
+// Wt is the A operand of v_mfma_f32_16x16x32_bf16 with its rows permuted: operand row m = 4 g + e
+// of block b is column 16 g + 4 b + e of the chunk, so a lane's 16 results of one token are 16
+// consecutive columns. Each wave passes its 32 x 64 results through 4 KB of LDS so that every
+// store instruction writes 8 whole 128-byte row pieces (16-byte pieces spread over 16 rows per
+// instruction: 8% slower). Staged Wt row R keeps its 16-byte chunk c at c ^ ex_swz(R), which
 // spreads the 16 rows read by one group of lanes over distinct banks; the output staging keeps
 // piece p of row r at p ^ (r % 8).
 constexpr int kExT = 128;  // tokens per band: four waves of 32
